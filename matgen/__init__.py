@@ -1,0 +1,35 @@
+"""Seeded synthetic sparse matrices shaped like the paper's SpGEMM workloads.
+
+This package only produces inputs. It holds none of the product's
+arithmetic, so both the CPU oracle and the GPU library can be fed from it
+without sharing any code with each other.
+"""
+from .csr import CSR
+from .generators import (
+    CONFIGS,
+    config,
+    er,
+    er_rect,
+    laplacian2d,
+    rmat,
+    arrowhead,
+    identity,
+    permutation,
+    diagonal,
+    random_sparse,
+)
+
+__all__ = [
+    "CSR",
+    "CONFIGS",
+    "config",
+    "er",
+    "er_rect",
+    "laplacian2d",
+    "rmat",
+    "arrowhead",
+    "identity",
+    "permutation",
+    "diagonal",
+    "random_sparse",
+]
