@@ -1,0 +1,170 @@
+/*
+ * wingspan.h -- C ABI of the MI355X (gfx950) sparse-times-sparse matrix
+ * multiply C = A * B with CSR inputs and a CSR output (SpGEMM).
+ *
+ * The operation is the one the WingSpan paper benchmarks in Section 5.1
+ * ("the matrix product C = A*B where A, B and C are all sparse"), computed
+ * row by row with Gustavson's algorithm (Section 5.1, the four SpGEMM
+ * programs figure: for each output fiber, accumulate a * b into a workspace,
+ * then copy the workspace into the output fiber in coordinate order).
+ *
+ * C[i,j] = sum over stored entries A[i,k], B[k,j] of A[i,k] * B[k,j].
+ * The pattern of C is structural: (i, j) is stored whenever at least one
+ * product A[i,k]*B[k,j] is formed, even if the sum is exactly zero. Columns of
+ * every output row are strictly increasing.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers named *_dev, and the pointers inside wingspan_csr, are HIP device
+ *    pointers on the current device. Other pointers are host pointers.
+ *  - The caller owns all memory. The library never allocates device memory:
+ *    scratch space comes from the caller's workspace, sized by
+ *    wingspan_spgemm_workspace_size(). The workspace is scratch only; its
+ *    contents need not survive between calls.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream).
+ *  - Every function returns a wingspan_status and never aborts or prints.
+ *    Argument checks run on the host before any HIP call. On failure,
+ *    wingspan_last_error() returns a message (thread-local).
+ *  - Inputs must be canonical CSR: row_ptr[0] = 0, non-decreasing,
+ *    row_ptr[nrows] = nnz; columns in [0, ncols), strictly increasing within
+ *    each row. Non-canonical input is undefined behaviour unless
+ *    options->validate is set, in which case it is detected on the device and
+ *    reported as WINGSPAN_ERR_INVALID_MATRIX.
+ *  - A and B may alias (C = A * A). A, B and C share one value type.
+ *  - Calls on different streams with different workspaces are independent.
+ */
+#ifndef WINGSPAN_H
+#define WINGSPAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WINGSPAN_ABI_VERSION 1
+
+typedef enum { WINGSPAN_F32 = 0, WINGSPAN_F64 = 1 } wingspan_dtype;
+
+typedef enum {
+    WINGSPAN_OK = 0,
+    WINGSPAN_ERR_INVALID_ARGUMENT = 1,    /* null pointer, negative size, bad dtype/options */
+    WINGSPAN_ERR_DIMENSION_MISMATCH = 2,  /* A.ncols != B.nrows */
+    WINGSPAN_ERR_INDEX_OVERFLOW = 3,      /* a size does not fit the int32 index types */
+    WINGSPAN_ERR_WORKSPACE_TOO_SMALL = 4, /* workspace_bytes < wingspan_spgemm_workspace_size() */
+    WINGSPAN_ERR_INSUFFICIENT_CAPACITY = 5, /* nnz(C) > c_capacity (wingspan_spgemm only) */
+    WINGSPAN_ERR_INVALID_MATRIX = 6,      /* non-canonical input detected (options->validate) */
+    WINGSPAN_ERR_HIP = 7,                 /* a HIP runtime call failed; message has the HIP error */
+    WINGSPAN_ERR_UNSUPPORTED = 8,         /* a row is too long for the global spill pool */
+    WINGSPAN_ERR_INCONSISTENT = 9         /* numeric found a row whose entry count differs from
+                                             C.row_ptr (only reported when options->validate) */
+} wingspan_status;
+
+/* A CSR matrix on the device. row_ptr has nrows+1 int32 entries, col_idx and
+ * val have nnz entries; val holds float or double per the call's dtype. */
+typedef struct {
+    int64_t nrows;
+    int64_t ncols;
+    int64_t nnz;
+    const int32_t *row_ptr;
+    const int32_t *col_idx;
+    const void *val;
+} wingspan_csr;
+
+/* Optional tuning and test switches. Pass NULL for defaults, or zero-fill the
+ * struct and set version = WINGSPAN_ABI_VERSION; zero fields mean "default". */
+typedef struct {
+    uint32_t version;       /* must be WINGSPAN_ABI_VERSION */
+    int32_t validate;       /* 1: check A and B are canonical (and, in numeric, that
+                               C.row_ptr matches the product) on the device */
+    int32_t max_lds_slots;  /* cap on LDS hash-table slots per row (power of two,
+                               64..16384); longer rows use the dense or spill tier */
+    int32_t force_spill;    /* 1: every row above the register tier uses the global
+                               hash spill tier */
+    int32_t window_cols;    /* dense-window width in columns: 1024, 4096 or 16384 */
+    int32_t tiny_max;       /* largest per-row product count handled by the
+                               register-sort tier (8..64); -1 disables that tier */
+    int32_t dense_min_nnz;  /* numeric: rows with at least this many output entries use
+                               the dense-window tier even if they fit an LDS hash table;
+                               -1 disables the dense tier */
+    int32_t timing;         /* 1: time each tier's kernels with HIP events on `stream`
+                               (the call then synchronizes the stream before returning) */
+} wingspan_options;
+
+/* Tiers a row can be assigned to. */
+enum {
+    WINGSPAN_TIER_TINY = 0,   /* one wave segment per row, register bitonic sort */
+    WINGSPAN_TIER_HASH = 1,   /* one workgroup per row, LDS hash table + LDS sort */
+    WINGSPAN_TIER_DENSE = 2,  /* one workgroup per row, LDS bitmap (symbolic) or dense
+                                 LDS column windows (numeric) */
+    WINGSPAN_TIER_SPILL = 3,  /* persistent workgroups, global-memory hash + merge sort */
+    WINGSPAN_NUM_TIERS = 4
+};
+
+/* What the last symbolic (phase 0) or numeric (phase 1) call on this thread
+ * did. Products are the scalar multiplies A[i,k]*B[k,j]; kernel_ms is only
+ * filled when options->timing was set. */
+typedef struct {
+    int64_t rows[WINGSPAN_NUM_TIERS];
+    int64_t a_nnz[WINGSPAN_NUM_TIERS];
+    int64_t products[WINGSPAN_NUM_TIERS];
+    int64_t c_nnz[WINGSPAN_NUM_TIERS];   /* numeric phase only */
+    int32_t launches[WINGSPAN_NUM_TIERS];
+    float kernel_ms[WINGSPAN_NUM_TIERS];
+    float analysis_ms;                   /* product counting, binning, scans */
+    int64_t total_products;
+    int64_t c_nnz_total;
+} wingspan_phase_stats;
+
+/* Bytes of device workspace the calls below need for this A, B and options.
+ * Depends only on the sizes, never on the data; pure host code. */
+wingspan_status wingspan_spgemm_workspace_size(const wingspan_csr *A, const wingspan_csr *B,
+                                               wingspan_dtype dtype,
+                                               const wingspan_options *options,
+                                               size_t *bytes);
+
+/* Symbolic phase: the number of entries of every row of C, as the exclusive
+ * prefix sum c_row_ptr_dev[0..A.nrows] (int64, written by the library), and
+ * the total *c_nnz (host). Synchronizes `stream` twice (once to size its
+ * kernel launches, once to return *c_nnz); these are its only blocking
+ * points. A.val and B.val are not read. */
+wingspan_status wingspan_spgemm_symbolic(const wingspan_csr *A, const wingspan_csr *B,
+                                         int64_t *c_row_ptr_dev, int64_t *c_nnz,
+                                         void *workspace_dev, size_t workspace_bytes,
+                                         void *stream, const wingspan_options *options);
+
+/* Numeric phase: fills c_col_idx_dev (int32) and c_val_dev (dtype) for the
+ * structure c_row_ptr_dev produced by the symbolic phase for the same A and B
+ * patterns. Depends only on c_row_ptr_dev, so it can be re-run when the
+ * values of A or B change. Synchronizes `stream` once (to size its kernel
+ * launches); the output kernels run asynchronously. Writes never leave a
+ * row's range [c_row_ptr[i], c_row_ptr[i+1]). */
+wingspan_status wingspan_spgemm_numeric(const wingspan_csr *A, const wingspan_csr *B,
+                                        wingspan_dtype dtype, const int64_t *c_row_ptr_dev,
+                                        int32_t *c_col_idx_dev, void *c_val_dev,
+                                        void *workspace_dev, size_t workspace_bytes,
+                                        void *stream, const wingspan_options *options);
+
+/* Both phases. If nnz(C) exceeds c_capacity, returns
+ * WINGSPAN_ERR_INSUFFICIENT_CAPACITY with c_row_ptr_dev and *c_nnz valid, so
+ * the caller can allocate and call wingspan_spgemm_numeric. */
+wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                int64_t c_capacity, int64_t *c_nnz,
+                                void *workspace_dev, size_t workspace_bytes,
+                                void *stream, const wingspan_options *options);
+
+/* Statistics of the last call on this thread: phase 0 = symbolic, 1 = numeric. */
+wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out);
+
+/* Message for the last non-OK status on this thread ("" if none). */
+const char *wingspan_last_error(void);
+
+int wingspan_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINGSPAN_H */

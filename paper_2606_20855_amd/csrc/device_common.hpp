@@ -1,0 +1,188 @@
+// Wave-level building blocks shared by the SpGEMM kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wsp {
+
+constexpr int kWave = 64;
+constexpr int32_t kEmptyKey = -1;          // free hash slot
+constexpr int32_t kPadKey = 0x7fffffff;    // sorts after every real column
+
+// Control block bins. Rows are grouped by bin; each bin maps to one kernel
+// shape. Dense and spill rows are split into classes by log2(products) with
+// the heaviest class first, so launching a tier's bins in order hands out the
+// longest rows first.
+constexpr int kBinEmpty = 0;
+constexpr int kBinTiny0 = 1;      // 1..4: segment widths 8, 16, 32, 64
+constexpr int kNumTiny = 4;
+constexpr int kBinHash0 = 5;      // 5..13: table sizes 2^6 .. 2^14
+constexpr int kHashLog2Min = 6;
+constexpr int kHashLog2Max = 14;
+constexpr int kNumHash = kHashLog2Max - kHashLog2Min + 1;
+constexpr int kNumClasses = 16;
+constexpr int kBinDense0 = kBinHash0 + kNumHash;       // 14..29
+constexpr int kBinSpill0 = kBinDense0 + kNumClasses;   // 30..45
+constexpr int kNumBins = kBinSpill0 + kNumClasses;     // 46
+constexpr int kMaxBins = 64;
+
+enum : int32_t {
+    kErrProbeExhausted = 1,   // a hash table filled up (structure larger than C.row_ptr says)
+    kErrRowMismatch = 2,      // a row produced a different entry count than C.row_ptr
+    kErrInvalidMatrix = 4,    // validation found a non-canonical input
+};
+
+// Device-side control block, zeroed at the start of each phase and copied to
+// the host once the rows have been binned.
+struct Control {
+    int64_t total_products;
+    int64_t spill_max_bound;
+    int64_t c_nnz;
+    int32_t spill_next;
+    int32_t error_flags;
+    int32_t bin_count[kMaxBins];
+    int32_t bin_offset[kMaxBins];
+    int32_t bin_cursor[kMaxBins];
+    int64_t stat_products[kMaxBins];
+    int64_t stat_annz[kMaxBins];
+    int64_t stat_cnnz[kMaxBins];
+};
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ double to_d(float x) { return static_cast<double>(x); }
+__device__ __forceinline__ double to_d(double x) { return x; }
+
+// Inclusive prefix sum within aligned groups of W lanes (W a power of two).
+template <int W>
+__device__ __forceinline__ int group_incl_scan(int x) {
+    const int gl = lane_id() & (W - 1);
+#pragma unroll
+    for (int o = 1; o < W; o <<= 1) {
+        const int y = __shfl_up(x, o, W);
+        if (gl >= o) x += y;
+    }
+    return x;
+}
+
+// Within a group of W lanes holding a non-decreasing `incl`, the number of
+// lanes whose value is <= q. With incl the inclusive prefix of per-lane
+// lengths and q < incl[W-1], this is the lane that owns element q.
+template <int W>
+__device__ __forceinline__ int group_count_le(int incl, int q) {
+    int c = 0;
+#pragma unroll
+    for (int step = W / 2; step >= 1; step >>= 1) {
+        const int v = __shfl(incl, c + step - 1, W);
+        if (v <= q) c += step;
+    }
+    return c;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, kWave);
+    return x;
+}
+
+// Block-wide sum; every thread gets the result. `scratch` holds BLOCK/64 T.
+template <int BLOCK, typename T>
+__device__ __forceinline__ T block_sum(T x, T *scratch) {
+    constexpr int NW = BLOCK / kWave;
+    x = wave_sum(x);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) scratch[w] = x;
+    __syncthreads();
+    T t = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) t += scratch[i];
+    __syncthreads();
+    return t;
+}
+
+// Block-wide exclusive prefix sum of int; returns the exclusive value and the
+// block total. `scratch` holds BLOCK/64 ints.
+template <int BLOCK>
+__device__ __forceinline__ int block_excl_scan(int x, int *total, int *scratch) {
+    constexpr int NW = BLOCK / kWave;
+    const int incl = group_incl_scan<kWave>(x);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) scratch[w] = incl;
+    __syncthreads();
+    int before = 0, t = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        const int s = scratch[i];
+        before += (i < w) ? s : 0;
+        t += s;
+    }
+    __syncthreads();
+    *total = t;
+    return before + incl - x;
+}
+
+// Multiplicative (Fibonacci) hashing: the top `log2t` bits of key * 2^32/phi.
+__device__ __forceinline__ uint32_t hash_slot(int32_t key, int log2t) {
+    return (static_cast<uint32_t>(key) * 2654435761u) >> (32 - log2t);
+}
+
+__host__ __device__ __forceinline__ int ceil_log2(int64_t x) {
+    int l = 0;
+    while ((int64_t(1) << l) < x) ++l;
+    return l;
+}
+
+// Visit every product a * b of a set of A entries [a_lo, a_hi) of one row.
+// `range(k)` gives the slice [x, y) of B's entry arrays that multiplies A
+// entry k (a whole row of B, or its part inside a column window).
+//
+// The calling wave reads 64 A entries at a time, forms the prefix sum of their
+// slice lengths, and walks the flattened list of their products 64 at a time:
+// lane l of product block t handles product t*64 + l, locating its A entry by
+// binary search over the prefix sums held in the wave's lanes. Consecutive
+// lanes therefore read consecutive B entries whenever a slice is long, and no
+// lane idles on short slices. A workgroup of `nwaves` waves splits each chunk's
+// product blocks round-robin (wave `wave_rank` takes blocks rank, rank+nwaves,
+// ...), so every row is balanced across its waves whatever its B-row lengths.
+template <typename V, bool VALUES, typename RangeF, typename Visit>
+__device__ __forceinline__ void for_each_product(const int32_t *__restrict__ a_col,
+                                                 const V *__restrict__ a_val, int a_lo, int a_hi,
+                                                 RangeF range, const int32_t *__restrict__ b_col,
+                                                 const V *__restrict__ b_val, int wave_rank,
+                                                 int nwaves, Visit visit) {
+    const int ln = lane_id();
+    for (int a0 = a_lo; a0 < a_hi; a0 += kWave) {
+        const int a = a0 + ln;
+        int bs = 0, len = 0;
+        double av = 0.0;
+        if (a < a_hi) {
+            const int2 r = range(a_col[a]);
+            bs = r.x;
+            len = r.y - r.x;
+            if (VALUES) av = to_d(a_val[a]);
+        }
+        const int incl = group_incl_scan<kWave>(len);
+        const int tot = __shfl(incl, kWave - 1, kWave);
+        const int excl = incl - len;
+        for (int p0 = wave_rank * kWave; p0 < tot; p0 += nwaves * kWave) {
+            const int p = p0 + ln;
+            const int q = p < tot ? p : tot - 1;
+            const int o = group_count_le<kWave>(incl, q);
+            const int bs_o = __shfl(bs, o, kWave);
+            const int ex_o = __shfl(excl, o, kWave);
+            double av_o = 0.0;
+            if (VALUES) av_o = __shfl(av, o, kWave);
+            if (p < tot) {
+                const int b = bs_o + (q - ex_o);
+                const int col = b_col[b];
+                double prod = 0.0;
+                if (VALUES) prod = av_o * to_d(b_val[b]);
+                visit(col, prod);
+            }
+        }
+    }
+}
+
+}  // namespace wsp

@@ -1,0 +1,578 @@
+// The four row tiers of the symbolic and numeric phases.
+//
+// Every tier computes, for each of its rows i, the Gustavson accumulation of
+// the paper's SpGEMM program (Section 5.1): w[j] += A[i,k] * B[k,j] over the
+// entries of row i of A and of row k of B, then copies w into row i of C in
+// increasing column order. Products are formed in double and accumulated in
+// double for both value types; float outputs are rounded once when written.
+// The tiers differ only in where the workspace w lives:
+//   tiny  - in registers of one wave segment (products sorted, then reduced)
+//   hash  - an LDS open-addressing hash table per row
+//   dense - an LDS bitmap over all columns (symbolic) or a dense LDS window of
+//           columns swept across the row (numeric)
+//   spill - a global-memory hash table from a bounded pool (long rows)
+// Rows are independent: each row of C is written only by the threads that own
+// it, so no synchronization crosses rows.
+#pragma once
+
+#include "device_common.hpp"
+
+namespace wsp {
+
+struct BRowRange {
+    const int32_t *b_rp;
+    __device__ __forceinline__ int2 operator()(int32_t k) const {
+        return make_int2(b_rp[k], b_rp[k + 1]);
+    }
+};
+
+// Slice of B row k inside column window w, from the window table.
+struct BWindowRange {
+    const int32_t *wtab;
+    int64_t stride;
+    int w;
+    __device__ __forceinline__ int2 operator()(int32_t k) const {
+        const int32_t *t = wtab + static_cast<int64_t>(k) * stride + w;
+        return make_int2(t[0], t[1]);
+    }
+};
+
+template <typename V>
+struct Mats {
+    const int32_t *a_rp, *a_col;
+    const V *a_val;
+    const int32_t *b_rp, *b_col;
+    const V *b_val;
+};
+
+// ---------------------------------------------------------------------------
+// Tiny tier: rows with at most S products, one aligned segment of S lanes per
+// row. Lane l of the segment fetches product l into registers; the segment
+// bitonic-sorts (column, product) pairs with lane shuffles, sums runs of equal
+// columns with a segmented scan, and the last lane of each run emits.
+// ---------------------------------------------------------------------------
+template <int S, typename V, bool NUM>
+__global__ void __launch_bounds__(256) tiny_kernel(Mats<V> M, const int32_t *__restrict__ rows,
+                                                   int32_t nrows, int32_t *__restrict__ row_nnz,
+                                                   const int64_t *__restrict__ c_rp,
+                                                   int32_t *__restrict__ c_col, V *__restrict__ c_val,
+                                                   Control *ctrl) {
+    constexpr int G = 256 / S;
+    const int ln = lane_id();
+    const int sl = ln & (S - 1);
+    const int gidx = blockIdx.x * G + static_cast<int>(threadIdx.x) / S;
+    if (gidx >= nrows) return;   // whole segment leaves together
+    const int row = rows[gidx];
+    const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
+
+    int key = kPadKey;
+    double val = 0.0;
+    int base = 0;
+    for (int a0 = a_lo; a0 < a_hi; a0 += S) {
+        const int a = a0 + sl;
+        int bs = 0, len = 0;
+        double av = 0.0;
+        if (a < a_hi) {
+            const int32_t k = M.a_col[a];
+            bs = M.b_rp[k];
+            len = M.b_rp[k + 1] - bs;
+            if (NUM) av = to_d(M.a_val[a]);
+        }
+        const int incl = group_incl_scan<S>(len);
+        const int tot = __shfl(incl, S - 1, S);
+        if (tot > 0) {
+            const int p = sl - base;
+            const int q = p < 0 ? 0 : (p < tot ? p : tot - 1);
+            const int o = group_count_le<S>(incl, q);
+            const int bs_o = __shfl(bs, o, S);
+            const int ex_o = __shfl(incl - len, o, S);
+            double av_o = 0.0;
+            if (NUM) av_o = __shfl(av, o, S);
+            if (p >= 0 && p < tot) {
+                const int b = bs_o + (q - ex_o);
+                key = M.b_col[b];
+                if (NUM) val = av_o * to_d(M.b_val[b]);
+            }
+            base += tot;
+        }
+    }
+
+    // bitonic sort of the segment by column
+#pragma unroll
+    for (int k = 2; k <= S; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const int ok = __shfl_xor(key, j, S);
+            double ov = 0.0;
+            if (NUM) ov = __shfl_xor(val, j, S);
+            const bool up = (sl & k) == 0;
+            const bool lower = (sl & j) == 0;
+            const bool take = (lower == up) ? (ok < key) : (ok > key);
+            if (take) {
+                key = ok;
+                if (NUM) val = ov;
+            }
+        }
+    }
+
+    const int prv = __shfl_up(key, 1, S);
+    const int nxt = __shfl_down(key, 1, S);
+    if (NUM) {
+        // segmented inclusive sum over runs of equal keys
+        int start = (sl == 0 || prv != key) ? sl : 0;
+#pragma unroll
+        for (int o = 1; o < S; o <<= 1) {
+            const int y = __shfl_up(start, o, S);
+            if (sl >= o) start = start > y ? start : y;
+        }
+#pragma unroll
+        for (int o = 1; o < S; o <<= 1) {
+            const double y = __shfl_up(val, o, S);
+            if (sl - o >= start) val += y;
+        }
+    }
+    const bool tail = key != kPadKey && (sl == S - 1 || nxt != key);
+    const uint64_t bal = __ballot(tail);
+    const int gbase = ln & ~(S - 1);
+    const uint64_t gmask = (S == 64) ? ~0ull : (((1ull << S) - 1ull) << gbase);
+    const uint64_t mine = bal & gmask;
+    const int count = __popcll(mine);
+    if (!NUM) {
+        if (sl == 0) row_nnz[row] = count;
+        return;
+    }
+    const int rank = __popcll(mine & ((1ull << ln) - 1ull));
+    const int64_t cb = c_rp[row];
+    const int64_t seg = c_rp[row + 1] - cb;
+    if (sl == 0 && count != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    if (tail && rank < seg) {
+        c_col[cb + rank] = key;
+        c_val[cb + rank] = static_cast<V>(val);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Hash tier: one workgroup per row, an LDS table of 2^LOG2T slots.
+// Symbolic keeps keys only and counts first insertions. Numeric also adds the
+// product into the slot's double, then compacts the occupied slots, bitonic-
+// sorts them by column in LDS and writes the row.
+// ---------------------------------------------------------------------------
+template <int LOG2T, int BLOCK, typename V, bool NUM>
+__global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *__restrict__ rows,
+                                                     int32_t *__restrict__ row_nnz,
+                                                     const int64_t *__restrict__ c_rp,
+                                                     int32_t *__restrict__ c_col,
+                                                     V *__restrict__ c_val, Control *ctrl) {
+    constexpr int T = 1 << LOG2T;
+    constexpr int NW = BLOCK / kWave;
+    static_assert(T >= BLOCK, "table smaller than block");
+    __shared__ int32_t keys[T];
+    __shared__ double vals[NUM ? T : 1];
+    __shared__ int32_t scratch[NW];
+
+    const int row = rows[blockIdx.x];
+    for (int i = threadIdx.x; i < T; i += BLOCK) {
+        keys[i] = kEmptyKey;
+        if (NUM) vals[i] = 0.0;
+    }
+    __syncthreads();
+
+    const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
+    const int wv = threadIdx.x / kWave;
+    int inserted = 0;
+    bool overflow = false;
+    for_each_product<V, NUM>(
+        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
+        [&](int col, double prod) {
+            uint32_t h = hash_slot(col, LOG2T);
+            for (int probe = 0; probe < T; ++probe) {
+                const int cur = __hip_atomic_load(&keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                if (cur == col) {
+                    if (NUM) atomicAdd(&vals[h], prod);
+                    return;
+                }
+                if (cur == kEmptyKey) {
+                    const int old = atomicCAS(&keys[h], kEmptyKey, col);
+                    if (old == kEmptyKey || old == col) {
+                        inserted += (old == kEmptyKey);
+                        if (NUM) atomicAdd(&vals[h], prod);
+                        return;
+                    }
+                }
+                h = (h + 1) & (T - 1);
+            }
+            overflow = true;
+        });
+    if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
+
+    if (!NUM) {
+        const int total = block_sum<BLOCK>(inserted, scratch);
+        if (threadIdx.x == 0) row_nnz[row] = total;
+        return;
+    }
+    __syncthreads();
+
+    // compact occupied slots to the front of the table
+    constexpr int PER = T / BLOCK;
+    int kk[PER];
+    double vv[PER];
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int s = threadIdx.x + j * BLOCK;
+        kk[j] = keys[s];
+        vv[j] = vals[s];
+        cnt += kk[j] != kEmptyKey;
+    }
+    int total;
+    int pos = block_excl_scan<BLOCK>(cnt, &total, scratch);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        if (kk[j] != kEmptyKey) {
+            keys[pos] = kk[j];
+            vals[pos] = vv[j];
+            ++pos;
+        }
+    }
+    int n2 = 1;
+    while (n2 < total) n2 <<= 1;
+    for (int i = total + threadIdx.x; i < n2; i += BLOCK) keys[i] = kPadKey;
+    __syncthreads();
+
+    // bitonic sort of keys[0..n2) (values follow)
+    for (int k = 2; k <= n2; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < (n2 >> 1); i += BLOCK) {
+                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+                const int hi = lo + j;
+                const bool up = (lo & k) == 0;
+                const int kl = keys[lo], kh = keys[hi];
+                if ((kl > kh) == up) {
+                    keys[lo] = kh;
+                    keys[hi] = kl;
+                    const double t = vals[lo];
+                    vals[lo] = vals[hi];
+                    vals[hi] = t;
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    const int64_t cb = c_rp[row];
+    const int64_t seg = c_rp[row + 1] - cb;
+    if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    const int lim = static_cast<int64_t>(total) < seg ? total : static_cast<int>(seg);
+    for (int i = threadIdx.x; i < lim; i += BLOCK) {
+        c_col[cb + i] = keys[i];
+        c_val[cb + i] = static_cast<V>(vals[i]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Dense tier, symbolic: an LDS bitmap over all NWORDS*32 columns, one
+// workgroup per row. The row's entry count is the bitmap's population count.
+// ---------------------------------------------------------------------------
+template <int NWORDS, int BLOCK>
+__global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
+                                                           const int32_t *__restrict__ rows,
+                                                           int nwords_used,
+                                                           int32_t *__restrict__ row_nnz) {
+    constexpr int NW = BLOCK / kWave;
+    __shared__ uint32_t bm[NWORDS];
+    __shared__ int32_t scratch[NW];
+    const int row = rows[blockIdx.x];
+    for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
+    __syncthreads();
+    const int wv = threadIdx.x / kWave;
+    for_each_product<float, false>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1],
+                                   BRowRange{M.b_rp}, M.b_col, nullptr, wv, NW,
+                                   [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
+    __syncthreads();
+    int cnt = 0;
+    for (int i = threadIdx.x; i < nwords_used; i += BLOCK) cnt += __popc(bm[i]);
+    const int total = block_sum<BLOCK>(cnt, scratch);
+    if (threadIdx.x == 0) row_nnz[row] = total;
+}
+
+// ---------------------------------------------------------------------------
+// Dense tier, numeric: the row's columns are swept in windows of WV columns.
+// For each window the workgroup accumulates every product whose column falls
+// inside it into a dense LDS array of doubles (plus a presence bitmap), then
+// emits the window's entries in column order by scanning the bitmap: no hash
+// and no sort. Emission clears what it read, so the next window starts from
+// zero. The window table gives each B row's slice inside the window.
+// ---------------------------------------------------------------------------
+template <int WV, typename V>
+__global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_t *__restrict__ rows,
+                                                         const int32_t *__restrict__ wtab, int nwin,
+                                                         const int64_t *__restrict__ c_rp,
+                                                         int32_t *__restrict__ c_col,
+                                                         V *__restrict__ c_val, Control *ctrl) {
+    constexpr int BLOCK = 1024;
+    constexpr int NW = BLOCK / kWave;
+    constexpr int NWORDS = WV / 32;
+    constexpr int NCHUNK = WV / 64;
+    __shared__ double acc[WV];
+    __shared__ uint32_t bm[NWORDS];
+    __shared__ int32_t chunk_off[NCHUNK];
+    __shared__ int32_t win_total;
+
+    const int row = rows[blockIdx.x];
+    for (int i = threadIdx.x; i < WV; i += BLOCK) acc[i] = 0.0;
+    for (int i = threadIdx.x; i < NWORDS; i += BLOCK) bm[i] = 0u;
+    __syncthreads();
+
+    const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
+    const int64_t cb = c_rp[row];
+    const int64_t seg = c_rp[row + 1] - cb;
+    const int wv = threadIdx.x / kWave;
+    const int ln = lane_id();
+    int64_t out = 0;
+    for (int w = 0; w < nwin; ++w) {
+        const int w0 = w * WV;
+        for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi,
+                                  BWindowRange{wtab, static_cast<int64_t>(nwin) + 1, w}, M.b_col,
+                                  M.b_val, wv, NW, [&](int col, double prod) {
+                                      const int loc = col - w0;
+                                      atomicAdd(&acc[loc], prod);
+                                      atomicOr(&bm[loc >> 5], 1u << (loc & 31));
+                                  });
+        __syncthreads();
+        for (int c = threadIdx.x; c < NCHUNK; c += BLOCK)
+            chunk_off[c] = __popc(bm[2 * c]) + __popc(bm[2 * c + 1]);
+        __syncthreads();
+        if (wv == 0) {
+            int carry = 0;
+            for (int c0 = 0; c0 < NCHUNK; c0 += kWave) {
+                const int c = c0 + ln;
+                const int v = c < NCHUNK ? chunk_off[c] : 0;
+                const int inc = group_incl_scan<kWave>(v);
+                if (c < NCHUNK) chunk_off[c] = carry + inc - v;
+                carry += __shfl(inc, kWave - 1, kWave);
+            }
+            if (ln == 0) win_total = carry;
+        }
+        __syncthreads();
+        for (int c = wv; c < NCHUNK; c += NW) {
+            const int loc = c * kWave + ln;
+            const bool set = (bm[loc >> 5] >> (loc & 31)) & 1u;
+            const uint64_t bal = __ballot(set);
+            if (set) {
+                const int64_t pos = out + chunk_off[c] + __popcll(bal & ((1ull << ln) - 1ull));
+                if (pos < seg) {
+                    c_col[cb + pos] = w0 + loc;
+                    c_val[cb + pos] = static_cast<V>(acc[loc]);
+                }
+                acc[loc] = 0.0;
+            }
+        }
+        __syncthreads();
+        for (int i = threadIdx.x; i < NWORDS; i += BLOCK) bm[i] = 0u;
+        out += win_total;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0 && out != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+}
+
+// ---------------------------------------------------------------------------
+// Spill tier: persistent workgroups, each owning one slab of a bounded global
+// pool (keys then doubles, slab_cap slots each). A workgroup claims rows from
+// a shared counter (the dynamic schedule: whoever finishes takes the next
+// row), builds the row's hash table in its slab with global atomics, and in
+// the numeric phase compacts the table into the row of C and merge-sorts it
+// there, using the slab as the merge buffer.
+// ---------------------------------------------------------------------------
+constexpr int kSpillBlock = 512;
+constexpr int kRunLen = 2048;      // LDS-sorted run length
+constexpr int kMergeItems = 8;
+
+template <typename V>
+__device__ void merge_sort_segment(int32_t *__restrict__ col, V *__restrict__ val, int len,
+                                   int32_t *__restrict__ tcol, V *__restrict__ tval,
+                                   int32_t *s_keys, V *s_vals) {
+    constexpr int BLOCK = kSpillBlock;
+    // 1. sort runs of kRunLen in LDS
+    for (int r0 = 0; r0 < len; r0 += kRunLen) {
+        const int rl = (len - r0) < kRunLen ? (len - r0) : kRunLen;
+        int n2 = 1;
+        while (n2 < rl) n2 <<= 1;
+        for (int i = threadIdx.x; i < n2; i += BLOCK) {
+            if (i < rl) {
+                s_keys[i] = col[r0 + i];
+                s_vals[i] = val[r0 + i];
+            } else {
+                s_keys[i] = kPadKey;
+            }
+        }
+        __syncthreads();
+        for (int k = 2; k <= n2; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int i = threadIdx.x; i < (n2 >> 1); i += BLOCK) {
+                    const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+                    const int hi = lo + j;
+                    const bool up = (lo & k) == 0;
+                    const int kl = s_keys[lo], kh = s_keys[hi];
+                    if ((kl > kh) == up) {
+                        s_keys[lo] = kh;
+                        s_keys[hi] = kl;
+                        const V t = s_vals[lo];
+                        s_vals[lo] = s_vals[hi];
+                        s_vals[hi] = t;
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        for (int i = threadIdx.x; i < rl; i += BLOCK) {
+            col[r0 + i] = s_keys[i];
+            val[r0 + i] = s_vals[i];
+        }
+        __syncthreads();
+    }
+    // 2. merge runs pairwise, ping-ponging between the row and the slab
+    int32_t *sc = col, *dc = tcol;
+    V *sv = val, *dv = tval;
+    for (int w = kRunLen; w < len; w <<= 1) {
+        for (int p0 = 0; p0 < len; p0 += 2 * w) {
+            const int lsz = (len - p0) < w ? (len - p0) : w;
+            const int rsz = (len - p0 - lsz) < w ? (len - p0 - lsz) : w;
+            const int total = lsz + rsz;
+            const int32_t *L = sc + p0;
+            const int32_t *R = L + lsz;
+            for (int d0 = 0; d0 < total; d0 += BLOCK * kMergeItems) {
+                const int d = d0 + static_cast<int>(threadIdx.x) * kMergeItems;
+                if (d < total) {
+                    int lo = d - rsz > 0 ? d - rsz : 0;
+                    int hi = d < lsz ? d : lsz;
+                    while (lo < hi) {
+                        const int mid = (lo + hi) >> 1;
+                        if (L[mid] < R[d - 1 - mid]) lo = mid + 1;
+                        else hi = mid;
+                    }
+                    int i = lo, j = d - lo;
+                    for (int t = 0; t < kMergeItems && d + t < total; ++t) {
+                        const bool takeL = j >= rsz || (i < lsz && L[i] < R[j]);
+                        if (takeL) {
+                            dc[p0 + d + t] = L[i];
+                            dv[p0 + d + t] = sv[p0 + i];
+                            ++i;
+                        } else {
+                            dc[p0 + d + t] = R[j];
+                            dv[p0 + d + t] = sv[p0 + lsz + j];
+                            ++j;
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        int32_t *tc = sc; sc = dc; dc = tc;
+        V *tv = sv; sv = dv; dv = tv;
+    }
+    if (sc != col) {
+        for (int i = threadIdx.x; i < len; i += BLOCK) {
+            col[i] = sc[i];
+            val[i] = sv[i];
+        }
+        __syncthreads();
+    }
+}
+
+template <typename V, bool NUM>
+__global__ void __launch_bounds__(kSpillBlock) spill_kernel(
+    Mats<V> M, const int32_t *__restrict__ rows, int32_t nrows, const int64_t *__restrict__ pref,
+    int64_t ncols, char *__restrict__ pool, int64_t slab_cap, int32_t *__restrict__ row_nnz,
+    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val,
+    Control *ctrl) {
+    constexpr int BLOCK = kSpillBlock;
+    constexpr int NW = BLOCK / kWave;
+    __shared__ int32_t s_row;
+    __shared__ int32_t scratch[NW];
+    __shared__ int32_t s_keys[NUM ? kRunLen : 1];
+    __shared__ V s_vals[NUM ? kRunLen : 1];
+
+    int32_t *keys = reinterpret_cast<int32_t *>(pool + static_cast<int64_t>(blockIdx.x) * slab_cap * 12);
+    double *vals = reinterpret_cast<double *>(keys + slab_cap);
+    const int wv = threadIdx.x / kWave;
+
+    for (;;) {
+        if (threadIdx.x == 0) s_row = atomicAdd(&ctrl->spill_next, 1);
+        __syncthreads();
+        const int ri = s_row;
+        __syncthreads();
+        if (ri >= nrows) break;
+        const int row = rows[ri];
+        const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
+        int64_t bound;
+        if (NUM) {
+            bound = c_rp[row + 1] - c_rp[row];
+        } else {
+            const int64_t f = pref[a_hi] - pref[a_lo];
+            bound = f < ncols ? f : ncols;
+        }
+        int log2t = ceil_log2(2 * (bound > 0 ? bound : 1));
+        if (log2t < 6) log2t = 6;
+        const int64_t T = int64_t(1) << log2t;   // host guarantees T <= slab_cap
+        for (int64_t i = threadIdx.x; i < T; i += BLOCK) {
+            keys[i] = kEmptyKey;
+            if (NUM) vals[i] = 0.0;
+        }
+        __syncthreads();
+
+        int inserted = 0;
+        bool overflow = false;
+        for_each_product<V, NUM>(
+            M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
+            [&](int col, double prod) {
+                uint32_t h = hash_slot(col, log2t);
+                for (int64_t probe = 0; probe < T; ++probe) {
+                    const int old = atomicCAS(&keys[h], kEmptyKey, col);
+                    if (old == kEmptyKey || old == col) {
+                        inserted += (old == kEmptyKey);
+                        if (NUM) unsafeAtomicAdd(&vals[h], prod);
+                        return;
+                    }
+                    h = (h + 1) & static_cast<uint32_t>(T - 1);
+                }
+                overflow = true;
+            });
+        if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
+        if (!NUM) {
+            const int total = block_sum<BLOCK>(inserted, scratch);
+            if (threadIdx.x == 0) row_nnz[row] = total;
+            continue;
+        }
+        __syncthreads();
+
+        // compact the table into the row of C (slot order), then sort it
+        const int64_t cb = c_rp[row];
+        const int64_t seg = c_rp[row + 1] - cb;
+        int running = 0;
+        for (int64_t s0 = 0; s0 < T; s0 += BLOCK) {
+            const int64_t s = s0 + threadIdx.x;
+            int k = kEmptyKey;
+            double v = 0.0;
+            if (s < T) {
+                k = __hip_atomic_load(&keys[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (k != kEmptyKey) v = __hip_atomic_load(&vals[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            const int occ = k != kEmptyKey;
+            int tot;
+            const int ex = block_excl_scan<BLOCK>(occ, &tot, scratch);
+            if (occ && running + ex < seg) {
+                c_col[cb + running + ex] = k;
+                c_val[cb + running + ex] = static_cast<V>(v);
+            }
+            running += tot;
+        }
+        if (threadIdx.x == 0 && running != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+        __syncthreads();
+        const int len = static_cast<int64_t>(running) < seg ? running : static_cast<int>(seg);
+        merge_sort_segment<V>(c_col + cb, c_val + cb, len, keys, reinterpret_cast<V *>(vals),
+                              s_keys, s_vals);
+        __syncthreads();
+    }
+}
+
+}  // namespace wsp

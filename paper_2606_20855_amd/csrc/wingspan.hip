@@ -1,0 +1,682 @@
+// Host orchestration and C ABI of the gfx950 SpGEMM (see include/wingspan.h).
+//
+// Symbolic phase: count the products of every row of A (a scan over A's
+// entries of the lengths of the B rows they select), bin the rows by tier,
+// run each tier's symbolic kernel to get the entry count of every row of C,
+// and scan the counts into C.row_ptr.
+// Numeric phase: bin the rows again from C.row_ptr, then run each tier's
+// numeric kernel, which accumulates the row in its workspace and writes the
+// row's columns (sorted) and values.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/wingspan.h"
+#include "analysis.hpp"
+#include "device_common.hpp"
+#include "tiers.hpp"
+
+using namespace wsp;
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Limits and defaults.
+// ---------------------------------------------------------------------------
+constexpr int kHashLog2MaxSym = 14;           // 16K int32 keys = 64 KB of LDS
+constexpr int kHashLog2MaxNum = 13;           // 8K keys + 8K doubles = 96 KB of LDS
+constexpr int64_t kBitmapMaxCols = 38912 * 32; // 152 KB LDS bitmap
+constexpr int kMaxWindows = 128;              // dense numeric tier: windows per row
+constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
+constexpr int64_t kPoolBytes = int64_t(256) << 20;
+constexpr int64_t kMaxSlabCap = int64_t(1) << 27;
+constexpr int kMaxSlabs = 256;
+constexpr size_t kAlign = 256;
+
+thread_local std::string g_err;
+thread_local wingspan_phase_stats g_stats[2];
+
+wingspan_status fail(wingspan_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+#define HIP_TRY(call)                                                                     \
+    do {                                                                                  \
+        hipError_t e_ = (call);                                                           \
+        if (e_ != hipSuccess)                                                             \
+            return fail(WINGSPAN_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+
+#define LAUNCH_CHECK(what)                                                                 \
+    do {                                                                                   \
+        hipError_t e_ = hipGetLastError();                                                 \
+        if (e_ != hipSuccess)                                                              \
+            return fail(WINGSPAN_ERR_HIP, "launch of %s failed: %s", what, hipGetErrorString(e_)); \
+    } while (0)
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int64_t next_pow2(int64_t x) {
+    int64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+struct Opts {
+    bool validate = false;
+    bool force_spill = false;
+    bool timing = false;
+    bool dense_disabled = false;
+    int hash_log2_max_sym = kHashLog2MaxSym;
+    int hash_log2_max_num = kHashLog2MaxNum;
+    int wcols = kDefaultWindow;
+    int tiny_max = 64;
+    int64_t dense_min_nnz = INT64_MAX;
+};
+
+wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
+    Opts r;
+    if (o) {
+        if (o->version != WINGSPAN_ABI_VERSION)
+            return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "options->version is %u, expected %d", o->version,
+                        WINGSPAN_ABI_VERSION);
+        r.validate = o->validate != 0;
+        r.force_spill = o->force_spill != 0;
+        r.timing = o->timing != 0;
+        if (o->max_lds_slots != 0) {
+            const int32_t s = o->max_lds_slots;
+            if (s < 64 || s > (1 << 14) || (s & (s - 1)) != 0)
+                return fail(WINGSPAN_ERR_INVALID_ARGUMENT,
+                            "options->max_lds_slots must be a power of two in [64, 16384], got %d", s);
+            const int l = ceil_log2(s);
+            r.hash_log2_max_sym = std::min(r.hash_log2_max_sym, l);
+            r.hash_log2_max_num = std::min(r.hash_log2_max_num, l);
+        }
+        if (o->window_cols != 0) {
+            if (o->window_cols != 1024 && o->window_cols != 4096 && o->window_cols != 16384)
+                return fail(WINGSPAN_ERR_INVALID_ARGUMENT,
+                            "options->window_cols must be 1024, 4096 or 16384, got %d", o->window_cols);
+            r.wcols = o->window_cols;
+        }
+        if (o->tiny_max != 0) {
+            if (o->tiny_max == -1) r.tiny_max = 0;
+            else if (o->tiny_max < 8 || o->tiny_max > 64)
+                return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "options->tiny_max must be -1 or in [8, 64], got %d",
+                            o->tiny_max);
+            else r.tiny_max = o->tiny_max;
+        }
+        if (o->dense_min_nnz == -1) r.dense_disabled = true;
+        else if (o->dense_min_nnz < -1)
+            return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "options->dense_min_nnz must be >= -1");
+        else if (o->dense_min_nnz > 0) r.dense_min_nnz = o->dense_min_nnz;
+    }
+    *out = r;
+    return WINGSPAN_OK;
+}
+
+wingspan_status check_csr_desc(const wingspan_csr *M, const char *name) {
+    if (!M) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (M->nrows < 0 || M->ncols < 0 || M->nnz < 0)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "%s has a negative dimension or nnz", name);
+    if (M->nrows > INT32_MAX - 1 || M->ncols > INT32_MAX || M->nnz > INT32_MAX)
+        return fail(WINGSPAN_ERR_INDEX_OVERFLOW, "%s exceeds the int32 index range", name);
+    if (!M->row_ptr) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "%s->row_ptr is NULL", name);
+    if (M->nnz > 0 && (!M->col_idx || !M->val))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "%s has nnz > 0 but a NULL col_idx or val", name);
+    return WINGSPAN_OK;
+}
+
+wingspan_status check_pair(const wingspan_csr *A, const wingspan_csr *B) {
+    wingspan_status s = check_csr_desc(A, "A");
+    if (s != WINGSPAN_OK) return s;
+    s = check_csr_desc(B, "B");
+    if (s != WINGSPAN_OK) return s;
+    if (A->ncols != B->nrows)
+        return fail(WINGSPAN_ERR_DIMENSION_MISMATCH, "A.ncols (%lld) != B.nrows (%lld)",
+                    (long long)A->ncols, (long long)B->nrows);
+    return WINGSPAN_OK;
+}
+
+// Workspace layout, a pure function of the sizes and options.
+struct Layout {
+    size_t off_ctrl, off_pref, off_row_nnz, off_perm, off_partials, off_wtab, off_pool, total;
+    int nwin;          // numeric dense windows per row (0: dense numeric tier unavailable)
+    int64_t slab_cap;  // spill slab slots
+    int nslab;
+};
+
+Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
+    Layout L{};
+    const int64_t m = A->nrows, n = B->ncols, nnz_a = A->nnz;
+    size_t off = 0;
+    L.off_ctrl = off;
+    off += align_up(sizeof(Control));
+    L.off_pref = off;
+    off += align_up(sizeof(int64_t) * (nnz_a + 1));
+    L.off_row_nnz = off;
+    off += align_up(sizeof(int32_t) * std::max<int64_t>(m, 1));
+    L.off_perm = off;
+    off += align_up(sizeof(int32_t) * std::max<int64_t>(m, 1));
+    L.off_partials = off;
+    const int64_t tiles = (std::max<int64_t>(nnz_a, m + 1) + kScanTile - 1) / kScanTile + 2;
+    off += align_up(sizeof(int64_t) * tiles);
+    L.off_wtab = off;
+    const int64_t nwin = n > 0 ? (n + o.wcols - 1) / o.wcols : 1;
+    L.nwin = (!o.dense_disabled && nwin <= kMaxWindows) ? static_cast<int>(nwin) : 0;
+    if (L.nwin > 0) off += align_up(sizeof(int32_t) * B->nrows * (L.nwin + 1) + sizeof(int32_t));
+    L.off_pool = off;
+    L.slab_cap = std::min(kMaxSlabCap, std::max<int64_t>(64, next_pow2(2 * std::max<int64_t>(n, 1))));
+    const int64_t slab_bytes = L.slab_cap * 12;
+    L.nslab = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxSlabs, kPoolBytes / slab_bytes)));
+    off += align_up(static_cast<size_t>(slab_bytes) * L.nslab);
+    L.total = off;
+    return L;
+}
+
+// ---------------------------------------------------------------------------
+// Per-call context.
+// ---------------------------------------------------------------------------
+struct Ctx {
+    hipStream_t st;
+    Opts o;
+    Layout L;
+    char *ws;
+    Control *ctrl;
+    int64_t *pref;
+    int32_t *row_nnz;
+    int32_t *perm;
+    int64_t *partials;
+    int32_t *wtab;
+    char *pool;
+    Control host;
+};
+
+void carve(Ctx &c, void *ws) {
+    c.ws = static_cast<char *>(ws);
+    c.ctrl = reinterpret_cast<Control *>(c.ws + c.L.off_ctrl);
+    c.pref = reinterpret_cast<int64_t *>(c.ws + c.L.off_pref);
+    c.row_nnz = reinterpret_cast<int32_t *>(c.ws + c.L.off_row_nnz);
+    c.perm = reinterpret_cast<int32_t *>(c.ws + c.L.off_perm);
+    c.partials = reinterpret_cast<int64_t *>(c.ws + c.L.off_partials);
+    c.wtab = reinterpret_cast<int32_t *>(c.ws + c.L.off_wtab);
+    c.pool = c.ws + c.L.off_pool;
+}
+
+// HIP events for optional per-tier timing, created once per thread.
+struct Timer {
+    bool on = false;
+    hipEvent_t ev[2 * (WINGSPAN_NUM_TIERS + 1)] = {};
+    bool made = false;
+};
+thread_local Timer g_timer;
+
+wingspan_status timer_start(Ctx &c, int slot) {
+    if (!g_timer.on) return WINGSPAN_OK;
+    HIP_TRY(hipEventRecord(g_timer.ev[2 * slot], c.st));
+    return WINGSPAN_OK;
+}
+wingspan_status timer_stop(Ctx &c, int slot) {
+    if (!g_timer.on) return WINGSPAN_OK;
+    HIP_TRY(hipEventRecord(g_timer.ev[2 * slot + 1], c.st));
+    return WINGSPAN_OK;
+}
+
+wingspan_status timer_begin(bool on) {
+    g_timer.on = on;
+    if (on && !g_timer.made) {
+        for (auto &e : g_timer.ev) HIP_TRY(hipEventCreate(&e));
+        g_timer.made = true;
+    }
+    return WINGSPAN_OK;
+}
+
+constexpr int kSlotAnalysis = WINGSPAN_NUM_TIERS;
+
+template <typename In>
+wingspan_status run_scan(Ctx &c, In in, int64_t n, int64_t *out) {
+    const int64_t nb = std::max<int64_t>(1, (n + kScanTile - 1) / kScanTile);
+    scan_tile_sums<In><<<dim3(static_cast<unsigned>(nb)), kScanBlock, 0, c.st>>>(in, n, c.partials);
+    scan_partials<<<1, 1024, 0, c.st>>>(c.partials, nb);
+    scan_tiles<In><<<dim3(static_cast<unsigned>(nb)), kScanBlock, 0, c.st>>>(in, n, c.partials, nb, out);
+    LAUNCH_CHECK("scan");
+    return WINGSPAN_OK;
+}
+
+unsigned blocks_for(int64_t n, int per) { return static_cast<unsigned>((n + per - 1) / per); }
+
+// Product counts, optional validation, and binning. Ends with the control
+// block on the host.
+wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, bool numeric,
+                        const int64_t *c_rp, bool have_pref) {
+    wingspan_status s;
+    if ((s = timer_start(c, kSlotAnalysis)) != WINGSPAN_OK) return s;
+    const int64_t m = A->nrows;
+    const int64_t words = sizeof(Control) / sizeof(int32_t);
+    zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl), words);
+    LAUNCH_CHECK("zero_words");
+    if (c.o.validate) {
+        if (A->nrows > 0)
+            validate_csr<<<blocks_for(A->nrows * kWave, 256), 256, 0, c.st>>>(A->row_ptr, A->col_idx, A->nrows,
+                                                                             A->ncols, A->nnz, c.ctrl);
+        if (B->nrows > 0)
+            validate_csr<<<blocks_for(B->nrows * kWave, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows,
+                                                                             B->ncols, B->nnz, c.ctrl);
+        LAUNCH_CHECK("validate_csr");
+        // the product counts below index B.row_ptr through A.col_idx: stop
+        // here if the inputs are not canonical
+        HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
+        if (c.host.error_flags & kErrInvalidMatrix)
+            return fail(WINGSPAN_ERR_INVALID_MATRIX, "A or B is not canonical CSR");
+    }
+    if (!have_pref) {
+        s = run_scan(c, BRowLenIn{A->col_idx, B->row_ptr}, A->nnz, c.pref);
+        if (s != WINGSPAN_OK) return s;
+    }
+    BinCfg cfg{};
+    cfg.ncols = B->ncols;
+    cfg.numeric = numeric;
+    cfg.tiny_max = c.o.tiny_max;
+    cfg.force_spill = c.o.force_spill;
+    cfg.hash_log2_max = numeric ? c.o.hash_log2_max_num : c.o.hash_log2_max_sym;
+    cfg.dense_ok = numeric ? (c.L.nwin > 0) : (!c.o.dense_disabled && B->ncols <= kBitmapMaxCols);
+    cfg.dense_min_nnz = c.o.dense_min_nnz;
+    if (m > 0) {
+        bin_count<<<blocks_for(m, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, m, cfg, c.ctrl, c.row_nnz);
+        bin_offsets<<<1, 1, 0, c.st>>>(c.ctrl, c.pref, A->nnz);
+        bin_scatter<<<blocks_for(m, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, m, cfg, c.ctrl, c.perm);
+    } else {
+        bin_offsets<<<1, 1, 0, c.st>>>(c.ctrl, c.pref, A->nnz);
+    }
+    LAUNCH_CHECK("binning");
+    if ((s = timer_stop(c, kSlotAnalysis)) != WINGSPAN_OK) return s;
+    HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    const int64_t slab_limit = c.L.slab_cap / 2;
+    if (c.host.spill_max_bound > slab_limit)
+        return fail(WINGSPAN_ERR_UNSUPPORTED,
+                    "a row needs %lld hash slots but the spill pool's slabs hold %lld entries",
+                    (long long)c.host.spill_max_bound, (long long)slab_limit);
+    return WINGSPAN_OK;
+}
+
+int tier_of_bin(int b) {
+    if (b >= kBinTiny0 && b < kBinTiny0 + kNumTiny) return WINGSPAN_TIER_TINY;
+    if (b >= kBinHash0 && b < kBinHash0 + kNumHash) return WINGSPAN_TIER_HASH;
+    if (b >= kBinDense0 && b < kBinDense0 + kNumClasses) return WINGSPAN_TIER_DENSE;
+    if (b >= kBinSpill0 && b < kBinSpill0 + kNumClasses) return WINGSPAN_TIER_SPILL;
+    return -1;
+}
+
+void fill_stats(const Ctx &c, int phase) {
+    wingspan_phase_stats &st = g_stats[phase];
+    st = wingspan_phase_stats{};
+    for (int b = 0; b < kNumBins; ++b) {
+        const int t = tier_of_bin(b);
+        if (t < 0) continue;
+        st.rows[t] += c.host.bin_count[b];
+        st.a_nnz[t] += c.host.stat_annz[b];
+        st.products[t] += c.host.stat_products[b];
+        st.c_nnz[t] += c.host.stat_cnnz[b];
+    }
+    st.total_products = c.host.total_products;
+}
+
+// Contiguous range of perm covering bins [b0, b0+nb).
+void bin_range(const Ctx &c, int b0, int nb, int32_t *start, int32_t *count) {
+    *start = c.host.bin_offset[b0];
+    int32_t cnt = 0;
+    for (int b = b0; b < b0 + nb; ++b) cnt += c.host.bin_count[b];
+    *count = cnt;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel dispatch over compile-time shapes.
+// ---------------------------------------------------------------------------
+template <typename V, bool NUM>
+void launch_tiny(int s_idx, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
+                 int32_t cnt, int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val,
+                 Control *ctrl) {
+    switch (s_idx) {
+        case 0: tiny_kernel<8, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 1: tiny_kernel<16, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 2: tiny_kernel<32, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        default: tiny_kernel<64, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
+    }
+}
+
+template <int LOG2T, typename V, bool NUM>
+void launch_hash_t(unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows, int32_t *row_nnz,
+                   const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
+    constexpr int T = 1 << LOG2T;
+    constexpr int BLOCK = T <= 256 ? 64 : (T <= 512 ? 128 : (T <= 2048 ? 256 : (T <= 4096 ? 512 : 1024)));
+    hash_kernel<LOG2T, BLOCK, V, NUM><<<grid, BLOCK, 0, st>>>(M, rows, row_nnz, c_rp, c_col, c_val, ctrl);
+}
+
+template <typename V, bool NUM>
+void launch_hash(int log2t, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
+                 int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
+    switch (log2t) {
+        case 6: launch_hash_t<6, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 7: launch_hash_t<7, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 8: launch_hash_t<8, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 9: launch_hash_t<9, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 10: launch_hash_t<10, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 11: launch_hash_t<11, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 12: launch_hash_t<12, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 13: launch_hash_t<13, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        default:
+            if constexpr (!NUM) launch_hash_t<14, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl);
+            break;
+    }
+}
+
+void launch_bitmap(int64_t ncols, unsigned grid, hipStream_t st, const Mats<float> &M, const int32_t *rows,
+                   int32_t *row_nnz) {
+    const int nwords = static_cast<int>((ncols + 31) / 32);
+    if (nwords <= 2048) bitmap_sym_kernel<2048, 512><<<grid, 512, 0, st>>>(M, rows, nwords, row_nnz);
+    else if (nwords <= 8192) bitmap_sym_kernel<8192, 512><<<grid, 512, 0, st>>>(M, rows, nwords, row_nnz);
+    else if (nwords <= 16384) bitmap_sym_kernel<16384, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
+    else if (nwords <= 32768) bitmap_sym_kernel<32768, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
+    else bitmap_sym_kernel<38912, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
+}
+
+template <typename V>
+void launch_dense(int wcols, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
+                  const int32_t *wtab, int nwin, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
+    if (wcols == 1024) dense_num_kernel<1024, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, c_rp, c_col, c_val, ctrl);
+    else if (wcols == 4096) dense_num_kernel<4096, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, c_rp, c_col, c_val, ctrl);
+    else dense_num_kernel<16384, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, c_rp, c_col, c_val, ctrl);
+}
+
+// ---------------------------------------------------------------------------
+// Phases.
+// ---------------------------------------------------------------------------
+wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, int64_t *c_rp,
+                              int64_t *c_nnz) {
+    wingspan_status s = analyze(c, A, B, false, nullptr, false);
+    if (s != WINGSPAN_OK) return s;
+    fill_stats(c, 0);
+    wingspan_phase_stats &stats = g_stats[0];
+    const Mats<float> M{A->row_ptr, A->col_idx, static_cast<const float *>(A->val),
+                        B->row_ptr, B->col_idx, static_cast<const float *>(B->val)};
+    const int32_t *perm = c.perm;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+    for (int i = 0; i < kNumTiny; ++i) {
+        const int b = kBinTiny0 + i;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        const int S = 8 << i;
+        launch_tiny<float, false>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b],
+                                  cnt, c.row_nnz, nullptr, nullptr, nullptr, c.ctrl);
+        stats.launches[WINGSPAN_TIER_TINY]++;
+    }
+    LAUNCH_CHECK("tiny symbolic");
+    if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+    for (int i = 0; i < kNumHash; ++i) {
+        const int b = kBinHash0 + i;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        launch_hash<float, false>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M,
+                                  perm + c.host.bin_offset[b], c.row_nnz, nullptr, nullptr, nullptr, c.ctrl);
+        stats.launches[WINGSPAN_TIER_HASH]++;
+    }
+    LAUNCH_CHECK("hash symbolic");
+    if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+
+    int32_t start, cnt;
+    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+    bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
+    if (cnt) {
+        launch_bitmap(B->ncols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.row_nnz);
+        stats.launches[WINGSPAN_TIER_DENSE]++;
+        LAUNCH_CHECK("bitmap symbolic");
+    }
+    if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
+    bin_range(c, kBinSpill0, kNumClasses, &start, &cnt);
+    if (cnt) {
+        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
+        spill_kernel<float, false><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols,
+                                                                  c.pool, c.L.slab_cap, c.row_nnz, nullptr,
+                                                                  nullptr, nullptr, c.ctrl);
+        stats.launches[WINGSPAN_TIER_SPILL]++;
+        LAUNCH_CHECK("spill symbolic");
+    }
+    if ((s = timer_stop(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
+
+    s = run_scan(c, CountIn{c.row_nnz}, A->nrows, c_rp);
+    if (s != WINGSPAN_OK) return s;
+    int64_t total = 0;
+    HIP_TRY(hipMemcpyAsync(&total, c_rp + A->nrows, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    *c_nnz = total;
+    stats.c_nnz_total = total;
+    return WINGSPAN_OK;
+}
+
+template <typename V>
+wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, const int64_t *c_rp,
+                             int32_t *c_col, V *c_val, bool have_pref) {
+    wingspan_status s = analyze(c, A, B, true, c_rp, have_pref);
+    if (s != WINGSPAN_OK) return s;
+    fill_stats(c, 1);
+    wingspan_phase_stats &stats = g_stats[1];
+    int64_t c_entries = 0;
+    for (int b = 0; b < kNumBins; ++b) c_entries += c.host.stat_cnnz[b];
+    stats.c_nnz_total = c_entries;
+    if (c_entries > 0 && (!c_col || !c_val))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "C has %lld entries but c_col_idx_dev or c_val_dev is NULL",
+                    (long long)c_entries);
+    const Mats<V> M{A->row_ptr, A->col_idx, static_cast<const V *>(A->val),
+                    B->row_ptr, B->col_idx, static_cast<const V *>(B->val)};
+    const int32_t *perm = c.perm;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+    for (int i = 0; i < kNumTiny; ++i) {
+        const int b = kBinTiny0 + i;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        const int S = 8 << i;
+        launch_tiny<V, true>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b], cnt,
+                             nullptr, c_rp, c_col, c_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_TINY]++;
+    }
+    LAUNCH_CHECK("tiny numeric");
+    if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+    for (int i = 0; i < kNumHash; ++i) {
+        const int b = kBinHash0 + i;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        launch_hash<V, true>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M, perm + c.host.bin_offset[b],
+                             nullptr, c_rp, c_col, c_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_HASH]++;
+    }
+    LAUNCH_CHECK("hash numeric");
+    if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+
+    int32_t start, cnt;
+    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+    bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
+    if (cnt) {
+        const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
+        build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows, c.L.nwin,
+                                                                       c.o.wcols, c.wtab);
+        launch_dense<V>(c.o.wcols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.wtab, c.L.nwin, c_rp,
+                        c_col, c_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_DENSE]++;
+        LAUNCH_CHECK("dense numeric");
+    }
+    if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
+    bin_range(c, kBinSpill0, kNumClasses, &start, &cnt);
+    if (cnt) {
+        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
+        spill_kernel<V, true><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols, c.pool,
+                                                             c.L.slab_cap, nullptr, c_rp, c_col, c_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_SPILL]++;
+        LAUNCH_CHECK("spill numeric");
+    }
+    if ((s = timer_stop(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
+
+    if (c.o.validate) {
+        int32_t flags = 0;
+        HIP_TRY(hipMemcpyAsync(&flags, &c.ctrl->error_flags, sizeof(int32_t), hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
+        if (flags & (kErrRowMismatch | kErrProbeExhausted))
+            return fail(WINGSPAN_ERR_INCONSISTENT, "C.row_ptr does not match the structure of A*B (flags %d)",
+                        flags);
+    }
+    return WINGSPAN_OK;
+}
+
+wingspan_status finish_timing(int phase) {
+    if (!g_timer.on) return WINGSPAN_OK;
+    for (int slot = 0; slot <= WINGSPAN_NUM_TIERS; ++slot) {
+        HIP_TRY(hipEventSynchronize(g_timer.ev[2 * slot + 1]));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, g_timer.ev[2 * slot], g_timer.ev[2 * slot + 1]));
+        if (slot == kSlotAnalysis) g_stats[phase].analysis_ms = ms;
+        else g_stats[phase].kernel_ms[slot] = ms;
+    }
+    return WINGSPAN_OK;
+}
+
+wingspan_status setup(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, const wingspan_options *opt,
+                      void *ws, size_t ws_bytes, void *stream) {
+    wingspan_status s = parse_opts(opt, &c.o);
+    if (s != WINGSPAN_OK) return s;
+    c.L = plan(A, B, c.o);
+    if (ws_bytes < c.L.total)
+        return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", ws_bytes, c.L.total);
+    if (!ws) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kAlign);
+    c.st = static_cast<hipStream_t>(stream);
+    carve(c, ws);
+    return WINGSPAN_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+int wingspan_abi_version(void) { return WINGSPAN_ABI_VERSION; }
+
+const char *wingspan_last_error(void) { return g_err.c_str(); }
+
+wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out) {
+    if ((phase != 0 && phase != 1) || !out) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bad phase or NULL out");
+    *out = g_stats[phase];
+    return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_spgemm_workspace_size(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                               const wingspan_options *options, size_t *bytes) {
+    g_err.clear();
+    if (!bytes) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    wingspan_status s = check_pair(A, B);
+    if (s != WINGSPAN_OK) return s;
+    Opts o;
+    if ((s = parse_opts(options, &o)) != WINGSPAN_OK) return s;
+    *bytes = plan(A, B, o).total;
+    return WINGSPAN_OK;
+}
+
+static wingspan_status symbolic_entry(const wingspan_csr *A, const wingspan_csr *B, int64_t *c_row_ptr_dev,
+                                      int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes, void *stream,
+                                      const wingspan_options *options, Ctx &c) {
+    wingspan_status s = check_pair(A, B);
+    if (s != WINGSPAN_OK) return s;
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    if (!c_nnz) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_nnz is NULL");
+    if ((s = setup(c, A, B, options, workspace_dev, workspace_bytes, stream)) != WINGSPAN_OK) return s;
+    if ((s = timer_begin(c.o.timing)) != WINGSPAN_OK) return s;
+    if ((s = symbolic_impl(c, A, B, c_row_ptr_dev, c_nnz)) != WINGSPAN_OK) return s;
+    return finish_timing(0);
+}
+
+wingspan_status wingspan_spgemm_symbolic(const wingspan_csr *A, const wingspan_csr *B, int64_t *c_row_ptr_dev,
+                                         int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
+                                         void *stream, const wingspan_options *options) {
+    g_err.clear();
+    Ctx c{};
+    return symbolic_entry(A, B, c_row_ptr_dev, c_nnz, workspace_dev, workspace_bytes, stream, options, c);
+}
+
+static wingspan_status numeric_entry(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                     const int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                     void *workspace_dev, size_t workspace_bytes, void *stream,
+                                     const wingspan_options *options, bool have_pref, Ctx &c) {
+    wingspan_status s = check_pair(A, B);
+    if (s != WINGSPAN_OK) return s;
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    if (!have_pref && (s = setup(c, A, B, options, workspace_dev, workspace_bytes, stream)) != WINGSPAN_OK)
+        return s;
+    if ((s = timer_begin(c.o.timing)) != WINGSPAN_OK) return s;
+    if (dtype == WINGSPAN_F32)
+        s = numeric_impl<float>(c, A, B, c_row_ptr_dev, c_col_idx_dev, static_cast<float *>(c_val_dev), have_pref);
+    else
+        s = numeric_impl<double>(c, A, B, c_row_ptr_dev, c_col_idx_dev, static_cast<double *>(c_val_dev),
+                                 have_pref);
+    if (s != WINGSPAN_OK) return s;
+    return finish_timing(1);
+}
+
+wingspan_status wingspan_spgemm_numeric(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                        const int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream,
+                                        const wingspan_options *options) {
+    g_err.clear();
+    Ctx c{};
+    return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, workspace_dev, workspace_bytes,
+                         stream, options, false, c);
+}
+
+wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                int64_t c_capacity, int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
+                                void *stream, const wingspan_options *options) {
+    g_err.clear();
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (c_capacity < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_capacity is negative");
+    Ctx c{};
+    wingspan_status s =
+        symbolic_entry(A, B, c_row_ptr_dev, c_nnz, workspace_dev, workspace_bytes, stream, options, c);
+    if (s != WINGSPAN_OK) return s;
+    if (*c_nnz > c_capacity)
+        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "nnz(C) = %lld exceeds c_capacity = %lld",
+                    (long long)*c_nnz, (long long)c_capacity);
+    if (*c_nnz > 0 && (!c_col_idx_dev || !c_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_col_idx_dev or c_val_dev is NULL");
+    return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, workspace_dev, workspace_bytes,
+                         stream, options, true, c);
+}
+
+}  // extern "C"

@@ -1,0 +1,295 @@
+"""Python binding of the gfx950 SpGEMM C ABI (include/wingspan.h).
+
+The functions named ``wingspan_*`` mirror the C entry points one to one and
+only marshal arguments; all computation happens in libwingspan.so on the GPU.
+``spgemm()`` is a convenience wrapper that allocates the workspace and C with
+torch (device memory and streams only) and runs both phases.
+
+There is no fallback: if libwingspan.so is missing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libwingspan.so")
+
+ABI_VERSION = 1
+F32, F64 = 0, 1
+TIERS = ("tiny", "hash", "dense", "spill")
+
+STATUS = {
+    0: "WINGSPAN_OK",
+    1: "WINGSPAN_ERR_INVALID_ARGUMENT",
+    2: "WINGSPAN_ERR_DIMENSION_MISMATCH",
+    3: "WINGSPAN_ERR_INDEX_OVERFLOW",
+    4: "WINGSPAN_ERR_WORKSPACE_TOO_SMALL",
+    5: "WINGSPAN_ERR_INSUFFICIENT_CAPACITY",
+    6: "WINGSPAN_ERR_INVALID_MATRIX",
+    7: "WINGSPAN_ERR_HIP",
+    8: "WINGSPAN_ERR_UNSUPPORTED",
+    9: "WINGSPAN_ERR_INCONSISTENT",
+}
+STATUS_CODE = {v: k for k, v in STATUS.items()}
+
+
+class WingspanError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class wingspan_csr(ctypes.Structure):
+    _fields_ = [
+        ("nrows", ctypes.c_int64),
+        ("ncols", ctypes.c_int64),
+        ("nnz", ctypes.c_int64),
+        ("row_ptr", ctypes.c_void_p),
+        ("col_idx", ctypes.c_void_p),
+        ("val", ctypes.c_void_p),
+    ]
+
+
+class wingspan_options(ctypes.Structure):
+    _fields_ = [
+        ("version", ctypes.c_uint32),
+        ("validate", ctypes.c_int32),
+        ("max_lds_slots", ctypes.c_int32),
+        ("force_spill", ctypes.c_int32),
+        ("window_cols", ctypes.c_int32),
+        ("tiny_max", ctypes.c_int32),
+        ("dense_min_nnz", ctypes.c_int32),
+        ("timing", ctypes.c_int32),
+    ]
+
+
+_NT = 4
+
+
+class wingspan_phase_stats(ctypes.Structure):
+    _fields_ = [
+        ("rows", ctypes.c_int64 * _NT),
+        ("a_nnz", ctypes.c_int64 * _NT),
+        ("products", ctypes.c_int64 * _NT),
+        ("c_nnz", ctypes.c_int64 * _NT),
+        ("launches", ctypes.c_int32 * _NT),
+        ("kernel_ms", ctypes.c_float * _NT),
+        ("analysis_ms", ctypes.c_float),
+        ("total_products", ctypes.c_int64),
+        ("c_nnz_total", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libwingspan.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python __graft_entry__.py build` "
+                           "(or paper_2606_20855_amd._build.build())")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+    csr_p, opt_p = P(wingspan_csr), P(wingspan_options)
+    lib.wingspan_abi_version.argtypes = []
+    lib.wingspan_abi_version.restype = i32
+    lib.wingspan_last_error.argtypes = []
+    lib.wingspan_last_error.restype = ctypes.c_char_p
+    lib.wingspan_last_stats.argtypes = [i32, P(wingspan_phase_stats)]
+    lib.wingspan_last_stats.restype = i32
+    lib.wingspan_spgemm_workspace_size.argtypes = [csr_p, csr_p, i32, opt_p, P(sz)]
+    lib.wingspan_spgemm_workspace_size.restype = i32
+    lib.wingspan_spgemm_symbolic.argtypes = [csr_p, csr_p, vp, P(i64), vp, sz, vp, opt_p]
+    lib.wingspan_spgemm_symbolic.restype = i32
+    lib.wingspan_spgemm_numeric.argtypes = [csr_p, csr_p, i32, vp, vp, vp, vp, sz, vp, opt_p]
+    lib.wingspan_spgemm_numeric.restype = i32
+    lib.wingspan_spgemm.argtypes = [csr_p, csr_p, i32, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
+    lib.wingspan_spgemm.restype = i32
+    _lib = lib
+    return lib
+
+
+EXPORTED = (
+    "wingspan_abi_version",
+    "wingspan_last_error",
+    "wingspan_last_stats",
+    "wingspan_spgemm_workspace_size",
+    "wingspan_spgemm_symbolic",
+    "wingspan_spgemm_numeric",
+    "wingspan_spgemm",
+)
+
+
+def make_options(**kw) -> wingspan_options:
+    o = wingspan_options()
+    o.version = ABI_VERSION
+    for k, v in kw.items():
+        if not hasattr(o, k) or k == "version":
+            raise KeyError(k)
+        setattr(o, k, int(v))
+    return o
+
+
+def _opt_ptr(options):
+    if options is None:
+        return None
+    if isinstance(options, dict):
+        options = make_options(**options)
+    return ctypes.byref(options)
+
+
+def _check(status: int):
+    if status != 0:
+        raise WingspanError(status, load().wingspan_last_error().decode())
+
+
+def wingspan_abi_version() -> int:
+    return load().wingspan_abi_version()
+
+
+def wingspan_last_error() -> str:
+    return load().wingspan_last_error().decode()
+
+
+def wingspan_last_stats(phase: int) -> dict:
+    st = wingspan_phase_stats()
+    _check(load().wingspan_last_stats(phase, ctypes.byref(st)))
+    out = {name: {t: getattr(st, name)[i] for i, t in enumerate(TIERS)}
+           for name in ("rows", "a_nnz", "products", "c_nnz", "launches", "kernel_ms")}
+    out["analysis_ms"] = st.analysis_ms
+    out["total_products"] = st.total_products
+    out["c_nnz_total"] = st.c_nnz_total
+    return out
+
+
+def wingspan_spgemm_workspace_size(A: wingspan_csr, B: wingspan_csr, dtype: int, options=None) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().wingspan_spgemm_workspace_size(ctypes.byref(A), ctypes.byref(B), dtype, _opt_ptr(options),
+                                                 ctypes.byref(n)))
+    return n.value
+
+
+def wingspan_spgemm_symbolic(A: wingspan_csr, B: wingspan_csr, c_row_ptr: int, workspace: int,
+                             workspace_bytes: int, stream: int = 0, options=None) -> int:
+    nnz = ctypes.c_int64(0)
+    _check(load().wingspan_spgemm_symbolic(ctypes.byref(A), ctypes.byref(B), c_row_ptr, ctypes.byref(nnz),
+                                           workspace, workspace_bytes, stream or None, _opt_ptr(options)))
+    return nnz.value
+
+
+def wingspan_spgemm_numeric(A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int, c_col_idx: int,
+                            c_val: int, workspace: int, workspace_bytes: int, stream: int = 0,
+                            options=None) -> None:
+    _check(load().wingspan_spgemm_numeric(ctypes.byref(A), ctypes.byref(B), dtype, c_row_ptr, c_col_idx, c_val,
+                                          workspace, workspace_bytes, stream or None, _opt_ptr(options)))
+
+
+def wingspan_spgemm(A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int, c_col_idx: int, c_val: int,
+                    c_capacity: int, workspace: int, workspace_bytes: int, stream: int = 0,
+                    options=None) -> int:
+    nnz = ctypes.c_int64(0)
+    _check(load().wingspan_spgemm(ctypes.byref(A), ctypes.byref(B), dtype, c_row_ptr, c_col_idx, c_val,
+                                  c_capacity, ctypes.byref(nnz), workspace, workspace_bytes, stream or None,
+                                  _opt_ptr(options)))
+    return nnz.value
+
+
+# ---------------------------------------------------------------------------
+# torch-level convenience: device CSR handles, allocation, both phases.
+# ---------------------------------------------------------------------------
+
+@dataclass
+class DeviceCSR:
+    """CSR on the GPU, held in torch tensors. Inputs use int32 row_ptr; the
+    product C uses int64 row_ptr."""
+    nrows: int
+    ncols: int
+    row_ptr: "object"
+    col_idx: "object"
+    val: "object"
+
+    @property
+    def nnz(self) -> int:
+        return int(self.col_idx.numel())
+
+    @property
+    def dtype_code(self) -> int:
+        import torch
+        return F32 if self.val.dtype == torch.float32 else F64
+
+    def desc(self) -> wingspan_csr:
+        import torch
+        if self.row_ptr.dtype != torch.int32:
+            raise TypeError("input row_ptr must be int32")
+        d = wingspan_csr()
+        d.nrows, d.ncols, d.nnz = self.nrows, self.ncols, self.nnz
+        d.row_ptr = self.row_ptr.data_ptr()
+        d.col_idx = self.col_idx.data_ptr() if self.nnz else None
+        d.val = self.val.data_ptr() if self.nnz else None
+        return d
+
+    @classmethod
+    def from_host(cls, M, device="cuda") -> "DeviceCSR":
+        import torch
+        t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dtype=dt)).to(device)
+        return cls(int(M.nrows), int(M.ncols), t(M.row_ptr, np.int32), t(M.col_idx, np.int32),
+                   t(M.val, M.val.dtype))
+
+    def to_host(self):
+        return HostCSR(self.nrows, self.ncols, self.row_ptr.cpu().numpy(), self.col_idx.cpu().numpy(),
+                       self.val.cpu().numpy())
+
+
+@dataclass
+class HostCSR:
+    nrows: int
+    ncols: int
+    row_ptr: np.ndarray
+    col_idx: np.ndarray
+    val: np.ndarray
+
+
+def _stream_handle(stream) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def allocate_workspace(A: DeviceCSR, B: DeviceCSR, options=None):
+    import torch
+    nbytes = wingspan_spgemm_workspace_size(A.desc(), B.desc(), A.dtype_code, options)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=A.row_ptr.device)
+    if ws.data_ptr() % 256:
+        raise RuntimeError("torch returned a workspace that is not 256-byte aligned")
+    return ws, nbytes
+
+
+def spgemm(A: DeviceCSR, B: DeviceCSR, options=None, stream=None, workspace=None) -> DeviceCSR:
+    """C = A * B on the GPU: symbolic phase, allocate C, numeric phase."""
+    import torch
+    if A.val.dtype != B.val.dtype:
+        raise TypeError("A and B must share a value dtype")
+    dev = A.row_ptr.device
+    if workspace is None:
+        ws, nbytes = allocate_workspace(A, B, options)
+    else:
+        ws, nbytes = workspace, workspace.numel()
+    h = _stream_handle(stream)
+    Ad, Bd = A.desc(), B.desc()
+    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device=dev)
+    nnz = wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), ws.data_ptr(), nbytes, h, options)
+    c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(nnz, 1), dtype=A.val.dtype, device=dev)
+    wingspan_spgemm_numeric(Ad, Bd, A.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                            ws.data_ptr(), nbytes, h, options)
+    return DeviceCSR(A.nrows, B.ncols, c_rp, c_col[:nnz], c_val[:nnz])

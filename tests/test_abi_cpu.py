@@ -1,0 +1,156 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads and
+exports every function include/wingspan.h declares, the workspace size is a
+pure function of the sizes, and invalid arguments are rejected with the
+documented status codes before any HIP call is made."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_20855_amd import wingspan as ws
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wingspan.h")
+FAKE = 0x10000   # a non-null, 256-aligned address that is never dereferenced
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wingspan_\w+)\s*\(", text)))
+
+
+def desc(nrows, ncols, nnz, rp=FAKE, col=FAKE, val=FAKE):
+    d = ws.wingspan_csr()
+    d.nrows, d.ncols, d.nnz = nrows, ncols, nnz
+    d.row_ptr, d.col_idx, d.val = rp, col, val
+    return d
+
+
+def status_of(fn, *args, **kw):
+    with pytest.raises(ws.WingspanError) as e:
+        fn(*args, **kw)
+    return ws.STATUS[e.value.status], e.value.message
+
+
+def test_library_exports_every_header_function():
+    lib = ws.load()
+    declared = header_functions()
+    assert set(declared) == set(ws.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_abi_version():
+    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 1
+
+
+def test_struct_layouts_match_header():
+    # sizes the C side sees (x86-64 SysV)
+    assert ctypes.sizeof(ws.wingspan_csr) == 48
+    assert ctypes.sizeof(ws.wingspan_options) == 32
+    assert ctypes.sizeof(ws.wingspan_phase_stats) == 4 * 8 * 4 + 4 * 4 + 4 * 4 + 4 + 4 + 8 + 8
+
+
+def test_workspace_size_is_host_only_and_monotone():
+    small = ws.wingspan_spgemm_workspace_size(desc(1000, 1000, 10_000), desc(1000, 1000, 10_000), ws.F64)
+    big = ws.wingspan_spgemm_workspace_size(desc(100_000, 100_000, 1_000_000), desc(100_000, 100_000, 1_000_000),
+                                            ws.F64)
+    assert 0 < small < big
+    assert small % 256 == 0
+    # no dense tier -> smaller workspace
+    nodense = ws.wingspan_spgemm_workspace_size(desc(100_000, 100_000, 1_000_000),
+                                                desc(100_000, 100_000, 1_000_000), ws.F64,
+                                                ws.make_options(dense_min_nnz=-1))
+    assert nodense < big
+    # empty operands are fine
+    assert ws.wingspan_spgemm_workspace_size(desc(0, 0, 0), desc(0, 0, 0), ws.F32) > 0
+
+
+@pytest.mark.parametrize("A,B,code", [
+    (desc(10, 5, 3), desc(6, 4, 3), "WINGSPAN_ERR_DIMENSION_MISMATCH"),
+    (desc(-1, 5, 3), desc(5, 4, 3), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+    (desc(10, 5, -3), desc(5, 4, 3), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+    (desc(10, 5, 2**31), desc(5, 4, 3), "WINGSPAN_ERR_INDEX_OVERFLOW"),
+    (desc(2**31, 5, 3), desc(5, 4, 3), "WINGSPAN_ERR_INDEX_OVERFLOW"),
+    (desc(10, 5, 3), desc(5, 2**31, 3), "WINGSPAN_ERR_INDEX_OVERFLOW"),
+    (desc(10, 5, 3, rp=0), desc(5, 4, 3), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+    (desc(10, 5, 3, col=0), desc(5, 4, 3), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+    (desc(10, 5, 3), desc(5, 4, 3, val=0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+])
+def test_descriptor_errors(A, B, code):
+    got, msg = status_of(ws.wingspan_spgemm_workspace_size, A, B, ws.F64)
+    assert got == code and msg
+    got2, _ = status_of(ws.wingspan_spgemm_symbolic, A, B, FAKE, FAKE, 1 << 40, 0)
+    assert got2 == code
+    got3, _ = status_of(ws.wingspan_spgemm_numeric, A, B, ws.F64, FAKE, FAKE, FAKE, FAKE, 1 << 40, 0)
+    assert got3 == code
+
+
+def test_null_nnz_zero_pointers_allowed():
+    # nnz == 0 matrices may pass NULL col/val
+    n = ws.wingspan_spgemm_workspace_size(desc(4, 4, 0, col=0, val=0), desc(4, 4, 0, col=0, val=0), ws.F32)
+    assert n > 0
+
+
+def test_bad_dtype():
+    got, _ = status_of(ws.wingspan_spgemm_workspace_size, desc(4, 4, 1), desc(4, 4, 1), 7)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    got, _ = status_of(ws.wingspan_spgemm_numeric, desc(4, 4, 1), desc(4, 4, 1), 2, FAKE, FAKE, FAKE, FAKE,
+                       1 << 40, 0)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+
+
+@pytest.mark.parametrize("opts", [
+    dict(max_lds_slots=100), dict(max_lds_slots=32), dict(max_lds_slots=1 << 15),
+    dict(window_cols=2048), dict(tiny_max=7), dict(tiny_max=65), dict(dense_min_nnz=-2),
+])
+def test_bad_options(opts):
+    got, msg = status_of(ws.wingspan_spgemm_workspace_size, desc(4, 4, 1), desc(4, 4, 1), ws.F32,
+                         ws.make_options(**opts))
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT" and "options" in msg
+
+
+def test_bad_options_version():
+    o = ws.make_options()
+    o.version = 99
+    got, msg = status_of(ws.wingspan_spgemm_workspace_size, desc(4, 4, 1), desc(4, 4, 1), ws.F32, o)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT" and "version" in msg
+
+
+def test_workspace_too_small_and_misaligned():
+    A, B = desc(100, 100, 500), desc(100, 100, 500)
+    need = ws.wingspan_spgemm_workspace_size(A, B, ws.F64)
+    got, msg = status_of(ws.wingspan_spgemm_symbolic, A, B, FAKE, FAKE, need - 1, 0)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL" and str(need) in msg
+    got, _ = status_of(ws.wingspan_spgemm_numeric, A, B, ws.F64, FAKE, FAKE, FAKE, FAKE, need - 256, 0)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"
+    got, _ = status_of(ws.wingspan_spgemm_symbolic, A, B, FAKE, FAKE + 8, need, 0)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    got, _ = status_of(ws.wingspan_spgemm_symbolic, A, B, FAKE, 0, need, 0)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+
+
+def test_null_outputs():
+    A, B = desc(10, 10, 5), desc(10, 10, 5)
+    got, _ = status_of(ws.wingspan_spgemm_symbolic, A, B, 0, FAKE, 1 << 40, 0)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    got, _ = status_of(ws.wingspan_spgemm_numeric, A, B, ws.F64, 0, FAKE, FAKE, FAKE, 1 << 40, 0)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    got, _ = status_of(ws.wingspan_spgemm, A, B, ws.F64, FAKE, FAKE, FAKE, -1, FAKE, 1 << 40, 0)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+
+
+def test_last_stats_bad_phase():
+    got, _ = status_of(ws.wingspan_last_stats, 2)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+
+
+def test_error_message_is_thread_local_and_cleared():
+    with pytest.raises(ws.WingspanError):
+        ws.wingspan_spgemm_workspace_size(desc(3, 4, 1), desc(5, 4, 1), ws.F32)
+    assert "A.ncols" in ws.wingspan_last_error()
+    ws.wingspan_spgemm_workspace_size(desc(3, 4, 1), desc(4, 4, 1), ws.F32)
+    assert ws.wingspan_last_error() == ""

@@ -1,0 +1,285 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
+
+Structure (C.row_ptr, C.col_idx) must match bit for bit; values must lie
+within tol * sum_k |A[i,k] B[k,j]| with tol 1e-12 (fp64) and 1e-5 (fp32).
+Every tier is exercised on small inputs by routing rows to it with options.
+"""
+import numpy as np
+import pytest
+
+import matgen
+import oracle
+from gpu_util import assert_matches, golden, row_ptr_sha256, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def check(A, B, options=None, what=""):
+    got, sym, num = run_gpu(A, B, options)
+    ref = oracle.spgemm(A, B)
+    assert_matches(got, ref, A.val.dtype, what=what or str(options))
+    assert sym["total_products"] == int(ref.products.sum())
+    assert num["c_nnz_total"] == ref.nnz
+    return got, sym, num, ref
+
+
+# ---------------------------------------------------------------------------
+# degenerate and ragged shapes
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", [(0, 0, 0), (0, 5, 3), (4, 0, 6), (5, 6, 0), (1, 1, 1), (3, 2, 7)])
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_degenerate_shapes(shape, dtype):
+    m, k, n = shape
+    A = matgen.random_sparse(m, k, 0.7, 1, dtype)
+    B = matgen.random_sparse(k, n, 0.7, 2, dtype)
+    check(A, B, what=f"shape {shape}")
+
+
+def test_all_rows_empty():
+    A = matgen.random_sparse(50, 40, 0.0, 3)
+    B = matgen.random_sparse(40, 30, 0.5, 4)
+    got, _, num, _ = check(A, B)
+    assert got.row_ptr[-1] == 0
+
+
+def test_b_rows_empty():
+    # A has entries but every B row it selects is empty: no products at all
+    A = matgen.random_sparse(30, 40, 0.5, 5)
+    B = matgen.random_sparse(40, 30, 0.5, 6, empty_rows=1.0)
+    check(A, B)
+
+
+@pytest.mark.parametrize("shape", [(7, 33, 5), (33, 7, 64), (64, 64, 64), (17, 64, 33), (130, 70, 90)])
+@pytest.mark.parametrize("density", [0.1, 0.5, 1.0])
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_random_small(shape, density, dtype):
+    m, k, n = shape
+    A = matgen.random_sparse(m, k, density, m * 7 + k, dtype, empty_rows=0.2)
+    B = matgen.random_sparse(k, n, density, n * 5 + k, dtype, empty_rows=0.2)
+    check(A, B, what=f"{shape} d={density}")
+
+
+# ---------------------------------------------------------------------------
+# every tier, forced with options
+# ---------------------------------------------------------------------------
+
+TIER_OPTS = {
+    "default": None,
+    "tiny_off": dict(tiny_max=-1),
+    "tiny16": dict(tiny_max=16),
+    "hash_small": dict(tiny_max=-1, max_lds_slots=256, dense_min_nnz=-1),
+    "dense_w1024": dict(tiny_max=-1, max_lds_slots=64, window_cols=1024),
+    "dense_w4096": dict(tiny_max=-1, max_lds_slots=64, window_cols=4096),
+    "dense_pref": dict(dense_min_nnz=1, window_cols=1024),
+    "spill": dict(tiny_max=-1, force_spill=1),
+    "spill_tiny": dict(force_spill=1),
+    "validate": dict(validate=1),
+}
+
+
+def tier_inputs(kind, dtype):
+    if kind == "rmat":
+        A = matgen.rmat(11, 16, seed=7, dtype=dtype, dist="pm1" if dtype == np.float64 else "open01")
+        return A, A
+    if kind == "er":
+        return matgen.er_rect(400, 3000, 2500, 20, seed=8, dtype=dtype)
+    raise KeyError(kind)
+
+
+@pytest.mark.parametrize("opts", list(TIER_OPTS), ids=list(TIER_OPTS))
+@pytest.mark.parametrize("kind", ["rmat", "er"])
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+def test_tiers(opts, kind, dtype):
+    A, B = tier_inputs(kind, dtype)
+    got, sym, num, ref = check(A, B, TIER_OPTS[opts], what=f"{kind}/{opts}")
+    o = TIER_OPTS[opts] or {}
+    if o.get("tiny_max") == -1:
+        assert sym["rows"]["tiny"] == 0 and num["rows"]["tiny"] == 0
+    if o.get("force_spill") and o.get("tiny_max") == -1:
+        assert sym["rows"]["hash"] == sym["rows"]["dense"] == 0
+        assert num["rows"]["hash"] == num["rows"]["dense"] == 0
+        assert num["rows"]["spill"] > 0
+    if opts.startswith("dense"):
+        assert num["rows"]["dense"] > 0
+
+
+def test_tier_row_accounting():
+    A, B = tier_inputs("rmat", np.float32)
+    got, sym, num, ref = check(A, B, dict(max_lds_slots=512, window_cols=1024))
+    nonempty = int(np.sum(ref.products > 0))
+    assert sum(sym["rows"].values()) == nonempty
+    assert sum(num["products"].values()) == int(ref.products.sum())
+    assert sum(num["c_nnz"].values()) == ref.nnz
+    assert num["rows"]["dense"] > 0 and num["rows"]["hash"] > 0 and num["rows"]["tiny"] > 0
+
+
+# ---------------------------------------------------------------------------
+# identities, closed forms and special matrices
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_identity_and_permutation_bit_exact(dtype):
+    A = matgen.random_sparse(300, 300, 0.05, 9, dtype)
+    I = matgen.identity(300, dtype)
+    for L, R in ((I, A), (A, I)):
+        got, _, _ = run_gpu(L, R)
+        assert np.array_equal(got.row_ptr, A.row_ptr.astype(np.int64))
+        assert np.array_equal(got.col_idx, A.col_idx)
+        assert np.array_equal(got.val, A.val)
+    P = matgen.permutation(300, 10, dtype)
+    got, _, _ = run_gpu(P, A)
+    for i in range(300):
+        c, v = A.row(P.col_idx[i])
+        assert np.array_equal(got.col_idx[got.row_ptr[i]:got.row_ptr[i + 1]], c)
+        assert np.array_equal(got.val[got.row_ptr[i]:got.row_ptr[i + 1]], v)
+
+
+@pytest.mark.parametrize("opts", [None, dict(max_lds_slots=64, window_cols=1024), dict(force_spill=1)])
+def test_arrowhead_dense_square(opts):
+    n = 4096
+    A = matgen.arrowhead(n)
+    got, _, _ = run_gpu(A, A, opts)
+    assert got.row_ptr[-1] == n * n
+    rp = got.row_ptr
+    assert np.all(np.diff(rp) == n)
+    assert np.array_equal(got.col_idx.reshape(n, n), np.tile(np.arange(n, dtype=np.int32), (n, 1)))
+    C = got.val.reshape(n, n)
+    E = np.ones((n, n))
+    E[0, :] = 2
+    E[:, 0] = 2
+    E[np.arange(n), np.arange(n)] = 2
+    E[0, 0] = n
+    assert np.array_equal(C, E)
+
+
+def test_laplacian_512_bit_exact():
+    A, B = matgen.config("laplace512")
+    got, sym, num = run_gpu(A, B)
+    ref = oracle.spgemm(A, B)
+    assert np.array_equal(got.row_ptr, ref.row_ptr)
+    assert np.array_equal(got.col_idx, ref.col_idx)
+    assert np.array_equal(got.val, ref.val)        # small integers: exact in any order
+    g = golden("laplace512")
+    assert got.row_ptr[-1] == g["nnz_c"] == 3_397_636
+    assert sym["total_products"] == g["products"] == 6_535_176
+
+
+def test_er1000():
+    A, B = matgen.config("er1000")
+    got, sym, num, ref = check(A, B)
+    g = golden("er1000")
+    assert sym["total_products"] == g["products"] == 100_000
+    assert row_ptr_sha256(got.row_ptr) == g["row_ptr_sha256"]
+
+
+@pytest.mark.slow
+def test_er_rect_full():
+    A, B = matgen.config("er_rect")
+    got, sym, num = run_gpu(A, B)
+    g = golden("er_rect")
+    assert sym["total_products"] == g["products"] == 64_000_000
+    assert row_ptr_sha256(got.row_ptr) == g["row_ptr_sha256"]
+    ref = oracle.spgemm(A, B)
+    assert_matches(got, ref, A.val.dtype, what="er_rect")
+
+
+# ---------------------------------------------------------------------------
+# API behaviour on the device
+# ---------------------------------------------------------------------------
+
+def test_structure_deterministic():
+    A = matgen.rmat(12, 16, seed=11, dtype=np.float32)
+    first, _, _ = run_gpu(A, A, dict(max_lds_slots=256, window_cols=1024))
+    for _ in range(3):
+        again, _, _ = run_gpu(A, A, dict(max_lds_slots=256, window_cols=1024))
+        assert np.array_equal(first.row_ptr, again.row_ptr)
+        assert np.array_equal(first.col_idx, again.col_idx)
+
+
+def test_numeric_rerun_with_new_values():
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(11, 16, seed=12, dtype=np.float64, dist="pm1")
+    dA = ws.DeviceCSR.from_host(A, "cuda:0")
+    C = ws.spgemm(dA, dA)
+    A2 = matgen.CSR(A.nrows, A.ncols, A.row_ptr, A.col_idx, np.linspace(-1, 1, A.nnz))
+    dA2 = ws.DeviceCSR.from_host(A2, "cuda:0")
+    wsb, nbytes = ws.allocate_workspace(dA2, dA2)
+    h = torch.cuda.current_stream().cuda_stream
+    ws.wingspan_spgemm_numeric(dA2.desc(), dA2.desc(), ws.F64, C.row_ptr.data_ptr(), C.col_idx.data_ptr(),
+                               C.val.data_ptr(), wsb.data_ptr(), nbytes, h)
+    torch.cuda.synchronize()
+    assert_matches(C.to_host(), oracle.spgemm(A2, A2), np.float64, what="rerun")
+
+
+def test_combined_entry_and_capacity():
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(10, 16, seed=13, dtype=np.float32)
+    ref = oracle.spgemm(A, A)
+    dA = ws.DeviceCSR.from_host(A, "cuda:0")
+    wsb, nbytes = ws.allocate_workspace(dA, dA)
+    h = torch.cuda.current_stream().cuda_stream
+    rp = torch.empty(A.nrows + 1, dtype=torch.int64, device="cuda:0")
+    small = ref.nnz - 1
+    col = torch.empty(max(small, 1), dtype=torch.int32, device="cuda:0")
+    val = torch.empty(max(small, 1), dtype=torch.float32, device="cuda:0")
+    with pytest.raises(ws.WingspanError) as e:
+        ws.wingspan_spgemm(dA.desc(), dA.desc(), ws.F32, rp.data_ptr(), col.data_ptr(), val.data_ptr(), small,
+                           wsb.data_ptr(), nbytes, h)
+    assert ws.STATUS[e.value.status] == "WINGSPAN_ERR_INSUFFICIENT_CAPACITY"
+    assert np.array_equal(rp.cpu().numpy(), ref.row_ptr)
+    col = torch.empty(ref.nnz, dtype=torch.int32, device="cuda:0")
+    val = torch.empty(ref.nnz, dtype=torch.float32, device="cuda:0")
+    nnz = ws.wingspan_spgemm(dA.desc(), dA.desc(), ws.F32, rp.data_ptr(), col.data_ptr(), val.data_ptr(), ref.nnz,
+                             wsb.data_ptr(), nbytes, h)
+    torch.cuda.synchronize()
+    assert nnz == ref.nnz
+    got = ws.HostCSR(A.nrows, A.ncols, rp.cpu().numpy(), col.cpu().numpy(), val.cpu().numpy())
+    assert_matches(got, ref, np.float32, what="combined")
+
+
+def test_validate_rejects_noncanonical():
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.random_sparse(40, 40, 0.3, 14)
+    r = int(np.argmax(np.diff(A.row_ptr) >= 2))
+    col = A.col_idx.copy()
+    a = A.row_ptr[r]
+    col[a], col[a + 1] = col[a + 1], col[a]
+    bad = matgen.CSR(A.nrows, A.ncols, A.row_ptr, col, A.val)
+    dA = ws.DeviceCSR.from_host(A, "cuda:0")
+    dBad = ws.DeviceCSR.from_host(bad, "cuda:0")
+    with pytest.raises(ws.WingspanError) as e:
+        ws.spgemm(dBad, dA, options=dict(validate=1))
+    assert ws.STATUS[e.value.status] == "WINGSPAN_ERR_INVALID_MATRIX"
+    with pytest.raises(ws.WingspanError) as e:
+        ws.spgemm(dA, dBad, options=dict(validate=1))
+    assert ws.STATUS[e.value.status] == "WINGSPAN_ERR_INVALID_MATRIX"
+
+
+def test_validate_reports_inconsistent_row_ptr():
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(10, 16, seed=15, dtype=np.float64, dist="pm1")
+    dA = ws.DeviceCSR.from_host(A, "cuda:0")
+    C = ws.spgemm(dA, dA)
+    rp = C.row_ptr.clone()
+    # shift one row boundary: rows i and i+1 now disagree with the product
+    lens = torch.diff(rp)
+    i = int(torch.argmax(lens).item())
+    rp[i + 1] -= 1
+    wsb, nbytes = ws.allocate_workspace(dA, dA)
+    h = torch.cuda.current_stream().cuda_stream
+    with pytest.raises(ws.WingspanError) as e:
+        ws.wingspan_spgemm_numeric(dA.desc(), dA.desc(), ws.F64, rp.data_ptr(), C.col_idx.data_ptr(),
+                                   C.val.data_ptr(), wsb.data_ptr(), nbytes, h, dict(validate=1))
+    assert ws.STATUS[e.value.status] == "WINGSPAN_ERR_INCONSISTENT"
+
+
+def test_timing_option_fills_kernel_times():
+    A = matgen.rmat(12, 16, seed=16, dtype=np.float32)
+    got, sym, num = run_gpu(A, A, dict(timing=1, max_lds_slots=512, window_cols=1024))
+    assert num["analysis_ms"] > 0
+    assert all(v >= 0 for v in num["kernel_ms"].values())
+    assert sum(num["kernel_ms"].values()) > 0
