@@ -51,6 +51,17 @@ struct Control {
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+// Values every lane of the workgroup holds identically (read back from LDS
+// after a barrier) are moved to scalar registers, so loops and branches that
+// depend on them compile as uniform control flow. Barriers then never sit in
+// a region the compiler treats as divergent.
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ int64_t uniform(int64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(static_cast<uint64_t>(x) >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 __device__ __forceinline__ double to_d(float x) { return static_cast<double>(x); }
 __device__ __forceinline__ double to_d(double x) { return x; }
 
@@ -99,7 +110,7 @@ __device__ __forceinline__ T block_sum(T x, T *scratch) {
 #pragma unroll
     for (int i = 0; i < NW; ++i) t += scratch[i];
     __syncthreads();
-    return t;
+    return uniform(t);
 }
 
 // Block-wide exclusive prefix sum of int; returns the exclusive value and the
@@ -119,7 +130,7 @@ __device__ __forceinline__ int block_excl_scan(int x, int *total, int *scratch) 
         t += s;
     }
     __syncthreads();
-    *total = t;
+    *total = uniform(t);
     return before + incl - x;
 }
 
@@ -164,7 +175,7 @@ __device__ __forceinline__ void for_each_product(const int32_t *__restrict__ a_c
             if (VALUES) av = to_d(a_val[a]);
         }
         const int incl = group_incl_scan<kWave>(len);
-        const int tot = __shfl(incl, kWave - 1, kWave);
+        const int tot = uniform(__shfl(incl, kWave - 1, kWave));
         const int excl = incl - len;
         for (int p0 = wave_rank * kWave; p0 < tot; p0 += nwaves * kWave) {
             const int p = p0 + ln;

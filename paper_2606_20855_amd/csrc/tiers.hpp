@@ -178,7 +178,7 @@ __global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *_
     __syncthreads();
 
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
-    const int wv = threadIdx.x / kWave;
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int inserted = 0;
     bool overflow = false;
     for_each_product<V, NUM>(
@@ -284,7 +284,7 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
     __syncthreads();
-    const int wv = threadIdx.x / kWave;
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     for_each_product<float, false>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1],
                                    BRowRange{M.b_rp}, M.b_col, nullptr, wv, NW,
                                    [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
@@ -326,7 +326,7 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
     const int64_t cb = c_rp[row];
     const int64_t seg = c_rp[row + 1] - cb;
-    const int wv = threadIdx.x / kWave;
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     int64_t out = 0;
     for (int w = 0; w < nwin; ++w) {
@@ -479,73 +479,61 @@ __device__ void merge_sort_segment(int32_t *__restrict__ col, V *__restrict__ va
     }
 }
 
+// One row of the spill tier, processed by the whole workgroup in its slab.
 template <typename V, bool NUM>
-__global__ void __launch_bounds__(kSpillBlock) spill_kernel(
-    Mats<V> M, const int32_t *__restrict__ rows, int32_t nrows, const int64_t *__restrict__ pref,
-    int64_t ncols, char *__restrict__ pool, int64_t slab_cap, int32_t *__restrict__ row_nnz,
-    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val,
-    Control *ctrl) {
+__device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64_t *__restrict__ pref,
+                                          int64_t ncols, int32_t *__restrict__ keys, double *__restrict__ vals,
+                                          int32_t *__restrict__ row_nnz, const int64_t *__restrict__ c_rp,
+                                          int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
+                                          int32_t *scratch, int32_t *s_keys, V *s_vals) {
     constexpr int BLOCK = kSpillBlock;
     constexpr int NW = BLOCK / kWave;
-    __shared__ int32_t s_row;
-    __shared__ int32_t scratch[NW];
-    __shared__ int32_t s_keys[NUM ? kRunLen : 1];
-    __shared__ V s_vals[NUM ? kRunLen : 1];
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
+    const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
+    int64_t bound;
+    if (NUM) {
+        bound = c_rp[row + 1] - c_rp[row];
+    } else {
+        const int64_t f = pref[a_hi] - pref[a_lo];
+        bound = f < ncols ? f : ncols;
+    }
+    int log2t = ceil_log2(2 * (bound > 0 ? bound : 1));
+    if (log2t < 6) log2t = 6;
+    log2t = uniform(log2t);
+    const int64_t T = int64_t(1) << log2t;   // the host guarantees T <= slab capacity
+    for (int64_t i = threadIdx.x; i < T; i += BLOCK) {
+        keys[i] = kEmptyKey;
+        if (NUM) vals[i] = 0.0;
+    }
+    // make the cleared table visible at the device level before any atomic
+    __threadfence();
+    __syncthreads();
 
-    int32_t *keys = reinterpret_cast<int32_t *>(pool + static_cast<int64_t>(blockIdx.x) * slab_cap * 12);
-    double *vals = reinterpret_cast<double *>(keys + slab_cap);
-    const int wv = threadIdx.x / kWave;
-
-    for (;;) {
-        if (threadIdx.x == 0) s_row = atomicAdd(&ctrl->spill_next, 1);
-        __syncthreads();
-        const int ri = s_row;
-        __syncthreads();
-        if (ri >= nrows) break;
-        const int row = rows[ri];
-        const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
-        int64_t bound;
-        if (NUM) {
-            bound = c_rp[row + 1] - c_rp[row];
-        } else {
-            const int64_t f = pref[a_hi] - pref[a_lo];
-            bound = f < ncols ? f : ncols;
-        }
-        int log2t = ceil_log2(2 * (bound > 0 ? bound : 1));
-        if (log2t < 6) log2t = 6;
-        const int64_t T = int64_t(1) << log2t;   // host guarantees T <= slab_cap
-        for (int64_t i = threadIdx.x; i < T; i += BLOCK) {
-            keys[i] = kEmptyKey;
-            if (NUM) vals[i] = 0.0;
-        }
-        __syncthreads();
-
-        int inserted = 0;
-        bool overflow = false;
-        for_each_product<V, NUM>(
-            M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
-            [&](int col, double prod) {
-                uint32_t h = hash_slot(col, log2t);
-                for (int64_t probe = 0; probe < T; ++probe) {
-                    const int old = atomicCAS(&keys[h], kEmptyKey, col);
-                    if (old == kEmptyKey || old == col) {
-                        inserted += (old == kEmptyKey);
-                        if (NUM) unsafeAtomicAdd(&vals[h], prod);
-                        return;
-                    }
-                    h = (h + 1) & static_cast<uint32_t>(T - 1);
+    int inserted = 0;
+    bool overflow = false;
+    for_each_product<V, NUM>(
+        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
+        [&](int col, double prod) {
+            uint32_t h = hash_slot(col, log2t);
+            for (int64_t probe = 0; probe < T; ++probe) {
+                const int old = atomicCAS(&keys[h], kEmptyKey, col);
+                if (old == kEmptyKey || old == col) {
+                    inserted += (old == kEmptyKey);
+                    if (NUM) unsafeAtomicAdd(&vals[h], prod);
+                    return;
                 }
-                overflow = true;
-            });
-        if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
-        if (!NUM) {
-            const int total = block_sum<BLOCK>(inserted, scratch);
-            if (threadIdx.x == 0) row_nnz[row] = total;
-            continue;
-        }
+                h = (h + 1) & static_cast<uint32_t>(T - 1);
+            }
+            overflow = true;
+        });
+    if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
+    if constexpr (!NUM) {
+        const int total = block_sum<BLOCK>(inserted, scratch);
+        if (threadIdx.x == 0) row_nnz[row] = total;
+    } else {
+        __threadfence();
         __syncthreads();
-
-        // compact the table into the row of C (slot order), then sort it
+        // compact the table into the row of C (slot order), then sort it there
         const int64_t cb = c_rp[row];
         const int64_t seg = c_rp[row + 1] - cb;
         int running = 0;
@@ -568,10 +556,39 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
         }
         if (threadIdx.x == 0 && running != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
         __syncthreads();
-        const int len = static_cast<int64_t>(running) < seg ? running : static_cast<int>(seg);
-        merge_sort_segment<V>(c_col + cb, c_val + cb, len, keys, reinterpret_cast<V *>(vals),
-                              s_keys, s_vals);
+        const int len = uniform(static_cast<int64_t>(running) < seg ? running : static_cast<int>(seg));
+        merge_sort_segment<V>(c_col + cb, c_val + cb, len, keys, reinterpret_cast<V *>(vals), s_keys, s_vals);
+    }
+    __syncthreads();
+}
+
+template <typename V, bool NUM>
+__global__ void __launch_bounds__(kSpillBlock) spill_kernel(
+    Mats<V> M, const int32_t *__restrict__ rows, int32_t nrows, const int64_t *__restrict__ pref,
+    int64_t ncols, char *__restrict__ pool, int64_t slab_cap, int32_t *__restrict__ row_nnz,
+    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val,
+    Control *ctrl) {
+    constexpr int NW = kSpillBlock / kWave;
+    __shared__ int32_t s_row;
+    __shared__ int32_t scratch[NW];
+    __shared__ int32_t s_keys[NUM ? kRunLen : 1];
+    __shared__ V s_vals[NUM ? kRunLen : 1];
+
+    int32_t *keys = reinterpret_cast<int32_t *>(pool + static_cast<int64_t>(blockIdx.x) * slab_cap * 12);
+    double *vals = reinterpret_cast<double *>(keys + slab_cap);
+
+    // Rows are claimed one at a time from a shared counter until none are
+    // left. The claimed index is read back into a scalar register so the loop
+    // exit is uniform across the workgroup (every barrier below is reached by
+    // all waves with all lanes active).
+    for (;;) {
+        if (threadIdx.x == 0) s_row = atomicAdd(&ctrl->spill_next, 1);
         __syncthreads();
+        const int ri = uniform(s_row);
+        __syncthreads();
+        if (ri >= nrows) break;
+        spill_row<V, NUM>(M, rows[ri], pref, ncols, keys, vals, row_nnz, c_rp, c_col, c_val, ctrl, scratch,
+                          s_keys, s_vals);
     }
 }
 
