@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""SpGEMM benchmark on one MI355X: C = A*A for the R-MAT scale-18 workload.
+
+A step is one pass of the whole hot path: the symbolic phase (product counts,
+binning, per-tier entry counts, C.row_ptr scan) and the numeric phase
+(re-binning and the per-tier accumulate-and-emit kernels) over the resident
+input, writing into a preallocated C. Prints one JSON line:
+
+  value      GFLOP/s of the whole step, 2 * products / step time
+  roofline   the dominant numeric kernel against HBM bandwidth, from
+             algorithmic bytes and its HIP-event time on the library's stream
+  numeric_phase  algorithmic bytes of the numeric phase / its time
+  cpu_baseline   the CPU oracle (single thread) on a seeded random sample of rows
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rmat18]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SpGEMM GFLOP/s (2×products/s) + effective HBM GB/s vs peak, 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SOURCES = ["paper_2606_20855_amd/csrc/tiers.hpp", "paper_2606_20855_amd/csrc/device_common.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "numeric_dense_rmat18_traffic.md")
+KERNEL_NAMES = {
+    "tiny": "wsp::tiny_kernel (numeric)",
+    "hash": "wsp::hash_kernel (numeric)",
+    "dense": "wsp::dense_num_kernel",
+    "spill": "wsp::spill_kernel (numeric)",
+}
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_sha256() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dense numeric kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip().strip("-* `")] = v.strip().strip("`")
+    if vals.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    try:
+        return int(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def alg_bytes(rows, a_nnz, products, c_nnz, s):
+    """Algorithmic bytes of the numeric work on these rows: A.row_ptr and
+    C.row_ptr (4 + 8 per row), A entries (4 + s), a B.row_ptr pair per A entry
+    (8), one B entry per product (4 + s), one C entry per output (4 + s)."""
+    return 12 * rows + (12 + s) * a_nnz + (4 + s) * products + (4 + s) * c_nnz
+
+
+def cpu_baseline(A, B, fraction: float, seed: int):
+    import oracle
+    rng = np.random.default_rng(seed)
+    rows = np.sort(rng.choice(A.nrows, size=max(1, int(A.nrows * fraction)), replace=False)).astype(np.int64)
+    prods = int(oracle.row_products(A, B, rows).sum())
+    t0 = time.perf_counter()
+    res = oracle.spgemm(A, B, rows=rows, with_mag=False)
+    dt = time.perf_counter() - t0
+    return dict(
+        value=round(2.0 * prods / dt / 1e9, 5),
+        unit="GFLOP/s",
+        cores=1,
+        kind="oracle",
+        sample=(f"{len(rows)} rows ({fraction:.0%}) drawn uniformly at random (seed {seed}) from the same "
+                f"matrix; {prods} products, {res.nnz} output entries, {dt:.1f} s single-threaded"),
+    )
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="rmat18")
+    ap.add_argument("--cpu-fraction", type=float, default=0.08)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import matgen
+    from paper_2606_20855_amd import wingspan as ws
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    cfg = matgen.CONFIGS[args.workload]
+    t0 = time.time()
+    A, B = matgen.config(args.workload)
+    log(f"generated {args.workload}: m={A.nrows} nnz(A)={A.nnz} in {time.time() - t0:.1f}s")
+    dA = ws.DeviceCSR.from_host(A, dev)
+    dB = dA if B is A else ws.DeviceCSR.from_host(B, dev)
+    Ad, Bd = dA.desc(), dB.desc()
+    dt = dA.dtype_code
+    s = 4 if dt == ws.F32 else 8
+    opts = ws.make_options(timing=1)
+    wsb, nbytes = ws.allocate_workspace(dA, dB, opts)
+    stream = torch.cuda.current_stream()
+    h = stream.cuda_stream
+    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device=dev)
+    nnz = ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
+    c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(nnz, 1), dtype=dA.val.dtype, device=dev)
+    log(f"nnz(C)={nnz}, workspace {nbytes / 2**20:.1f} MiB")
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+
+    def step():
+        ev[0].record(stream)
+        ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
+        sym = ws.wingspan_last_stats(0)
+        ev[1].record(stream)
+        ws.wingspan_spgemm_numeric(Ad, Bd, dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                                   wsb.data_ptr(), nbytes, h, opts)
+        num = ws.wingspan_last_stats(1)
+        ev[2].record(stream)
+        return sym, num
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sym_ms, num_ms, tier_ms, ana_ms = [], [], {t: [] for t in ws.TIERS}, []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        sym, num = step()
+        ev[2].synchronize()
+        sym_ms.append(ev[0].elapsed_time(ev[1]))
+        num_ms.append(ev[1].elapsed_time(ev[2]))
+        ana_ms.append(num["analysis_ms"])
+        for t in ws.TIERS:
+            tier_ms[t].append(num["kernel_ms"][t])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed / args.steps * 1e3
+
+    P = int(sym["total_products"])
+    nnz_c = int(num["c_nnz_total"])
+    gflops = 2.0 * P / (ms_per_step / 1e3) / 1e9
+
+    # numeric phase against HBM bandwidth on algorithmic bytes
+    b_num = alg_bytes(A.nrows, A.nnz, P, nnz_c, s)
+    t_num = float(np.mean(num_ms))
+    numeric_phase = dict(ms=round(t_num, 4), ms_min=round(float(np.min(num_ms)), 4),
+                         alg_bytes=b_num, GBps=round(b_num / (t_num / 1e3) / 1e9, 1),
+                         frac=round(b_num / (t_num / 1e3) / 1e9 / HBM_PEAK_GBPS, 4))
+
+    # dominant numeric kernel
+    dom = max(ws.TIERS, key=lambda t: np.mean(tier_ms[t]))
+    k_ms = float(np.mean(tier_ms[dom]))
+    launches = int(num["launches"][dom])
+    b_dom = alg_bytes(num["rows"][dom], num["a_nnz"][dom], num["products"][dom], num["c_nnz"][dom], s)
+    per_launch = b_dom / max(launches, 1)
+    achieved = per_launch / (k_ms / max(launches, 1) / 1e3) / 1e9 if k_ms > 0 else 0.0
+    traffic = measured_traffic() if dom == "dense" else None
+    roofline = dict(bound="hbm", kernel=KERNEL_NAMES[dom], achieved=round(achieved, 1), peak=HBM_PEAK_GBPS,
+                    unit="GB/s", frac=round(achieved / HBM_PEAK_GBPS, 4), traffic=traffic,
+                    alg_bytes_per_launch=int(per_launch), launches_per_step=launches,
+                    avg_launch_ms=round(k_ms / max(launches, 1), 4))
+
+    out = dict(
+        metric=METRIC,
+        value=round(gflops, 2),
+        unit="GFLOP/s",
+        n_gpus=1,
+        steps=args.steps,
+        warmup=args.warmup,
+        ms_per_step=round(ms_per_step, 4),
+        higher_is_better=True,
+        scaling="weak",
+        vs_baseline=None,
+        dtype="f64",
+        data="synthetic",
+        config=dict(
+            workload=f"{args.workload}: {cfg['desc']}",
+            m=A.nrows, n=B.ncols, nnz_a=A.nnz, nnz_b=B.nnz, products=P, nnz_c=nnz_c,
+            value_dtype=str(A.val.dtype), accumulate="f64",
+            seed=cfg["seed"], options="defaults (timing on)",
+        ),
+        roofline=roofline,
+        numeric_phase=numeric_phase,
+        symbolic_ms=round(float(np.mean(sym_ms)), 4),
+        numeric_ms=round(t_num, 4),
+        numeric_tier_ms={t: round(float(np.mean(tier_ms[t])), 4) for t in ws.TIERS},
+        numeric_analysis_ms=round(float(np.mean(ana_ms)), 4),
+        numeric_tier_rows={t: int(num["rows"][t]) for t in ws.TIERS},
+        numeric_tier_products={t: int(num["products"][t]) for t in ws.TIERS},
+    )
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a row sample")
+        out["cpu_baseline"] = cpu_baseline(A, B, args.cpu_fraction, seed=20261)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

