@@ -26,14 +26,16 @@ struct BRowRange {
     }
 };
 
-// Slice of B row k inside column window w, from the window table.
+// Slice of B row k covering column windows [w, w_end) (w_end = w + 1 by
+// default), from the window table.
 struct BWindowRange {
     const int32_t *wtab;
     int64_t stride;
     int w;
+    int w_end = -1;
     __device__ __forceinline__ int2 operator()(int32_t k) const {
-        const int32_t *t = wtab + static_cast<int64_t>(k) * stride + w;
-        return make_int2(t[0], t[1]);
+        const int32_t *t = wtab + static_cast<int64_t>(k) * stride;
+        return make_int2(t[w], t[w_end < 0 ? w + 1 : w_end]);
     }
 };
 
@@ -152,22 +154,129 @@ __global__ void __launch_bounds__(256) tiny_kernel(Mats<V> M, const int32_t *__r
 }
 
 // ---------------------------------------------------------------------------
+// LDS hash table helpers.
+// ---------------------------------------------------------------------------
+
+// Adds `prod` at key `col` of an LDS open-addressing table of 2^log2t slots
+// (Fibonacci hash, linear probing). Returns 1 if the key was new, 0 if it was
+// already present, -1 if every slot was probed without finding room.
+template <bool NUM>
+__device__ __forceinline__ int lds_insert(int32_t *keys, double *vals, int log2t, int col, double prod) {
+    const uint32_t mask = (1u << log2t) - 1u;
+    uint32_t h = hash_slot(col, log2t);
+    for (uint32_t probe = 0; probe <= mask; ++probe) {
+        const int cur = __hip_atomic_load(&keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (cur == col) {
+            if (NUM) atomicAdd(&vals[h], prod);
+            return 0;
+        }
+        if (cur == kEmptyKey) {
+            const int old = atomicCAS(&keys[h], kEmptyKey, col);
+            if (old == kEmptyKey || old == col) {
+                if (NUM) atomicAdd(&vals[h], prod);
+                return old == kEmptyKey ? 1 : 0;
+            }
+        }
+        h = (h + 1) & mask;
+    }
+    return -1;
+}
+
+// Writes the occupied slots of an LDS hash table (keys[0..T), vals[0..T)) to
+// C[cb + out0 ...] in increasing column order without sorting them. Columns
+// [col_lo, col_hi) are covered in bitmap windows of BWW*32 columns: the table's
+// columns are marked in an LDS presence bitmap, words are grouped by eight
+// and the groups' exclusive prefix counts taken, and every entry's position is
+// its group's offset plus the set bits before it in its group. Writes never
+// reach past C[cb + seg). Returns the new output count (uniform).
+template <int BLOCK, int BWW, typename V>
+__device__ int64_t rank_emit(const int32_t *keys, const double *vals, int T, int64_t col_lo, int64_t col_hi,
+                             uint32_t *bm, int32_t *goff, int32_t *scratch, int32_t *__restrict__ c_col,
+                             V *__restrict__ c_val, int64_t cb, int64_t out0, int64_t seg) {
+    constexpr int64_t SPAN = int64_t(BWW) * 32;
+    int64_t out = out0;
+    for (int64_t wb = col_lo; wb < col_hi; wb += SPAN) {
+        const int span = static_cast<int>((col_hi - wb) < SPAN ? (col_hi - wb) : SPAN);
+        const int ngroups = (span + 255) >> 8;
+        for (int i = threadIdx.x; i < ngroups * 8; i += BLOCK) bm[i] = 0u;
+        __syncthreads();
+        for (int s = threadIdx.x; s < T; s += BLOCK) {
+            const int k = keys[s];
+            if (k != kEmptyKey && k >= wb && k < wb + span) {
+                const int rel = static_cast<int>(k - wb);
+                atomicOr(&bm[rel >> 5], 1u << (rel & 31));
+            }
+        }
+        __syncthreads();
+        int carry = 0;
+        for (int g0 = 0; g0 < ngroups; g0 += BLOCK) {
+            const int g = g0 + threadIdx.x;
+            int cnt = 0;
+            if (g < ngroups) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) cnt += __popc(bm[g * 8 + i]);
+            }
+            int tot;
+            const int ex = block_excl_scan<BLOCK>(cnt, &tot, scratch);
+            if (g < ngroups) goff[g] = carry + ex;
+            carry += tot;
+        }
+        __syncthreads();
+        for (int s = threadIdx.x; s < T; s += BLOCK) {
+            const int k = keys[s];
+            if (k != kEmptyKey && k >= wb && k < wb + span) {
+                const int rel = static_cast<int>(k - wb);
+                const int word = rel >> 5;
+                int r = goff[word >> 3];
+                for (int i = word & ~7; i < word; ++i) r += __popc(bm[i]);
+                r += __popc(bm[word] & ((1u << (rel & 31)) - 1u));
+                const int64_t pos = out + r;
+                if (pos < seg) {
+                    c_col[cb + pos] = k;
+                    c_val[cb + pos] = static_cast<V>(vals[s]);
+                }
+            }
+        }
+        out += carry;
+        __syncthreads();
+    }
+    return out;
+}
+
+// ---------------------------------------------------------------------------
 // Hash tier: one workgroup per row, an LDS table of 2^LOG2T slots.
 // Symbolic keeps keys only and counts first insertions. Numeric also adds the
-// product into the slot's double, then compacts the occupied slots, bitonic-
-// sorts them by column in LDS and writes the row.
+// product into the slot's double, then writes the row in column order: large
+// tables by rank emission (presence bitmap + popcount ranks, no sort) when the
+// column space takes at most kMaxRankWindows bitmap windows, otherwise (and
+// for small tables) by compacting the slots and bitonic-sorting them in LDS.
 // ---------------------------------------------------------------------------
-template <int LOG2T, int BLOCK, typename V, bool NUM>
-__global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *__restrict__ rows,
-                                                     int32_t *__restrict__ row_nnz,
-                                                     const int64_t *__restrict__ c_rp,
-                                                     int32_t *__restrict__ c_col,
-                                                     V *__restrict__ c_val, Control *ctrl) {
-    constexpr int T = 1 << LOG2T;
+constexpr int kMaxRankWindows = 4;
+
+template <int LOG2T>
+struct HashShape {
+    static constexpr int T = 1 << LOG2T;
+    static constexpr int BLOCK = T <= 256 ? 64 : (T <= 512 ? 128 : (T <= 2048 ? 256 : (T <= 4096 ? 512 : 1024)));
+    // bitmap words for rank emission (0: always sort)
+    static constexpr int BWW = LOG2T >= 13 ? 8192 : (LOG2T >= 11 ? 2048 : 0);
+};
+
+template <int LOG2T, typename V, bool NUM>
+__global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M, const int32_t *__restrict__ rows,
+                                                                       int64_t ncols,
+                                                                       int32_t *__restrict__ row_nnz,
+                                                                       const int64_t *__restrict__ c_rp,
+                                                                       int32_t *__restrict__ c_col,
+                                                                       V *__restrict__ c_val, Control *ctrl) {
+    constexpr int T = HashShape<LOG2T>::T;
+    constexpr int BLOCK = HashShape<LOG2T>::BLOCK;
+    constexpr int BWW = NUM ? HashShape<LOG2T>::BWW : 0;
     constexpr int NW = BLOCK / kWave;
     static_assert(T >= BLOCK, "table smaller than block");
     __shared__ int32_t keys[T];
     __shared__ double vals[NUM ? T : 1];
+    __shared__ uint32_t bm[BWW > 0 ? BWW : 1];
+    __shared__ int32_t goff[BWW > 0 ? BWW / 8 : 1];
     __shared__ int32_t scratch[NW];
 
     const int row = rows[blockIdx.x];
@@ -181,28 +290,12 @@ __global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *_
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int inserted = 0;
     bool overflow = false;
-    for_each_product<V, NUM>(
-        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
-        [&](int col, double prod) {
-            uint32_t h = hash_slot(col, LOG2T);
-            for (int probe = 0; probe < T; ++probe) {
-                const int cur = __hip_atomic_load(&keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                if (cur == col) {
-                    if (NUM) atomicAdd(&vals[h], prod);
-                    return;
-                }
-                if (cur == kEmptyKey) {
-                    const int old = atomicCAS(&keys[h], kEmptyKey, col);
-                    if (old == kEmptyKey || old == col) {
-                        inserted += (old == kEmptyKey);
-                        if (NUM) atomicAdd(&vals[h], prod);
-                        return;
-                    }
-                }
-                h = (h + 1) & (T - 1);
-            }
-            overflow = true;
-        });
+    for_each_product<V, NUM>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
+                             [&](int col, double prod) {
+                                 const int r = lds_insert<NUM>(keys, vals, LOG2T, col, prod);
+                                 inserted += r > 0;
+                                 overflow |= r < 0;
+                             });
     if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
 
     if (!NUM) {
@@ -212,6 +305,18 @@ __global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *_
     }
     __syncthreads();
 
+    const int64_t cb = c_rp[row];
+    const int64_t seg = c_rp[row + 1] - cb;
+    if constexpr (BWW > 0) {
+        const int64_t nbw = (ncols + int64_t(BWW) * 32 - 1) / (int64_t(BWW) * 32);
+        if (nbw <= kMaxRankWindows) {
+            const int64_t total = rank_emit<BLOCK, BWW, V>(keys, vals, T, 0, ncols, bm, goff, scratch, c_col,
+                                                           c_val, cb, 0, seg);
+            if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+            return;
+        }
+    }
+
     // compact occupied slots to the front of the table
     constexpr int PER = T / BLOCK;
     int kk[PER];
@@ -219,9 +324,9 @@ __global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *_
     int cnt = 0;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-        const int s = threadIdx.x + j * BLOCK;
-        kk[j] = keys[s];
-        vv[j] = vals[s];
+        const int s2 = threadIdx.x + j * BLOCK;
+        kk[j] = keys[s2];
+        vv[j] = vals[s2];
         cnt += kk[j] != kEmptyKey;
     }
     int total;
@@ -236,6 +341,7 @@ __global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *_
     }
     int n2 = 1;
     while (n2 < total) n2 <<= 1;
+    n2 = uniform(n2);
     for (int i = total + threadIdx.x; i < n2; i += BLOCK) keys[i] = kPadKey;
     __syncthreads();
 
@@ -259,8 +365,6 @@ __global__ void __launch_bounds__(BLOCK) hash_kernel(Mats<V> M, const int32_t *_
         }
     }
 
-    const int64_t cb = c_rp[row];
-    const int64_t seg = c_rp[row + 1] - cb;
     if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
     const int lim = static_cast<int64_t>(total) < seg ? total : static_cast<int>(seg);
     for (int i = threadIdx.x; i < lim; i += BLOCK) {
@@ -300,77 +404,128 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
 // For each window the workgroup accumulates every product whose column falls
 // inside it into a dense LDS array of doubles (plus a presence bitmap), then
 // emits the window's entries in column order by scanning the bitmap: no hash
-// and no sort. Emission clears what it read, so the next window starts from
-// zero. The window table gives each B row's slice inside the window.
+// and no sort. Each wave emits its own slice of the window after one barrier
+// and clears what it read, so the next window starts from zero. The window
+// table gives each B row's slice inside the window.
+//
+// Because C.row_ptr gives the row's entry count, the kernel knows how many
+// entries are still to come after each window. As soon as the remainder fits
+// an LDS hash table carved out of the window's own storage, the rest of the
+// row (all remaining columns at once) is accumulated in that table and written
+// by rank emission. Sparse tails therefore cost one pass instead of one pass
+// per window.
 // ---------------------------------------------------------------------------
+template <int WV>
+struct DenseShape {
+    static constexpr int BLOCK = 1024;
+    static constexpr int NW = BLOCK / kWave;
+    static constexpr int NWORDS = WV / 32;
+    static constexpr int WCOLS = WV / NW;            // columns each wave emits
+    static constexpr int TAIL_LOG2 = 0 + (WV == 16384 ? 13 : (WV == 4096 ? 11 : 9));
+    static constexpr int TAIL_T = 1 << TAIL_LOG2;    // tail table slots (12 B each)
+    static constexpr int TAIL_CAP = (TAIL_T * 2) / 3;
+    static constexpr int BWW = WV / 2;               // tail rank bitmap words
+    static_assert(WCOLS % kWave == 0, "window must split into 64-column chunks per wave");
+    static_assert(TAIL_T * 12 + BWW * 4 <= WV * 8, "tail table and bitmap must fit in the window");
+};
+
 template <int WV, typename V>
 __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_t *__restrict__ rows,
                                                          const int32_t *__restrict__ wtab, int nwin,
-                                                         const int64_t *__restrict__ c_rp,
+                                                         int64_t ncols, const int64_t *__restrict__ c_rp,
                                                          int32_t *__restrict__ c_col,
                                                          V *__restrict__ c_val, Control *ctrl) {
-    constexpr int BLOCK = 1024;
-    constexpr int NW = BLOCK / kWave;
-    constexpr int NWORDS = WV / 32;
-    constexpr int NCHUNK = WV / 64;
+    using S = DenseShape<WV>;
+    constexpr int BLOCK = S::BLOCK;
+    constexpr int NW = S::NW;
+    constexpr int WWORDS = S::WCOLS / 32;
     __shared__ double acc[WV];
-    __shared__ uint32_t bm[NWORDS];
-    __shared__ int32_t chunk_off[NCHUNK];
-    __shared__ int32_t win_total;
+    __shared__ uint32_t bm[S::NWORDS];
+    __shared__ int32_t wave_cnt[NW];
+    __shared__ int32_t goff[S::BWW / 8];
+    __shared__ int32_t scratch[NW];
 
     const int row = rows[blockIdx.x];
-    for (int i = threadIdx.x; i < WV; i += BLOCK) acc[i] = 0.0;
-    for (int i = threadIdx.x; i < NWORDS; i += BLOCK) bm[i] = 0u;
-    __syncthreads();
-
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
     const int64_t cb = c_rp[row];
     const int64_t seg = c_rp[row + 1] - cb;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
+    const int64_t stride = static_cast<int64_t>(nwin) + 1;
+
     int64_t out = 0;
-    for (int w = 0; w < nwin; ++w) {
+    int w = 0;
+    if (seg > S::TAIL_CAP) {
+        for (int i = threadIdx.x; i < WV; i += BLOCK) acc[i] = 0.0;
+        for (int i = threadIdx.x; i < S::NWORDS; i += BLOCK) bm[i] = 0u;
+        __syncthreads();
+    }
+    for (; w < nwin && seg - out > S::TAIL_CAP; ++w) {
         const int w0 = w * WV;
-        for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi,
-                                  BWindowRange{wtab, static_cast<int64_t>(nwin) + 1, w}, M.b_col,
-                                  M.b_val, wv, NW, [&](int col, double prod) {
+        for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w}, M.b_col, M.b_val,
+                                  wv, NW, [&](int col, double prod) {
                                       const int loc = col - w0;
                                       atomicAdd(&acc[loc], prod);
                                       atomicOr(&bm[loc >> 5], 1u << (loc & 31));
                                   });
         __syncthreads();
-        for (int c = threadIdx.x; c < NCHUNK; c += BLOCK)
-            chunk_off[c] = __popc(bm[2 * c]) + __popc(bm[2 * c + 1]);
+        // each wave counts its slice, then emits it at its offset
+        const int wbase = wv * S::WCOLS;
+        int cnt = 0;
+        for (int i = ln; i < WWORDS; i += kWave) cnt += __popc(bm[(wbase >> 5) + i]);
+        cnt = wave_sum(cnt);
+        if (ln == 0) wave_cnt[wv] = cnt;
         __syncthreads();
-        if (wv == 0) {
-            int carry = 0;
-            for (int c0 = 0; c0 < NCHUNK; c0 += kWave) {
-                const int c = c0 + ln;
-                const int v = c < NCHUNK ? chunk_off[c] : 0;
-                const int inc = group_incl_scan<kWave>(v);
-                if (c < NCHUNK) chunk_off[c] = carry + inc - v;
-                carry += __shfl(inc, kWave - 1, kWave);
-            }
-            if (ln == 0) win_total = carry;
+        int before = 0, wtot = 0;
+        for (int i = 0; i < NW; ++i) {
+            const int x = wave_cnt[i];
+            before += i < wv ? x : 0;
+            wtot += x;
         }
-        __syncthreads();
-        for (int c = wv; c < NCHUNK; c += NW) {
-            const int loc = c * kWave + ln;
+        int64_t pos0 = out + uniform(before);
+        for (int c = 0; c < S::WCOLS / kWave; ++c) {
+            const int loc = wbase + c * kWave + ln;
             const bool set = (bm[loc >> 5] >> (loc & 31)) & 1u;
             const uint64_t bal = __ballot(set);
             if (set) {
-                const int64_t pos = out + chunk_off[c] + __popcll(bal & ((1ull << ln) - 1ull));
+                const int64_t pos = pos0 + __popcll(bal & ((1ull << ln) - 1ull));
                 if (pos < seg) {
                     c_col[cb + pos] = w0 + loc;
                     c_val[cb + pos] = static_cast<V>(acc[loc]);
                 }
                 acc[loc] = 0.0;
             }
+            pos0 += __popcll(bal);
+        }
+        for (int i = ln; i < WWORDS; i += kWave) bm[(wbase >> 5) + i] = 0u;
+        out += uniform(wtot);
+        __syncthreads();
+    }
+
+    if (w < nwin && seg - out > 0) {
+        // the remaining columns [w*WV, ncols) fit an LDS hash table
+        const int64_t rem = seg - out;
+        int log2t = ceil_log2(rem + (rem >> 1));
+        if (log2t < 6) log2t = 6;
+        log2t = uniform(log2t);
+        const int T = 1 << log2t;
+        int32_t *tk = reinterpret_cast<int32_t *>(acc);
+        double *tv = reinterpret_cast<double *>(tk + T);
+        uint32_t *tbm = reinterpret_cast<uint32_t *>(acc) + (2 * WV - S::BWW);
+        for (int i = threadIdx.x; i < T; i += BLOCK) {
+            tk[i] = kEmptyKey;
+            tv[i] = 0.0;
         }
         __syncthreads();
-        for (int i = threadIdx.x; i < NWORDS; i += BLOCK) bm[i] = 0u;
-        out += win_total;
+        bool overflow = false;
+        for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w, nwin}, M.b_col,
+                                  M.b_val, wv, NW, [&](int col, double prod) {
+                                      overflow |= lds_insert<true>(tk, tv, log2t, col, prod) < 0;
+                                  });
+        if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
         __syncthreads();
+        out = rank_emit<BLOCK, S::BWW, V>(tk, tv, T, static_cast<int64_t>(w) * WV, ncols, tbm, goff, scratch,
+                                          c_col, c_val, cb, out, seg);
     }
     if (threadIdx.x == 0 && out != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
 }

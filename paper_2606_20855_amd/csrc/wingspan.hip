@@ -357,29 +357,31 @@ void launch_tiny(int s_idx, unsigned grid, hipStream_t st, const Mats<V> &M, con
 }
 
 template <int LOG2T, typename V, bool NUM>
-void launch_hash_t(unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows, int32_t *row_nnz,
-                   const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
-    constexpr int T = 1 << LOG2T;
-    constexpr int BLOCK = T <= 256 ? 64 : (T <= 512 ? 128 : (T <= 2048 ? 256 : (T <= 4096 ? 512 : 1024)));
-    hash_kernel<LOG2T, BLOCK, V, NUM><<<grid, BLOCK, 0, st>>>(M, rows, row_nnz, c_rp, c_col, c_val, ctrl);
+void launch_hash_t(unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows, int64_t ncols,
+                   int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
+    hash_kernel<LOG2T, V, NUM><<<grid, HashShape<LOG2T>::BLOCK, 0, st>>>(M, rows, ncols, row_nnz, c_rp, c_col,
+                                                                        c_val, ctrl);
 }
 
 template <typename V, bool NUM>
-void launch_hash(int log2t, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
+void launch_hash(int log2t, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows, int64_t ncols,
                  int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
+#define WS_HASH_CASE(L) \
+    case L: launch_hash_t<L, V, NUM>(grid, st, M, rows, ncols, row_nnz, c_rp, c_col, c_val, ctrl); break;
     switch (log2t) {
-        case 6: launch_hash_t<6, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 7: launch_hash_t<7, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 8: launch_hash_t<8, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 9: launch_hash_t<9, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 10: launch_hash_t<10, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 11: launch_hash_t<11, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 12: launch_hash_t<12, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 13: launch_hash_t<13, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        WS_HASH_CASE(6)
+        WS_HASH_CASE(7)
+        WS_HASH_CASE(8)
+        WS_HASH_CASE(9)
+        WS_HASH_CASE(10)
+        WS_HASH_CASE(11)
+        WS_HASH_CASE(12)
+        WS_HASH_CASE(13)
         default:
-            if constexpr (!NUM) launch_hash_t<14, V, NUM>(grid, st, M, rows, row_nnz, c_rp, c_col, c_val, ctrl);
+            if constexpr (!NUM) launch_hash_t<14, V, NUM>(grid, st, M, rows, ncols, row_nnz, c_rp, c_col, c_val, ctrl);
             break;
     }
+#undef WS_HASH_CASE
 }
 
 void launch_bitmap(int64_t ncols, unsigned grid, hipStream_t st, const Mats<float> &M, const int32_t *rows,
@@ -394,10 +396,14 @@ void launch_bitmap(int64_t ncols, unsigned grid, hipStream_t st, const Mats<floa
 
 template <typename V>
 void launch_dense(int wcols, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
-                  const int32_t *wtab, int nwin, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
-    if (wcols == 1024) dense_num_kernel<1024, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, c_rp, c_col, c_val, ctrl);
-    else if (wcols == 4096) dense_num_kernel<4096, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, c_rp, c_col, c_val, ctrl);
-    else dense_num_kernel<16384, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, c_rp, c_col, c_val, ctrl);
+                  const int32_t *wtab, int nwin, int64_t ncols, const int64_t *c_rp, int32_t *c_col, V *c_val,
+                  Control *ctrl) {
+    if (wcols == 1024)
+        dense_num_kernel<1024, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+    else if (wcols == 4096)
+        dense_num_kernel<4096, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+    else
+        dense_num_kernel<16384, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
 }
 
 // ---------------------------------------------------------------------------
@@ -432,7 +438,8 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
         const int32_t cnt = c.host.bin_count[b];
         if (!cnt) continue;
         launch_hash<float, false>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M,
-                                  perm + c.host.bin_offset[b], c.row_nnz, nullptr, nullptr, nullptr, c.ctrl);
+                                  perm + c.host.bin_offset[b], B->ncols, c.row_nnz, nullptr, nullptr, nullptr,
+                                  c.ctrl);
         stats.launches[WINGSPAN_TIER_HASH]++;
     }
     LAUNCH_CHECK("hash symbolic");
@@ -506,7 +513,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         const int32_t cnt = c.host.bin_count[b];
         if (!cnt) continue;
         launch_hash<V, true>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M, perm + c.host.bin_offset[b],
-                             nullptr, c_rp, c_col, c_val, c.ctrl);
+                             B->ncols, nullptr, c_rp, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_HASH]++;
     }
     LAUNCH_CHECK("hash numeric");
@@ -523,8 +530,8 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     // the dense tier's time covers its one kernel launch only
     if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     if (cnt) {
-        launch_dense<V>(c.o.wcols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.wtab, c.L.nwin, c_rp,
-                        c_col, c_val, c.ctrl);
+        launch_dense<V>(c.o.wcols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.wtab, c.L.nwin, B->ncols,
+                        c_rp, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense numeric");
     }
