@@ -248,6 +248,21 @@ __global__ void fill_i64(int64_t *p, int64_t n, int64_t v) {
     if (i < n) p[i] = v;
 }
 
+// Flags values that could produce a zero product: exact zeros, and (for
+// double) magnitudes below 2^-537, whose products with each other could
+// underflow to zero. float products are formed in double and cannot underflow.
+template <typename V>
+__global__ void __launch_bounds__(256) find_zero_values(const V *__restrict__ val, int64_t n, Control *ctrl) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    bool small = false;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const double v = static_cast<double>(val[i]);
+        const double a = v < 0 ? -v : v;
+        small |= sizeof(V) == 4 ? (a == 0.0) : !(a >= 0x1p-537);
+    }
+    if (__ballot(small) != 0ull && lane_id() == 0) atomicOr(&ctrl->has_zero_values, 1);
+}
+
 // ---------------------------------------------------------------------------
 // Column-window table of B: wtab[k*(nwin+1) + w] is the first entry of row k
 // with column >= w*wcols (w = nwin gives the row end). With it, the part of a

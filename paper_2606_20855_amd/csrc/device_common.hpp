@@ -41,6 +41,8 @@ struct Control {
     int64_t c_nnz;
     int32_t spill_next;
     int32_t error_flags;
+    int32_t has_zero_values;   // some A or B value could give a zero product
+    int32_t pad_;
     int32_t bin_count[kMaxBins];
     int32_t bin_offset[kMaxBins];
     int32_t bin_cursor[kMaxBins];
@@ -145,25 +147,79 @@ __host__ __device__ __forceinline__ int ceil_log2(int64_t x) {
     return l;
 }
 
+// ---------------------------------------------------------------------------
+// Wave-wide inclusive scans with DPP lane moves (row shifts within 16-lane
+// rows, then row broadcasts of lanes 15 and 31): VALU only, no LDS traffic.
+// ---------------------------------------------------------------------------
+constexpr int kDppRowShr1 = 0x111;
+constexpr int kDppRowShr2 = 0x112;
+constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+__device__ __forceinline__ int wave_incl_sum(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr1, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr2, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr4, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr8, 0xf, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowBcast15, 0xa, 0xf, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowBcast31, 0xc, 0xf, false);
+    return v;
+}
+
+// Inclusive max-scan of values >= -1 (identity -1).
+__device__ __forceinline__ int wave_incl_max(int v) {
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr1, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr2, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr4, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr8, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowBcast15, 0xa, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowBcast31, 0xc, 0xf, false));
+    return v;
+}
+
+// Orders a wave's LDS accesses to different addresses (compiler and hardware).
+__device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
+
+// Per-wave LDS scratch of kProductUnroll*64 ints used by for_each_product to
+// locate the A entry of every product. It must hold -1 everywhere before the
+// first call; for_each_product leaves it that way.
+constexpr int kProductUnroll = 2;
+constexpr int kMarkInts = kProductUnroll * kWave;
+
+// Sets this wave's mark array (kMarkInts ints) to -1.
+__device__ __forceinline__ void init_marks(int32_t *mark) {
+    for (int i = lane_id(); i < kMarkInts; i += kWave) mark[i] = -1;
+    wave_lds_fence();
+}
+
 // Visit every product a * b of a set of A entries [a_lo, a_hi) of one row.
 // `range(k)` gives the slice [x, y) of B's entry arrays that multiplies A
-// entry k (a whole row of B, or its part inside a column window).
+// entry k (a whole row of B, or its part inside column windows).
 //
-// The calling wave reads 64 A entries at a time, forms the prefix sum of their
-// slice lengths, and walks the flattened list of their products 64 at a time:
-// lane l of product block t handles product t*64 + l, locating its A entry by
-// binary search over the prefix sums held in the wave's lanes. Consecutive
-// lanes therefore read consecutive B entries whenever a slice is long, and no
-// lane idles on short slices. A workgroup of `nwaves` waves splits each chunk's
-// product blocks round-robin (wave `wave_rank` takes blocks rank, rank+nwaves,
-// ...), so every row is balanced across its waves whatever its B-row lengths.
+// The calling wave reads 64 A entries at a time and forms the prefix sum of
+// their slice lengths (lane l holds the first product index `excl` of its
+// entry). It then walks the flattened list of their products in blocks of 64:
+// lane j of a block starting at product `base` handles product base + j. The
+// entry owning product `base` is the highest non-empty lane with excl <= base
+// (one ballot); every entry starting inside the block writes its lane number
+// at its start offset in the wave's LDS mark array, and an inclusive max-scan
+// of the marks gives each lane its owner. Consecutive lanes therefore read
+// consecutive B entries whenever a slice is long, and no lane idles on short
+// slices. Each wave handles kProductUnroll blocks per step so that several
+// gathers are in flight. A workgroup of `nwaves` waves splits each chunk's
+// blocks round-robin, so every row is balanced across its waves whatever its
+// B-row lengths.
 template <typename V, bool VALUES, typename RangeF, typename Visit>
 __device__ __forceinline__ void for_each_product(const int32_t *__restrict__ a_col,
                                                  const V *__restrict__ a_val, int a_lo, int a_hi,
                                                  RangeF range, const int32_t *__restrict__ b_col,
                                                  const V *__restrict__ b_val, int wave_rank,
-                                                 int nwaves, Visit visit) {
+                                                 int nwaves, int32_t *mark, Visit visit) {
+    constexpr int U = kProductUnroll;
     const int ln = lane_id();
+    const int step = nwaves * kWave;
     for (int a0 = a_lo; a0 < a_hi; a0 += kWave) {
         const int a = a0 + ln;
         int bs = 0, len = 0;
@@ -174,23 +230,47 @@ __device__ __forceinline__ void for_each_product(const int32_t *__restrict__ a_c
             len = r.y - r.x;
             if (VALUES) av = to_d(a_val[a]);
         }
-        const int incl = group_incl_scan<kWave>(len);
-        const int tot = uniform(__shfl(incl, kWave - 1, kWave));
+        const int incl = wave_incl_sum(len);
+        const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
         const int excl = incl - len;
-        for (int p0 = wave_rank * kWave; p0 < tot; p0 += nwaves * kWave) {
-            const int p = p0 + ln;
-            const int q = p < tot ? p : tot - 1;
-            const int o = group_count_le<kWave>(incl, q);
-            const int bs_o = __shfl(bs, o, kWave);
-            const int ex_o = __shfl(excl, o, kWave);
-            double av_o = 0.0;
-            if (VALUES) av_o = __shfl(av, o, kWave);
-            if (p < tot) {
-                const int b = bs_o + (q - ex_o);
-                const int col = b_col[b];
-                double prod = 0.0;
-                if (VALUES) prod = av_o * to_d(b_val[b]);
-                visit(col, prod);
+        const int boff = bs - excl;   // B entry of product p of this entry is boff + p
+        for (int p0 = wave_rank * kWave; p0 < tot; p0 += U * step) {
+            int o[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int base = p0 + u * step;
+                if (len > 0 && excl > base && excl < base + kWave) mark[u * kWave + excl - base] = ln;
+            }
+            wave_lds_fence();
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int base = p0 + u * step;
+                const uint64_t before = __ballot(len > 0 && excl <= base);
+                const int ob = before ? 63 - __clzll(before) : 0;
+                int m = mark[u * kWave + ln];
+                mark[u * kWave + ln] = -1;
+                m = wave_incl_max(m);
+                o[u] = m > ob ? m : ob;
+            }
+            wave_lds_fence();
+            int bidx[U];
+            double aval[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                bidx[u] = __shfl(boff, o[u], kWave) + p0 + u * step + ln;
+                aval[u] = VALUES ? __shfl(av, o[u], kWave) : 0.0;
+            }
+            int col[U];
+            double bv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const bool live = p0 + u * step + ln < tot;
+                col[u] = live ? b_col[bidx[u]] : -1;
+                bv[u] = (VALUES && live) ? to_d(b_val[bidx[u]]) : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (col[u] >= 0) visit(col[u], VALUES ? aval[u] * bv[u] : 0.0);
             }
         }
     }

@@ -278,19 +278,22 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     __shared__ uint32_t bm[BWW > 0 ? BWW : 1];
     __shared__ int32_t goff[BWW > 0 ? BWW / 8 : 1];
     __shared__ int32_t scratch[NW];
+    __shared__ int32_t marks[NW * kMarkInts];
 
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < T; i += BLOCK) {
         keys[i] = kEmptyKey;
         if (NUM) vals[i] = 0.0;
     }
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
+    int32_t *mark = marks + wv * kMarkInts;
+    init_marks(mark);
     __syncthreads();
 
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
-    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int inserted = 0;
     bool overflow = false;
-    for_each_product<V, NUM>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
+    for_each_product<V, NUM>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW, mark,
                              [&](int col, double prod) {
                                  const int r = lds_insert<NUM>(keys, vals, LOG2T, col, prod);
                                  inserted += r > 0;
@@ -385,12 +388,15 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     constexpr int NW = BLOCK / kWave;
     __shared__ uint32_t bm[NWORDS];
     __shared__ int32_t scratch[NW];
+    __shared__ int32_t marks[NW * kMarkInts];
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
-    __syncthreads();
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
+    int32_t *mark = marks + wv * kMarkInts;
+    init_marks(mark);
+    __syncthreads();
     for_each_product<float, false>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1],
-                                   BRowRange{M.b_rp}, M.b_col, nullptr, wv, NW,
+                                   BRowRange{M.b_rp}, M.b_col, nullptr, wv, NW, mark,
                                    [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
     __syncthreads();
     int cnt = 0;
@@ -429,7 +435,7 @@ struct DenseShape {
     static_assert(TAIL_T * 12 + BWW * 4 <= WV * 8, "tail table and bitmap must fit in the window");
 };
 
-template <int WV, typename V>
+template <int WV, typename V, bool SENT>
 __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_t *__restrict__ rows,
                                                          const int32_t *__restrict__ wtab, int nwin,
                                                          int64_t ncols, const int64_t *__restrict__ c_rp,
@@ -439,11 +445,16 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
     constexpr int BLOCK = S::BLOCK;
     constexpr int NW = S::NW;
     constexpr int WWORDS = S::WCOLS / 32;
+    constexpr int NCH = S::WCOLS / kWave;            // 64-column chunks per wave
+    // SENT: slots start at -0.0 and a slot is occupied iff its bits differ
+    // from -0.0 (no product is zero, so no sum of products is -0.0); no bitmap.
+    constexpr uint64_t kNegZero = 0x8000000000000000ull;
     __shared__ double acc[WV];
-    __shared__ uint32_t bm[S::NWORDS];
+    __shared__ uint32_t bm[SENT ? 1 : S::NWORDS];
     __shared__ int32_t wave_cnt[NW];
     __shared__ int32_t goff[S::BWW / 8];
     __shared__ int32_t scratch[NW];
+    __shared__ int32_t marks[NW * kMarkInts];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -452,28 +463,39 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
+    int32_t *mark = marks + wv * kMarkInts;
+    init_marks(mark);
 
     int64_t out = 0;
     int w = 0;
     if (seg > S::TAIL_CAP) {
-        for (int i = threadIdx.x; i < WV; i += BLOCK) acc[i] = 0.0;
-        for (int i = threadIdx.x; i < S::NWORDS; i += BLOCK) bm[i] = 0u;
-        __syncthreads();
+        for (int i = threadIdx.x; i < WV; i += BLOCK) acc[i] = SENT ? __longlong_as_double(kNegZero) : 0.0;
+        if (!SENT)
+            for (int i = threadIdx.x; i < S::NWORDS; i += BLOCK) bm[i] = 0u;
     }
+    __syncthreads();
     for (; w < nwin && seg - out > S::TAIL_CAP; ++w) {
         const int w0 = w * WV;
         for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w}, M.b_col, M.b_val,
-                                  wv, NW, [&](int col, double prod) {
+                                  wv, NW, mark, [&](int col, double prod) {
                                       const int loc = col - w0;
                                       atomicAdd(&acc[loc], prod);
-                                      atomicOr(&bm[loc >> 5], 1u << (loc & 31));
+                                      if (!SENT) atomicOr(&bm[loc >> 5], 1u << (loc & 31));
                                   });
         __syncthreads();
         // each wave counts its slice, then emits it at its offset
         const int wbase = wv * S::WCOLS;
+        uint64_t occ[NCH];
         int cnt = 0;
-        for (int i = ln; i < WWORDS; i += kWave) cnt += __popc(bm[(wbase >> 5) + i]);
-        cnt = wave_sum(cnt);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int loc = wbase + c * kWave + ln;
+            bool set;
+            if (SENT) set = static_cast<uint64_t>(__double_as_longlong(acc[loc])) != kNegZero;
+            else set = (bm[loc >> 5] >> (loc & 31)) & 1u;
+            occ[c] = __ballot(set);
+            cnt += __popcll(occ[c]);
+        }
         if (ln == 0) wave_cnt[wv] = cnt;
         __syncthreads();
         int before = 0, wtot = 0;
@@ -483,21 +505,21 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
             wtot += x;
         }
         int64_t pos0 = out + uniform(before);
-        for (int c = 0; c < S::WCOLS / kWave; ++c) {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
             const int loc = wbase + c * kWave + ln;
-            const bool set = (bm[loc >> 5] >> (loc & 31)) & 1u;
-            const uint64_t bal = __ballot(set);
-            if (set) {
-                const int64_t pos = pos0 + __popcll(bal & ((1ull << ln) - 1ull));
+            if ((occ[c] >> ln) & 1ull) {
+                const int64_t pos = pos0 + __popcll(occ[c] & ((1ull << ln) - 1ull));
                 if (pos < seg) {
                     c_col[cb + pos] = w0 + loc;
                     c_val[cb + pos] = static_cast<V>(acc[loc]);
                 }
-                acc[loc] = 0.0;
+                acc[loc] = SENT ? __longlong_as_double(kNegZero) : 0.0;
             }
-            pos0 += __popcll(bal);
+            pos0 += __popcll(occ[c]);
         }
-        for (int i = ln; i < WWORDS; i += kWave) bm[(wbase >> 5) + i] = 0u;
+        if (!SENT)
+            for (int i = ln; i < WWORDS; i += kWave) bm[(wbase >> 5) + i] = 0u;
         out += uniform(wtot);
         __syncthreads();
     }
@@ -519,7 +541,7 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
         __syncthreads();
         bool overflow = false;
         for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w, nwin}, M.b_col,
-                                  M.b_val, wv, NW, [&](int col, double prod) {
+                                  M.b_val, wv, NW, mark, [&](int col, double prod) {
                                       overflow |= lds_insert<true>(tk, tv, log2t, col, prod) < 0;
                                   });
         if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
@@ -640,7 +662,7 @@ __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64
                                           int64_t ncols, int32_t *__restrict__ keys, double *__restrict__ vals,
                                           int32_t *__restrict__ row_nnz, const int64_t *__restrict__ c_rp,
                                           int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
-                                          int32_t *scratch, int32_t *s_keys, V *s_vals) {
+                                          int32_t *scratch, int32_t *s_keys, V *s_vals, int32_t *mark) {
     constexpr int BLOCK = kSpillBlock;
     constexpr int NW = BLOCK / kWave;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
@@ -667,7 +689,7 @@ __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64
     int inserted = 0;
     bool overflow = false;
     for_each_product<V, NUM>(
-        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW,
+        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW, mark,
         [&](int col, double prod) {
             uint32_t h = hash_slot(col, log2t);
             for (int64_t probe = 0; probe < T; ++probe) {
@@ -728,9 +750,12 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
     __shared__ int32_t scratch[NW];
     __shared__ int32_t s_keys[NUM ? kRunLen : 1];
     __shared__ V s_vals[NUM ? kRunLen : 1];
+    __shared__ int32_t marks[NW * kMarkInts];
 
     int32_t *keys = reinterpret_cast<int32_t *>(pool + static_cast<int64_t>(blockIdx.x) * slab_cap * 12);
     double *vals = reinterpret_cast<double *>(keys + slab_cap);
+    int32_t *mark = marks + uniform(static_cast<int>(threadIdx.x) / kWave) * kMarkInts;
+    init_marks(mark);
 
     // Rows are claimed one at a time from a shared counter until none are
     // left. The claimed index is read back into a scalar register so the loop
@@ -743,7 +768,7 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
         __syncthreads();
         if (ri >= nrows) break;
         spill_row<V, NUM>(M, rows[ri], pref, ncols, keys, vals, row_nnz, c_rp, c_col, c_val, ctrl, scratch,
-                          s_keys, s_vals);
+                          s_keys, s_vals, mark);
     }
 }
 

@@ -30,7 +30,7 @@ namespace {
 // ---------------------------------------------------------------------------
 constexpr int kHashLog2MaxSym = 14;           // 16K int32 keys = 64 KB of LDS
 constexpr int kHashLog2MaxNum = 13;           // 8K keys + 8K doubles = 96 KB of LDS
-constexpr int64_t kBitmapMaxCols = 38912 * 32; // 152 KB LDS bitmap
+constexpr int64_t kBitmapMaxCols = 36864 * 32; // 144 KB LDS bitmap (plus per-wave marks)
 constexpr int kMaxWindows = 128;              // dense numeric tier: windows per row
 constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
 constexpr int64_t kPoolBytes = int64_t(256) << 20;
@@ -189,6 +189,7 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
 // ---------------------------------------------------------------------------
 struct Ctx {
     hipStream_t st;
+    int dtype_f64 = -1;   // numeric value type: 1 double, 0 float, -1 unknown (symbolic)
     Opts o;
     Layout L;
     char *ws;
@@ -283,6 +284,19 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, bo
     if (!have_pref) {
         s = run_scan(c, BRowLenIn{A->col_idx, B->row_ptr}, A->nnz, c.pref);
         if (s != WINGSPAN_OK) return s;
+    }
+    if (numeric && c.dtype_f64 >= 0) {
+        const unsigned zb = 1024;
+        if (c.dtype_f64) {
+            find_zero_values<double><<<zb, 256, 0, c.st>>>(static_cast<const double *>(A->val), A->nnz, c.ctrl);
+            if (B->val != A->val)
+                find_zero_values<double><<<zb, 256, 0, c.st>>>(static_cast<const double *>(B->val), B->nnz, c.ctrl);
+        } else {
+            find_zero_values<float><<<zb, 256, 0, c.st>>>(static_cast<const float *>(A->val), A->nnz, c.ctrl);
+            if (B->val != A->val)
+                find_zero_values<float><<<zb, 256, 0, c.st>>>(static_cast<const float *>(B->val), B->nnz, c.ctrl);
+        }
+        LAUNCH_CHECK("find_zero_values");
     }
     BinCfg cfg{};
     cfg.ncols = B->ncols;
@@ -391,19 +405,29 @@ void launch_bitmap(int64_t ncols, unsigned grid, hipStream_t st, const Mats<floa
     else if (nwords <= 8192) bitmap_sym_kernel<8192, 512><<<grid, 512, 0, st>>>(M, rows, nwords, row_nnz);
     else if (nwords <= 16384) bitmap_sym_kernel<16384, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
     else if (nwords <= 32768) bitmap_sym_kernel<32768, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
-    else bitmap_sym_kernel<38912, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
+    else bitmap_sym_kernel<36864, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
+}
+
+template <int WV, typename V>
+void launch_dense_w(bool sentinel, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
+                    const int32_t *wtab, int nwin, int64_t ncols, const int64_t *c_rp, int32_t *c_col, V *c_val,
+                    Control *ctrl) {
+    if (sentinel)
+        dense_num_kernel<WV, V, true><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+    else
+        dense_num_kernel<WV, V, false><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
 }
 
 template <typename V>
-void launch_dense(int wcols, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
+void launch_dense(int wcols, bool sentinel, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
                   const int32_t *wtab, int nwin, int64_t ncols, const int64_t *c_rp, int32_t *c_col, V *c_val,
                   Control *ctrl) {
     if (wcols == 1024)
-        dense_num_kernel<1024, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+        launch_dense_w<1024, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
     else if (wcols == 4096)
-        dense_num_kernel<4096, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+        launch_dense_w<4096, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
     else
-        dense_num_kernel<16384, V><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+        launch_dense_w<16384, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
 }
 
 // ---------------------------------------------------------------------------
@@ -530,8 +554,8 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     // the dense tier's time covers its one kernel launch only
     if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     if (cnt) {
-        launch_dense<V>(c.o.wcols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.wtab, c.L.nwin, B->ncols,
-                        c_rp, c_col, c_val, c.ctrl);
+        launch_dense<V>(c.o.wcols, c.host.has_zero_values == 0, static_cast<unsigned>(cnt), c.st, M, perm + start,
+                        c.wtab, c.L.nwin, B->ncols, c_rp, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense numeric");
     }
@@ -650,6 +674,7 @@ static wingspan_status numeric_entry(const wingspan_csr *A, const wingspan_csr *
     if (!have_pref && (s = setup(c, A, B, options, workspace_dev, workspace_bytes, stream)) != WINGSPAN_OK)
         return s;
     if ((s = timer_begin(c.o.timing)) != WINGSPAN_OK) return s;
+    c.dtype_f64 = dtype == WINGSPAN_F64 ? 1 : 0;
     if (dtype == WINGSPAN_F32)
         s = numeric_impl<float>(c, A, B, c_row_ptr_dev, c_col_idx_dev, static_cast<float *>(c_val_dev), have_pref);
     else
