@@ -35,7 +35,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "numeric_dense_rmat18_traffic.md")
 KERNEL_NAMES = {
     "tiny": "wsp::tiny_kernel (numeric)",
     "hash": "wsp::hash_kernel (numeric)",
-    "dense": "wsp::dense_num_kernel",
+    "dense": "wsp::dense_rank_kernel",
     "spill": "wsp::spill_kernel (numeric)",
 }
 

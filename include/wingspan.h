@@ -82,7 +82,7 @@ typedef struct {
                                64..16384); longer rows use the dense or spill tier */
     int32_t force_spill;    /* 1: every row above the register tier uses the global
                                hash spill tier */
-    int32_t window_cols;    /* dense-window width in columns: 1024, 4096 or 16384 */
+    int32_t window_cols;    /* dense-window width in columns: 1024, 4096, 8192 or 16384 */
     int32_t tiny_max;       /* largest per-row product count handled by the
                                register-sort tier (8..64); -1 disables that tier */
     int32_t dense_min_nnz;  /* numeric: rows with at least this many output entries use

@@ -182,9 +182,9 @@ __device__ __forceinline__ int wave_incl_max(int v) {
 // Orders a wave's LDS accesses to different addresses (compiler and hardware).
 __device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 
-// Per-wave LDS scratch of kProductUnroll*64 ints used by for_each_product to
+// Per-wave LDS scratch of kProductUnroll*64 ints used by for_each_product_wg to
 // locate the A entry of every product. It must hold -1 everywhere before the
-// first call; for_each_product leaves it that way.
+// first call; for_each_product_wg leaves it that way.
 constexpr int kProductUnroll = 2;
 constexpr int kMarkInts = kProductUnroll * kWave;
 
@@ -194,85 +194,178 @@ __device__ __forceinline__ void init_marks(int32_t *mark) {
     wave_lds_fence();
 }
 
-// Visit every product a * b of a set of A entries [a_lo, a_hi) of one row.
-// `range(k)` gives the slice [x, y) of B's entry arrays that multiplies A
-// entry k (a whole row of B, or its part inside column windows).
+__device__ __forceinline__ double readlane_d(double x, int lane) {
+    const int lo = __builtin_amdgcn_readlane(__double2loint(x), lane);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), lane);
+    return __hiloint2double(hi, lo);
+}
+
+// Processes blocks [lb0, lb1) (block = 64 consecutive products) of one
+// 64-entry A chunk whose lanes hold (boff, av, len, incl): the shared body of
+// the product iterators. `mark` is this wave's LDS mark array (all -1).
 //
-// The calling wave reads 64 A entries at a time and forms the prefix sum of
-// their slice lengths (lane l holds the first product index `excl` of its
-// entry). It then walks the flattened list of their products in blocks of 64:
-// lane j of a block starting at product `base` handles product base + j. The
-// entry owning product `base` is the highest non-empty lane with excl <= base
-// (one ballot); every entry starting inside the block writes its lane number
-// at its start offset in the wave's LDS mark array, and an inclusive max-scan
-// of the marks gives each lane its owner. Consecutive lanes therefore read
-// consecutive B entries whenever a slice is long, and no lane idles on short
-// slices. Each wave handles kProductUnroll blocks per step so that several
-// gathers are in flight. A workgroup of `nwaves` waves splits each chunk's
-// blocks round-robin, so every row is balanced across its waves whatever its
-// B-row lengths.
-template <typename V, bool VALUES, typename RangeF, typename Visit>
-__device__ __forceinline__ void for_each_product(const int32_t *__restrict__ a_col,
-                                                 const V *__restrict__ a_val, int a_lo, int a_hi,
-                                                 RangeF range, const int32_t *__restrict__ b_col,
-                                                 const V *__restrict__ b_val, int wave_rank,
-                                                 int nwaves, int32_t *mark, Visit visit) {
+// A block whose first and last products belong to the same entry (the
+// common case on long B slices) takes that entry's data from scalar
+// registers; only blocks that straddle entries run the mark/max-scan lookup.
+template <typename V, bool VALUES, typename Visit>
+__device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int incl, int tot, int lb0, int lb1,
+                                             const int32_t *__restrict__ b_col, const V *__restrict__ b_val,
+                                             int32_t *mark, Visit visit) {
     constexpr int U = kProductUnroll;
     const int ln = lane_id();
-    const int step = nwaves * kWave;
-    for (int a0 = a_lo; a0 < a_hi; a0 += kWave) {
-        const int a = a0 + ln;
-        int bs = 0, len = 0;
-        double av = 0.0;
-        if (a < a_hi) {
-            const int2 r = range(a_col[a]);
-            bs = r.x;
-            len = r.y - r.x;
-            if (VALUES) av = to_d(a_val[a]);
+    const int excl = incl - len;
+    for (int lb = lb0; lb < lb1; lb += U) {
+        int ob[U];
+        bool fast = true;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int base = (lb + u) * kWave;
+            const uint64_t before = __ballot(len > 0 && excl <= base);
+            ob[u] = before ? 63 - __clzll(before) : 0;
+            const int last = (base + kWave < tot ? base + kWave : tot) - 1;
+            fast = fast && (lb + u >= lb1 || __builtin_amdgcn_readlane(incl, ob[u]) > last);
         }
-        const int incl = wave_incl_sum(len);
-        const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
-        const int excl = incl - len;
-        const int boff = bs - excl;   // B entry of product p of this entry is boff + p
-        for (int p0 = wave_rank * kWave; p0 < tot; p0 += U * step) {
-            int o[U];
+        int bidx[U];
+        double aval[U];
+        if (fast) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int base = p0 + u * step;
+                bidx[u] = __builtin_amdgcn_readlane(boff, ob[u]) + (lb + u) * kWave + ln;
+                aval[u] = VALUES ? readlane_d(av, ob[u]) : 0.0;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int base = (lb + u) * kWave;
                 if (len > 0 && excl > base && excl < base + kWave) mark[u * kWave + excl - base] = ln;
             }
             wave_lds_fence();
+            int o[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int base = p0 + u * step;
-                const uint64_t before = __ballot(len > 0 && excl <= base);
-                const int ob = before ? 63 - __clzll(before) : 0;
                 int m = mark[u * kWave + ln];
                 mark[u * kWave + ln] = -1;
                 m = wave_incl_max(m);
-                o[u] = m > ob ? m : ob;
+                o[u] = m > ob[u] ? m : ob[u];
             }
             wave_lds_fence();
-            int bidx[U];
-            double aval[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                bidx[u] = __shfl(boff, o[u], kWave) + p0 + u * step + ln;
+                bidx[u] = __shfl(boff, o[u], kWave) + (lb + u) * kWave + ln;
                 aval[u] = VALUES ? __shfl(av, o[u], kWave) : 0.0;
             }
-            int col[U];
-            double bv[U];
+        }
+        int col[U];
+        double bv[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const bool live = p0 + u * step + ln < tot;
-                col[u] = live ? b_col[bidx[u]] : -1;
-                bv[u] = (VALUES && live) ? to_d(b_val[bidx[u]]) : 0.0;
+        for (int u = 0; u < U; ++u) {
+            const bool live = lb + u < lb1 && (lb + u) * kWave + ln < tot;
+            col[u] = live ? b_col[bidx[u]] : -1;
+            bv[u] = (VALUES && live) ? to_d(b_val[bidx[u]]) : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (col[u] >= 0) visit(col[u], VALUES ? aval[u] * bv[u] : 0.0);
+        }
+    }
+}
+
+// Visits every product a * b of A entries [a_lo, a_hi) of one row: visit(col,
+// prod) with col = B.col_idx[b] and prod = A.val[a] * B.val[b] formed in double
+// (0 when VALUES is false). `range(k)` gives the slice [x, y) of B's entry
+// arrays that multiplies A entry k (a whole row of B, or its part inside
+// column windows).
+//
+// Products are flattened per 64-entry chunk of A: lane l of a chunk holds the
+// prefix sum of slice lengths, and block t of the chunk covers products
+// 64t .. 64t+63, lane j of the block taking product 64t + j. Consecutive lanes
+// therefore read consecutive B entries whenever a slice is long, and no lane
+// idles on short slices. Entries are taken in groups of
+// up to kMaxChunks chunks of 64. For each group:
+//   1. wave w measures chunks w, w+NW, ...: its count of 64-product blocks;
+//   2. one wave scans the counts into block offsets (ctot, in LDS);
+//   3. wave w takes the contiguous block range [w*nb/NW, (w+1)*nb/NW) and
+//      loads only the chunks that range touches.
+// Every wave thus reads about 2/NW of the chunks instead of all of them, and
+// the products are split evenly. All threads of the workgroup must call it.
+// ctot holds kMaxChunks + 1 ints of LDS.
+constexpr int kMaxChunks = 256;
+
+template <int BLOCK, typename V, bool VALUES, typename RangeF, typename Visit>
+__device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ a_col,
+                                                    const V *__restrict__ a_val, int a_lo, int a_hi,
+                                                    RangeF range, const int32_t *__restrict__ b_col,
+                                                    const V *__restrict__ b_val, int32_t *mark, int32_t *ctot,
+                                                    Visit visit) {
+    constexpr int NW = BLOCK / kWave;
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
+    const int ln = lane_id();
+    for (int g0 = a_lo; g0 < a_hi; g0 += kMaxChunks * kWave) {
+        const int g1 = (a_hi - g0) < kMaxChunks * kWave ? a_hi : g0 + kMaxChunks * kWave;
+        const int nch = (g1 - g0 + kWave - 1) / kWave;
+        // 1. blocks per chunk
+        for (int c = wv; c < nch; c += NW) {
+            const int a = g0 + c * kWave + ln;
+            int len = 0;
+            if (a < g1) {
+                const int2 r = range(a_col[a]);
+                len = r.y - r.x;
             }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (col[u] >= 0) visit(col[u], VALUES ? aval[u] * bv[u] : 0.0);
+            const int tot = __builtin_amdgcn_readlane(wave_incl_sum(len), kWave - 1);
+            if (ln == 0) ctot[c] = (tot + kWave - 1) / kWave;
+        }
+        __syncthreads();
+        // 2. exclusive scan of the block counts; ctot[nch] = total blocks
+        if (wv == 0) {
+            int carry = 0;
+            for (int c0 = 0; c0 < nch; c0 += kWave) {
+                const int c = c0 + ln;
+                const int v = c < nch ? ctot[c] : 0;
+                const int inc = wave_incl_sum(v);
+                if (c < nch) ctot[c] = carry + inc - v;
+                carry += __builtin_amdgcn_readlane(inc, kWave - 1);
+            }
+            if (ln == 0) ctot[nch] = carry;
+        }
+        __syncthreads();
+        // 3. this wave's share of the blocks
+        const int nb = uniform(ctot[nch]);
+        const int b0 = static_cast<int>(static_cast<int64_t>(nb) * wv / NW);
+        const int b1 = static_cast<int>(static_cast<int64_t>(nb) * (wv + 1) / NW);
+        if (b0 < b1) {
+            // last chunk whose first block is <= b0
+            int lo = 0, hi = nch - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (uniform(ctot[mid]) <= b0) lo = mid;
+                else hi = mid - 1;
+            }
+            int c = lo;
+            int b = b0;
+            while (b < b1) {
+                const int cb0 = uniform(ctot[c]);
+                const int cb1 = uniform(ctot[c + 1]);
+                if (cb1 > b) {
+                    const int a = g0 + c * kWave + ln;
+                    int bs = 0, len = 0;
+                    double av = 0.0;
+                    if (a < g1) {
+                        const int2 r = range(a_col[a]);
+                        bs = r.x;
+                        len = r.y - r.x;
+                        if (VALUES) av = to_d(a_val[a]);
+                    }
+                    const int incl = wave_incl_sum(len);
+                    const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
+                    const int e = cb1 < b1 ? cb1 : b1;
+                    chunk_blocks<V, VALUES>(bs - (incl - len), av, len, incl, tot, b - cb0, e - cb0, b_col, b_val,
+                                            mark, visit);
+                    b = e;
+                }
+                ++c;
             }
         }
+        __syncthreads();
     }
 }
 

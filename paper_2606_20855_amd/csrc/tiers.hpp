@@ -279,6 +279,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     __shared__ int32_t goff[BWW > 0 ? BWW / 8 : 1];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t ctot[kMaxChunks + 1];
 
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < T; i += BLOCK) {
@@ -293,8 +294,8 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
     int inserted = 0;
     bool overflow = false;
-    for_each_product<V, NUM>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW, mark,
-                             [&](int col, double prod) {
+    for_each_product_wg<BLOCK, V, NUM>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, mark,
+                                       ctot, [&](int col, double prod) {
                                  const int r = lds_insert<NUM>(keys, vals, LOG2T, col, prod);
                                  inserted += r > 0;
                                  overflow |= r < 0;
@@ -389,15 +390,16 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     __shared__ uint32_t bm[NWORDS];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t ctot[kMaxChunks + 1];
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
     __syncthreads();
-    for_each_product<float, false>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1],
-                                   BRowRange{M.b_rp}, M.b_col, nullptr, wv, NW, mark,
-                                   [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
+    for_each_product_wg<BLOCK, float, false>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1], BRowRange{M.b_rp},
+                                             M.b_col, nullptr, mark, ctot,
+                                             [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
     __syncthreads();
     int cnt = 0;
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) cnt += __popc(bm[i]);
@@ -423,20 +425,22 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
 // ---------------------------------------------------------------------------
 template <int WV>
 struct DenseShape {
-    static constexpr int BLOCK = 1024;
+    // smaller windows use smaller workgroups so more of them share a CU
+    static constexpr int BLOCK = WV >= 8192 ? 1024 : (WV >= 4096 ? 512 : 256);
     static constexpr int NW = BLOCK / kWave;
     static constexpr int NWORDS = WV / 32;
     static constexpr int WCOLS = WV / NW;            // columns each wave emits
-    static constexpr int TAIL_LOG2 = 0 + (WV == 16384 ? 13 : (WV == 4096 ? 11 : 9));
-    static constexpr int TAIL_T = 1 << TAIL_LOG2;    // tail table slots (12 B each)
+    static constexpr int TAIL_T = WV / 2;            // tail table slots (12 B each)
+    static constexpr int TAIL_LOG2 = WV == 16384 ? 13 : (WV == 8192 ? 12 : (WV == 4096 ? 11 : 9));
     static constexpr int TAIL_CAP = (TAIL_T * 2) / 3;
     static constexpr int BWW = WV / 2;               // tail rank bitmap words
     static_assert(WCOLS % kWave == 0, "window must split into 64-column chunks per wave");
     static_assert(TAIL_T * 12 + BWW * 4 <= WV * 8, "tail table and bitmap must fit in the window");
+    static_assert((1 << TAIL_LOG2) == TAIL_T, "tail table size");
 };
 
 template <int WV, typename V, bool SENT>
-__global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_t *__restrict__ rows,
+__global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V> M, const int32_t *__restrict__ rows,
                                                          const int32_t *__restrict__ wtab, int nwin,
                                                          int64_t ncols, const int64_t *__restrict__ c_rp,
                                                          int32_t *__restrict__ c_col,
@@ -455,6 +459,7 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
     __shared__ int32_t goff[S::BWW / 8];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t ctot[kMaxChunks + 1];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -476,8 +481,8 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
     __syncthreads();
     for (; w < nwin && seg - out > S::TAIL_CAP; ++w) {
         const int w0 = w * WV;
-        for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w}, M.b_col, M.b_val,
-                                  wv, NW, mark, [&](int col, double prod) {
+        for_each_product_wg<BLOCK, V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w}, M.b_col,
+                                            M.b_val, mark, ctot, [&](int col, double prod) {
                                       const int loc = col - w0;
                                       atomicAdd(&acc[loc], prod);
                                       if (!SENT) atomicOr(&bm[loc >> 5], 1u << (loc & 31));
@@ -508,6 +513,7 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int loc = wbase + c * kWave + ln;
+            if (occ[c] == 0ull) continue;
             if ((occ[c] >> ln) & 1ull) {
                 const int64_t pos = pos0 + __popcll(occ[c] & ((1ull << ln) - 1ull));
                 if (pos < seg) {
@@ -540,14 +546,209 @@ __global__ void __launch_bounds__(1024) dense_num_kernel(Mats<V> M, const int32_
         }
         __syncthreads();
         bool overflow = false;
-        for_each_product<V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w, nwin}, M.b_col,
-                                  M.b_val, wv, NW, mark, [&](int col, double prod) {
+        for_each_product_wg<BLOCK, V, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, w, nwin},
+                                            M.b_col, M.b_val, mark, ctot, [&](int col, double prod) {
                                       overflow |= lds_insert<true>(tk, tv, log2t, col, prod) < 0;
                                   });
         if (overflow) atomicOr(&ctrl->error_flags, kErrProbeExhausted);
         __syncthreads();
         out = rank_emit<BLOCK, S::BWW, V>(tk, tv, T, static_cast<int64_t>(w) * WV, ncols, tbm, goff, scratch,
                                           c_col, c_val, cb, out, seg);
+    }
+    if (threadIdx.x == 0 && out != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+}
+
+// ---------------------------------------------------------------------------
+// Dense tier, numeric, rank-indexed (default when ncols <= 128 * 8192).
+//
+// The row is processed in regions of REGION_COLS columns. For a region:
+//  1. a structure pass marks every column the row touches in an LDS bitmap;
+//  2. each bitmap word gets the exclusive popcount prefix of the words before
+//     it, stored beside its bits (one 64-bit LDS read then gives any column's
+//     rank among the row's entries in the region);
+//  3. the region's ranks are taken in slices of at most CAP entries that end
+//     on 8192-column window boundaries where possible; for each slice the
+//     values of the products whose columns fall in it are accumulated into a
+//     dense LDS array indexed by rank (no hash, no probing), then the slice is
+//     staged in rank order (column beside value) and copied to C with
+//     coalesced stores.
+// Most rows need one region and one or two slices; the accumulator holds
+// entries, not columns, so sparse stretches of columns cost nothing. The
+// window table (8192-column windows) gives each B row's part inside a range
+// of windows.
+// ---------------------------------------------------------------------------
+constexpr int kRankWinCols = 8192;
+
+// Shape: 1024 threads, regions of 8192 bitmap words (262144 columns), and a
+// rank accumulator of CAP doubles. With float output a staged entry (column,
+// value) packs into its own 8-byte accumulator slot; double output stages the
+// columns in an array of their own, so its accumulator is smaller.
+template <typename V>
+struct RankShape {
+    static constexpr int BLOCK = 1024;
+    static constexpr int REGION_WORDS = 8192;
+    static constexpr int REGION_COLS = REGION_WORDS * 32;
+    static constexpr int REGION_WINS = REGION_COLS / kRankWinCols;
+    static constexpr bool PACKED = sizeof(V) == 4;
+    static constexpr int CAP = PACKED ? 10240 : 7168;
+    static constexpr int STAGE = PACKED ? 1 : CAP;   // separate column stage (ints)
+    static_assert(REGION_COLS % kRankWinCols == 0, "regions hold whole windows");
+    static_assert(REGION_WORDS % (BLOCK / kWave * kWave) == 0, "prefix scan takes whole word rows per wave");
+};
+
+template <typename V>
+__global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
+    Mats<V> M, const int32_t *__restrict__ rows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
+    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl) {
+    using SH = RankShape<V>;
+    constexpr int BLOCK = SH::BLOCK;
+    constexpr int NW = BLOCK / kWave;
+    constexpr int RW = SH::REGION_WORDS;
+    constexpr int WROWS = RW / NW / kWave;   // 64-word rows per wave in the prefix scan
+    constexpr int WIN_WORDS = kRankWinCols / 32;
+    constexpr int CAP = SH::CAP;
+    __shared__ uint2 bw[RW];                 // x: column bits, y: exclusive prefix within the region
+    __shared__ double acc[CAP];
+    __shared__ int32_t stage[SH::STAGE];
+    __shared__ int32_t scratch[NW];
+    __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t ctot[kMaxChunks + 1];
+
+    const int row = rows[blockIdx.x];
+    const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
+    const int64_t cb = c_rp[row];
+    const int64_t seg = c_rp[row + 1] - cb;
+    const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
+    const int ln = lane_id();
+    const int64_t stride = static_cast<int64_t>(nwin) + 1;
+    int32_t *mark = marks + wv * kMarkInts;
+    init_marks(mark);
+    for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
+
+    int64_t out = 0;   // entries of the row emitted in earlier regions
+    for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
+        const int rg1 = nwin - rg0 < SH::REGION_WINS ? nwin : rg0 + SH::REGION_WINS;
+        const int64_t col0 = static_cast<int64_t>(rg0) * kRankWinCols;
+        const int ncw = static_cast<int>(ncols - col0 < SH::REGION_COLS ? ncols - col0 : SH::REGION_COLS);
+        const int nwords = (ncw + 31) >> 5;
+        for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
+        __syncthreads();
+        // 1. structure
+        for_each_product_wg<BLOCK, V, false>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0, rg1},
+                                             M.b_col, M.b_val, mark, ctot, [&](int col, double) {
+                                                 const int rel = static_cast<int>(col - col0);
+                                                 atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
+                                             });
+        // 2. exclusive popcount prefix: wave w owns words [w*RW/NW, (w+1)*RW/NW), read one 64-word row at a
+        //    time (lane-contiguous, so free of bank conflicts)
+        {
+            const int wbase = wv * (RW / NW);
+            uint32_t cnt[WROWS];
+            int wtot = 0;
+#pragma unroll
+            for (int q = 0; q < WROWS; ++q) {
+                cnt[q] = __popc(bw[wbase + q * kWave + ln].x);
+                wtot += static_cast<int>(cnt[q]);
+            }
+            wtot = __builtin_amdgcn_readlane(wave_incl_sum(wtot), kWave - 1);
+            if (ln == 0) scratch[wv] = wtot;
+            __syncthreads();
+            int run = 0;
+#pragma unroll
+            for (int i = 0; i < NW; ++i) run += i < wv ? scratch[i] : 0;
+#pragma unroll
+            for (int q = 0; q < WROWS; ++q) {
+                const int inc = wave_incl_sum(static_cast<int>(cnt[q]));
+                bw[wbase + q * kWave + ln].y = static_cast<uint32_t>(run + inc - static_cast<int>(cnt[q]));
+                run += __builtin_amdgcn_readlane(inc, kWave - 1);
+            }
+        }
+        int region_total = 0;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) region_total += scratch[i];
+        region_total = uniform(region_total);
+        __syncthreads();
+        // 3. rank slices: whole windows while they fit CAP entries; a window
+        //    denser than CAP is taken in slices of CAP ranks
+        auto rank_at_window = [&](int jw) -> int {
+            return jw * WIN_WORDS < nwords ? uniform(static_cast<int>(bw[jw * WIN_WORDS].y)) : region_total;
+        };
+        const int nwr = rg1 - rg0;
+        int j = 0;
+        int r0 = 0;   // first rank of the current slice
+        while (j < nwr) {
+            int j2 = j + 1;
+            while (j2 < nwr && rank_at_window(j2 + 1) - r0 <= CAP) ++j2;
+            const int rend_w = rank_at_window(j2);
+            const int r1 = rend_w - r0 > CAP ? r0 + CAP : rend_w;    // this slice covers ranks [r0, r1)
+            // values
+            for_each_product_wg<BLOCK, V, true>(M.a_col, M.a_val, a_lo, a_hi,
+                                                BWindowRange{wtab, stride, rg0 + j, rg0 + j2}, M.b_col, M.b_val,
+                                                mark, ctot, [&](int col, double prod) {
+                                                    const int rel = static_cast<int>(col - col0);
+                                                    const uint2 e = bw[rel >> 5];
+                                                    const int r = static_cast<int>(e.y) +
+                                                                  __popc(e.x & ((1u << (rel & 31)) - 1u));
+                                                    if (r >= r0 && r < r1) atomicAdd(&acc[r - r0], prod);
+                                                });
+            // stage ranks [r0, r1) in rank order: each wave a contiguous run of the windows' words, one word
+            // per lane; a lane walks its word's set bits (the wave loops while any lane still holds one), so
+            // the cost follows the entries, not the columns. Every rank is staged by exactly one lane.
+            const int wa = j * WIN_WORDS;
+            const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
+            const int w0w = wa + static_cast<int>(static_cast<int64_t>(wb - wa) * wv / NW);
+            const int w1w = wa + static_cast<int>(static_cast<int64_t>(wb - wa) * (wv + 1) / NW);
+            for (int wbase = w0w; wbase < w1w; wbase += kWave) {
+                const int wd = wbase + ln;
+                uint2 e = wd < w1w ? bw[wd] : make_uint2(0u, 0u);
+                uint32_t wbits = e.x;
+                int r = static_cast<int>(e.y);
+                // drop the entries below r0
+                while (wbits != 0u && r < r0) {
+                    wbits &= wbits - 1u;
+                    ++r;
+                }
+                while (__ballot(wbits != 0u && r < r1) != 0ull) {
+                    if (wbits != 0u && r < r1) {
+                        const int b = __builtin_ctz(wbits);
+                        wbits &= wbits - 1u;
+                        const int32_t colv = static_cast<int32_t>(col0 + wd * 32 + b);
+                        if constexpr (SH::PACKED) {
+                            const float v = static_cast<float>(acc[r - r0]);
+                            reinterpret_cast<uint2 *>(acc)[r - r0] = make_uint2(static_cast<uint32_t>(colv),
+                                                                                __float_as_uint(v));
+                        } else {
+                            stage[r - r0] = colv;
+                        }
+                        ++r;
+                    }
+                }
+            }
+            __syncthreads();
+            // copy the slice to C with coalesced stores, clearing the accumulator
+            const int64_t pbase = out + r0;
+            for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
+                int32_t colv;
+                V v;
+                if constexpr (SH::PACKED) {
+                    const uint2 e = reinterpret_cast<const uint2 *>(acc)[i];
+                    colv = static_cast<int32_t>(e.x);
+                    v = static_cast<V>(__uint_as_float(e.y));
+                } else {
+                    colv = stage[i];
+                    v = static_cast<V>(acc[i]);
+                }
+                acc[i] = 0.0;
+                if (pbase + i < seg) {
+                    c_col[cb + pbase + i] = colv;
+                    c_val[cb + pbase + i] = v;
+                }
+            }
+            __syncthreads();
+            r0 = r1;
+            if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
+        }
+        out += region_total;
     }
     if (threadIdx.x == 0 && out != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
 }
@@ -662,7 +863,8 @@ __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64
                                           int64_t ncols, int32_t *__restrict__ keys, double *__restrict__ vals,
                                           int32_t *__restrict__ row_nnz, const int64_t *__restrict__ c_rp,
                                           int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
-                                          int32_t *scratch, int32_t *s_keys, V *s_vals, int32_t *mark) {
+                                          int32_t *scratch, int32_t *s_keys, V *s_vals, int32_t *mark,
+                                          int32_t *ctot) {
     constexpr int BLOCK = kSpillBlock;
     constexpr int NW = BLOCK / kWave;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
@@ -688,8 +890,8 @@ __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64
 
     int inserted = 0;
     bool overflow = false;
-    for_each_product<V, NUM>(
-        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, wv, NW, mark,
+    for_each_product_wg<BLOCK, V, NUM>(
+        M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col, M.b_val, mark, ctot,
         [&](int col, double prod) {
             uint32_t h = hash_slot(col, log2t);
             for (int64_t probe = 0; probe < T; ++probe) {
@@ -751,6 +953,7 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
     __shared__ int32_t s_keys[NUM ? kRunLen : 1];
     __shared__ V s_vals[NUM ? kRunLen : 1];
     __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t ctot[kMaxChunks + 1];
 
     int32_t *keys = reinterpret_cast<int32_t *>(pool + static_cast<int64_t>(blockIdx.x) * slab_cap * 12);
     double *vals = reinterpret_cast<double *>(keys + slab_cap);
@@ -768,7 +971,7 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
         __syncthreads();
         if (ri >= nrows) break;
         spill_row<V, NUM>(M, rows[ri], pref, ncols, keys, vals, row_nnz, c_rp, c_col, c_val, ctrl, scratch,
-                          s_keys, s_vals, mark);
+                          s_keys, s_vals, mark, ctot);
     }
 }
 

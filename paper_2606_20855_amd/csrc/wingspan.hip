@@ -81,6 +81,7 @@ struct Opts {
     int hash_log2_max_sym = kHashLog2MaxSym;
     int hash_log2_max_num = kHashLog2MaxNum;
     int wcols = kDefaultWindow;
+    bool wcols_explicit = false;   // window_cols given: use the column-window dense kernel
     int tiny_max = 64;
     int64_t dense_min_nnz = INT64_MAX;
 };
@@ -104,10 +105,12 @@ wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
             r.hash_log2_max_num = std::min(r.hash_log2_max_num, l);
         }
         if (o->window_cols != 0) {
-            if (o->window_cols != 1024 && o->window_cols != 4096 && o->window_cols != 16384)
+            if (o->window_cols != 1024 && o->window_cols != 4096 && o->window_cols != 8192 &&
+                o->window_cols != 16384)
                 return fail(WINGSPAN_ERR_INVALID_ARGUMENT,
-                            "options->window_cols must be 1024, 4096 or 16384, got %d", o->window_cols);
+                            "options->window_cols must be 1024, 4096, 8192 or 16384, got %d", o->window_cols);
             r.wcols = o->window_cols;
+            r.wcols_explicit = true;
         }
         if (o->tiny_max != 0) {
             if (o->tiny_max == -1) r.tiny_max = 0;
@@ -152,6 +155,8 @@ wingspan_status check_pair(const wingspan_csr *A, const wingspan_csr *B) {
 struct Layout {
     size_t off_ctrl, off_pref, off_row_nnz, off_perm, off_partials, off_wtab, off_pool, total;
     int nwin;          // numeric dense windows per row (0: dense numeric tier unavailable)
+    int wcols;         // columns per window of the window table
+    bool rank_mode;    // dense numeric rows use the rank-indexed kernel
     int64_t slab_cap;  // spill slab slots
     int nslab;
 };
@@ -172,7 +177,14 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
     const int64_t tiles = (std::max<int64_t>(nnz_a, m + 1) + kScanTile - 1) / kScanTile + 2;
     off += align_up(sizeof(int64_t) * tiles);
     L.off_wtab = off;
-    const int64_t nwin = n > 0 ? (n + o.wcols - 1) / o.wcols : 1;
+    auto windows = [n](int64_t w) { return n > 0 ? (n + w - 1) / w : int64_t(1); };
+    L.rank_mode = false;
+    L.wcols = o.wcols;
+    if (!o.wcols_explicit && windows(kRankWinCols) <= kMaxWindows) {
+        L.rank_mode = true;
+        L.wcols = kRankWinCols;
+    }
+    const int64_t nwin = windows(L.wcols);
     L.nwin = (!o.dense_disabled && nwin <= kMaxWindows) ? static_cast<int>(nwin) : 0;
     if (L.nwin > 0) off += align_up(sizeof(int32_t) * B->nrows * (L.nwin + 1) + sizeof(int32_t));
     L.off_pool = off;
@@ -412,10 +424,11 @@ template <int WV, typename V>
 void launch_dense_w(bool sentinel, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
                     const int32_t *wtab, int nwin, int64_t ncols, const int64_t *c_rp, int32_t *c_col, V *c_val,
                     Control *ctrl) {
+    constexpr int BLOCK = DenseShape<WV>::BLOCK;
     if (sentinel)
-        dense_num_kernel<WV, V, true><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+        dense_num_kernel<WV, V, true><<<grid, BLOCK, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
     else
-        dense_num_kernel<WV, V, false><<<grid, 1024, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+        dense_num_kernel<WV, V, false><<<grid, BLOCK, 0, st>>>(M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
 }
 
 template <typename V>
@@ -426,6 +439,8 @@ void launch_dense(int wcols, bool sentinel, unsigned grid, hipStream_t st, const
         launch_dense_w<1024, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
     else if (wcols == 4096)
         launch_dense_w<4096, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
+    else if (wcols == 8192)
+        launch_dense_w<8192, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
     else
         launch_dense_w<16384, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
 }
@@ -548,13 +563,18 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt) {
         const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
         build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows, c.L.nwin,
-                                                                       c.o.wcols, c.wtab);
+                                                                       c.L.wcols, c.wtab);
         LAUNCH_CHECK("build_window_table");
     }
     // the dense tier's time covers its one kernel launch only
     if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
-    if (cnt) {
-        launch_dense<V>(c.o.wcols, c.host.has_zero_values == 0, static_cast<unsigned>(cnt), c.st, M, perm + start,
+    if (cnt && c.L.rank_mode) {
+        dense_rank_kernel<V><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+            M, perm + start, c.wtab, c.L.nwin, B->ncols, c_rp, c_col, c_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_DENSE]++;
+        LAUNCH_CHECK("dense rank numeric");
+    } else if (cnt) {
+        launch_dense<V>(c.L.wcols, c.host.has_zero_values == 0, static_cast<unsigned>(cnt), c.st, M, perm + start,
                         c.wtab, c.L.nwin, B->ncols, c_rp, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense numeric");

@@ -71,7 +71,10 @@ TIER_OPTS = {
     "hash_small": dict(tiny_max=-1, max_lds_slots=256, dense_min_nnz=-1),
     "dense_w1024": dict(tiny_max=-1, max_lds_slots=64, window_cols=1024),
     "dense_w4096": dict(tiny_max=-1, max_lds_slots=64, window_cols=4096),
+    "dense_w8192": dict(tiny_max=-1, max_lds_slots=64, window_cols=8192),
     "dense_pref": dict(dense_min_nnz=1, window_cols=1024),
+    "dense_rank": dict(tiny_max=-1, max_lds_slots=64),
+    "dense_rank_pref": dict(dense_min_nnz=1),
     "spill": dict(tiny_max=-1, force_spill=1),
     "spill_tiny": dict(force_spill=1),
     "validate": dict(validate=1),
@@ -135,10 +138,14 @@ def test_identity_and_permutation_bit_exact(dtype):
         assert np.array_equal(got.val[got.row_ptr[i]:got.row_ptr[i + 1]], v)
 
 
-@pytest.mark.parametrize("opts", [None, dict(max_lds_slots=64, window_cols=1024), dict(force_spill=1)])
-def test_arrowhead_dense_square(opts):
-    n = 4096
-    A = matgen.arrowhead(n)
+@pytest.mark.parametrize("n,opts,dtype", [(4096, None, np.float64),
+                                          (4096, dict(max_lds_slots=64, window_cols=1024), np.float64),
+                                          (4096, dict(force_spill=1), np.float64), (12288, None, np.float64),
+                                          (12288, None, np.float32), (12288, dict(window_cols=4096), np.float64)])
+def test_arrowhead_dense_square(n, opts, dtype):
+    # n = 12288: every row has 12288 entries, 8192 of them in the first
+    # 8192-column window; with double output that window takes two rank slices
+    A = matgen.arrowhead(n, dtype)
     got, _, _ = run_gpu(A, A, opts)
     assert got.row_ptr[-1] == n * n
     rp = got.row_ptr
@@ -151,6 +158,29 @@ def test_arrowhead_dense_square(opts):
     E[np.arange(n), np.arange(n)] = 2
     E[0, 0] = n
     assert np.array_equal(C, E)
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+@pytest.mark.parametrize("opts", [None, dict(dense_min_nnz=1)])
+def test_dense_rows_across_regions(dtype, opts):
+    # rows of ~12K entries spread over 600K columns: several 262144-column
+    # regions and several super-windows per row in the rank-indexed kernel
+    A = matgen.er(48, 2000, 200, seed=31, dtype=dtype, dist="pm1" if dtype == np.float64 else "open01")
+    B = matgen.er(2000, 600_000, 60, seed=32, dtype=dtype, dist="pm1" if dtype == np.float64 else "open01")
+    got, sym, num, ref = check(A, B, opts, what="regions")
+    assert num["rows"]["dense"] > 0
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_rank_slices_inside_one_window(dtype):
+    # ~8,600 entries per row, ~7,800 of them inside the first 8192-column
+    # window: more than the double-output rank accumulator holds, so that
+    # window is taken in several rank slices
+    dist = "pm1" if dtype == np.float64 else "open01"
+    A = matgen.random_sparse(64, 50, 0.9, 41, dtype, dist)
+    B = matgen.random_sparse(50, 9000, 0.07, 42, dtype, dist)
+    got, sym, num, ref = check(A, B, None, what="rank slices")
+    assert num["rows"]["dense"] == 64
 
 
 def test_laplacian_512_bit_exact():
