@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace wsp {
 
 constexpr int kWave = 64;
@@ -200,21 +202,72 @@ __device__ __forceinline__ double readlane_d(double x, int lane) {
     return __hiloint2double(hi, lo);
 }
 
+// A visitor deriving from TwoPhaseVisit splits a visit into k = pre(col), a
+// lookup, and post(k, prod), the update; operator()(col, prod) must equal
+// post(pre(col), prod). Span steps then issue all lookups before any update.
+struct TwoPhaseVisit {};
+
 // Processes blocks [lb0, lb1) (block = 64 consecutive products) of one
 // 64-entry A chunk whose lanes hold (boff, av, len, incl): the shared body of
 // the product iterators. `mark` is this wave's LDS mark array (all -1).
 //
-// A block whose first and last products belong to the same entry (the
-// common case on long B slices) takes that entry's data from scalar
-// registers; only blocks that straddle entries run the mark/max-scan lookup.
+// Long B slices (the bulk of the products on skewed inputs) take a span
+// step: kSpanBlocks blocks that all lie inside one entry are read with one
+// address computation (lane l takes products l, l+64, l+128, l+192) and
+// visited without any per-product branch. Other blocks go U at a time; a
+// block whose first and last products belong to the same entry takes that
+// entry's data from scalar registers, and only blocks that straddle entries
+// run the mark/max-scan lookup. Within a step every lane loads (a dead lane
+// from entry 0, which exists whenever a block does), so the step's loads are
+// issued back to back and waited for once.
+constexpr int kSpanBlocks = 4;
+
 template <typename V, bool VALUES, typename Visit>
 __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int incl, int tot, int lb0, int lb1,
                                              const int32_t *__restrict__ b_col, const V *__restrict__ b_val,
-                                             int32_t *mark, Visit visit) {
+                                             int32_t *mark, Visit &visit) {
     constexpr int U = kProductUnroll;
+    constexpr int SB = kSpanBlocks;
     const int ln = lane_id();
     const int excl = incl - len;
-    for (int lb = lb0; lb < lb1; lb += U) {
+    for (int lb = lb0; lb < lb1;) {
+        if (lb + SB <= lb1) {
+            const int base = lb * kWave;
+            const uint64_t before = __ballot(len > 0 && excl <= base);
+            const int o = before ? 63 - __clzll(before) : 0;
+            // the entry's products reach past the span's last one (so the span is also below tot)
+            if (__builtin_amdgcn_readlane(incl, o) > base + SB * kWave - 1) {
+                const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(boff, o)) + base;
+                const int32_t *cp = b_col + b0 + ln;
+                const V *vp = b_val + b0 + ln;
+                const double a = VALUES ? readlane_d(av, o) : 0.0;
+                int c[SB];
+                V v[SB];
+#pragma unroll
+                for (int u = 0; u < SB; ++u) {
+                    c[u] = cp[u * kWave];
+                    if (VALUES) v[u] = vp[u * kWave];
+                }
+                // keep the compiler from sinking a load into its use
+#pragma unroll
+                for (int u = 0; u < SB; ++u) {
+                    asm volatile("" : "+v"(c[u]));
+                    if (VALUES) asm volatile("" : "+v"(v[u]));
+                }
+                if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
+                    int k[SB];
+#pragma unroll
+                    for (int u = 0; u < SB; ++u) k[u] = visit.pre(c[u]);
+#pragma unroll
+                    for (int u = 0; u < SB; ++u) visit.post(k[u], VALUES ? a * to_d(v[u]) : 0.0);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < SB; ++u) visit(c[u], VALUES ? a * to_d(v[u]) : 0.0);
+                }
+                lb += SB;
+                continue;
+            }
+        }
         int ob[U];
         bool fast = true;
 #pragma unroll
@@ -255,18 +308,30 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
                 aval[u] = VALUES ? __shfl(av, o[u], kWave) : 0.0;
             }
         }
-        int col[U];
-        double bv[U];
+        bool live[U];
+        int ix[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const bool live = lb + u < lb1 && (lb + u) * kWave + ln < tot;
-            col[u] = live ? b_col[bidx[u]] : -1;
-            bv[u] = (VALUES && live) ? to_d(b_val[bidx[u]]) : 0.0;
+            live[u] = lb + u < lb1 && (lb + u) * kWave + ln < tot;
+            ix[u] = live[u] ? bidx[u] : 0;
+        }
+        int craw[U];
+        V vraw[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            craw[u] = b_col[ix[u]];
+            if (VALUES) vraw[u] = b_val[ix[u]];
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (col[u] >= 0) visit(col[u], VALUES ? aval[u] * bv[u] : 0.0);
+            asm volatile("" : "+v"(craw[u]));
+            if (VALUES) asm volatile("" : "+v"(vraw[u]));
         }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (live[u]) visit(craw[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+        }
+        lb += U;
     }
 }
 
@@ -280,18 +345,24 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
 // prefix sum of slice lengths, and block t of the chunk covers products
 // 64t .. 64t+63, lane j of the block taking product 64t + j. Consecutive lanes
 // therefore read consecutive B entries whenever a slice is long, and no lane
-// idles on short slices. Entries are taken in groups of
-// up to kMaxChunks chunks of 64. For each group:
+// idles on short slices. Entries are taken in groups of up to kMaxChunks
+// chunks of 64. For each group:
 //   1. wave w measures chunks w, w+NW, ...: its count of 64-product blocks;
 //   2. one wave scans the counts into block offsets (ctot, in LDS);
-//   3. wave w takes the contiguous block range [w*nb/NW, (w+1)*nb/NW) and
-//      loads only the chunks that range touches.
-// Every wave thus reads about 2/NW of the chunks instead of all of them, and
-// the products are split evenly. All threads of the workgroup must call it.
-// ctot holds kMaxChunks + 1 ints of LDS.
+//   3. the blocks are shared out. Static (DYNAMIC false): wave w takes the
+//      contiguous range [w*nb/NW, (w+1)*nb/NW). Dynamic: waves claim units of
+//      kUnitBlocks consecutive blocks from an LDS counter until none are
+//      left. A block costs more where slices are short (entry boundaries
+//      inside blocks) than inside a long slice, so on long rows claiming small
+//      units keeps the waves finishing together; on short rows the claims
+//      cost more than they save. Either way a wave moves forward through the
+//      chunks, keeping its current one in registers.
+// All threads of the workgroup must call it. ctot holds kCtotInts ints of LDS.
 constexpr int kMaxChunks = 256;
+constexpr int kCtotInts = kMaxChunks + 2;   // block offsets, total, claim counter
+constexpr int kUnitBlocks = 8;
 
-template <int BLOCK, typename V, bool VALUES, typename RangeF, typename Visit>
+template <int BLOCK, typename V, bool VALUES, bool DYNAMIC = false, typename RangeF, typename Visit>
 __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ a_col,
                                                     const V *__restrict__ a_val, int a_lo, int a_hi,
                                                     RangeF range, const int32_t *__restrict__ b_col,
@@ -300,6 +371,7 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
     constexpr int NW = BLOCK / kWave;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
+    int32_t *claim = ctot + kMaxChunks + 1;
     for (int g0 = a_lo; g0 < a_hi; g0 += kMaxChunks * kWave) {
         const int g1 = (a_hi - g0) < kMaxChunks * kWave ? a_hi : g0 + kMaxChunks * kWave;
         const int nch = (g1 - g0 + kWave - 1) / kWave;
@@ -314,6 +386,7 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
             const int tot = __builtin_amdgcn_readlane(wave_incl_sum(len), kWave - 1);
             if (ln == 0) ctot[c] = (tot + kWave - 1) / kWave;
         }
+        if (threadIdx.x == 0) *claim = 0;
         __syncthreads();
         // 2. exclusive scan of the block counts; ctot[nch] = total blocks
         if (wv == 0) {
@@ -328,41 +401,64 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
             if (ln == 0) ctot[nch] = carry;
         }
         __syncthreads();
-        // 3. this wave's share of the blocks
         const int nb = uniform(ctot[nch]);
-        const int b0 = static_cast<int>(static_cast<int64_t>(nb) * wv / NW);
-        const int b1 = static_cast<int>(static_cast<int64_t>(nb) * (wv + 1) / NW);
-        if (b0 < b1) {
-            // last chunk whose first block is <= b0
-            int lo = 0, hi = nch - 1;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (uniform(ctot[mid]) <= b0) lo = mid;
-                else hi = mid - 1;
-            }
-            int c = lo;
-            int b = b0;
-            while (b < b1) {
-                const int cb0 = uniform(ctot[c]);
-                const int cb1 = uniform(ctot[c + 1]);
-                if (cb1 > b) {
+        // a wave's chunk, held in registers, and its block range
+        int c = -1, cb0 = 0, cb1 = 0;
+        int boff = 0, len = 0, incl = 0, tot = 0;
+        double av = 0.0;
+        // processes blocks [b, e) of the group, moving forward through the chunks
+        auto run = [&](int b, int e) {
+            while (b < e) {
+                if (b >= cb1) {
+                    int cc = c < 0 ? 0 : c;
+                    while (uniform(ctot[cc + 1]) <= b) ++cc;
+                    c = cc;
+                    cb0 = uniform(ctot[c]);
+                    cb1 = uniform(ctot[c + 1]);
                     const int a = g0 + c * kWave + ln;
-                    int bs = 0, len = 0;
-                    double av = 0.0;
+                    int bs = 0;
+                    len = 0;
+                    av = 0.0;
                     if (a < g1) {
                         const int2 r = range(a_col[a]);
                         bs = r.x;
                         len = r.y - r.x;
                         if (VALUES) av = to_d(a_val[a]);
                     }
-                    const int incl = wave_incl_sum(len);
-                    const int tot = __builtin_amdgcn_readlane(incl, kWave - 1);
-                    const int e = cb1 < b1 ? cb1 : b1;
-                    chunk_blocks<V, VALUES>(bs - (incl - len), av, len, incl, tot, b - cb0, e - cb0, b_col, b_val,
-                                            mark, visit);
-                    b = e;
+                    incl = wave_incl_sum(len);
+                    tot = __builtin_amdgcn_readlane(incl, kWave - 1);
+                    boff = bs - (incl - len);
                 }
-                ++c;
+                const int ee = cb1 < e ? cb1 : e;
+                chunk_blocks<V, VALUES>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark, visit);
+                b = ee;
+            }
+        };
+        if constexpr (DYNAMIC) {
+            // 3. claimed units of blocks
+            const int nunits = (nb + kUnitBlocks - 1) / kUnitBlocks;
+            while (true) {
+                int u = 0;
+                if (ln == 0) u = atomicAdd(claim, 1);
+                u = uniform(u);
+                if (u >= nunits) break;
+                const int b = u * kUnitBlocks;
+                run(b, nb - b < kUnitBlocks ? nb : b + kUnitBlocks);
+            }
+        } else {
+            // 3. this wave's even share of the blocks
+            const int b0 = static_cast<int>(static_cast<int64_t>(nb) * wv / NW);
+            const int b1 = static_cast<int>(static_cast<int64_t>(nb) * (wv + 1) / NW);
+            if (b0 < b1) {
+                // last chunk whose first block is <= b0
+                int lo = 0, hi = nch - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (uniform(ctot[mid]) <= b0) lo = mid;
+                    else hi = mid - 1;
+                }
+                c = lo;   // run() searches forward from here
+                run(b0, b1);
             }
         }
         __syncthreads();

@@ -279,7 +279,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     __shared__ int32_t goff[BWW > 0 ? BWW / 8 : 1];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
-    __shared__ int32_t ctot[kMaxChunks + 1];
+    __shared__ int32_t ctot[kCtotInts];
 
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < T; i += BLOCK) {
@@ -390,16 +390,16 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     __shared__ uint32_t bm[NWORDS];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
-    __shared__ int32_t ctot[kMaxChunks + 1];
+    __shared__ int32_t ctot[kCtotInts];
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
     __syncthreads();
-    for_each_product_wg<BLOCK, float, false>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1], BRowRange{M.b_rp},
-                                             M.b_col, nullptr, mark, ctot,
-                                             [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
+    for_each_product_wg<BLOCK, float, false, true>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1],
+                                                   BRowRange{M.b_rp}, M.b_col, nullptr, mark, ctot,
+                                                   [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
     __syncthreads();
     int cnt = 0;
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) cnt += __popc(bm[i]);
@@ -459,7 +459,7 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
     __shared__ int32_t goff[S::BWW / 8];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
-    __shared__ int32_t ctot[kMaxChunks + 1];
+    __shared__ int32_t ctot[kCtotInts];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -596,6 +596,25 @@ struct RankShape {
     static_assert(REGION_WORDS % (BLOCK / kWave * kWave) == 0, "prefix scan takes whole word rows per wave");
 };
 
+// Value visit of the rank kernel: the product's rank among the region's
+// entries (bitmap word prefix plus the set bits below it), then an LDS add at
+// that rank when it falls in the current slice [r0, r1).
+struct RankAccumulate : TwoPhaseVisit {
+    const uint2 *bw;
+    double *acc;
+    int col0, r0, r1;
+    __device__ __forceinline__ int pre(int col) const {
+        const int rel = col - col0;
+        const uint2 e = bw[rel >> 5];
+        const int r = static_cast<int>(e.y) + __popc(e.x & ((1u << (rel & 31)) - 1u));
+        return (r >= r0 && r < r1) ? r - r0 : -1;
+    }
+    __device__ __forceinline__ void post(int k, double prod) const {
+        if (k >= 0) atomicAdd(&acc[k], prod);
+    }
+    __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
+};
+
 template <typename V>
 __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     Mats<V> M, const int32_t *__restrict__ rows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
@@ -608,11 +627,11 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     constexpr int WIN_WORDS = kRankWinCols / 32;
     constexpr int CAP = SH::CAP;
     __shared__ uint2 bw[RW];                 // x: column bits, y: exclusive prefix within the region
-    __shared__ double acc[CAP];
+    __shared__ double acc[CAP + 4];          // 4 slots of padding for the staging reads
     __shared__ int32_t stage[SH::STAGE];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
-    __shared__ int32_t ctot[kMaxChunks + 1];
+    __shared__ int32_t ctot[kCtotInts];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -634,11 +653,11 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
         __syncthreads();
         // 1. structure
-        for_each_product_wg<BLOCK, V, false>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0, rg1},
-                                             M.b_col, M.b_val, mark, ctot, [&](int col, double) {
-                                                 const int rel = static_cast<int>(col - col0);
-                                                 atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
-                                             });
+        for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0, rg1},
+                                                   M.b_col, M.b_val, mark, ctot, [&](int col, double) {
+                                                       const int rel = static_cast<int>(col - col0);
+                                                       atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
+                                                   });
         // 2. exclusive popcount prefix: wave w owns words [w*RW/NW, (w+1)*RW/NW), read one 64-word row at a
         //    time (lane-contiguous, so free of bank conflicts)
         {
@@ -682,17 +701,12 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             const int rend_w = rank_at_window(j2);
             const int r1 = rend_w - r0 > CAP ? r0 + CAP : rend_w;    // this slice covers ranks [r0, r1)
             // values
-            for_each_product_wg<BLOCK, V, true>(M.a_col, M.a_val, a_lo, a_hi,
-                                                BWindowRange{wtab, stride, rg0 + j, rg0 + j2}, M.b_col, M.b_val,
-                                                mark, ctot, [&](int col, double prod) {
-                                                    const int rel = static_cast<int>(col - col0);
-                                                    const uint2 e = bw[rel >> 5];
-                                                    const int r = static_cast<int>(e.y) +
-                                                                  __popc(e.x & ((1u << (rel & 31)) - 1u));
-                                                    if (r >= r0 && r < r1) atomicAdd(&acc[r - r0], prod);
-                                                });
+            for_each_product_wg<BLOCK, V, true, true>(
+                M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0 + j, rg0 + j2}, M.b_col, M.b_val, mark,
+                ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1});
             // stage ranks [r0, r1) in rank order: each wave a contiguous run of the windows' words, one word
-            // per lane; a lane walks its word's set bits (the wave loops while any lane still holds one), so
+            // per lane. A word's entries hold consecutive ranks, so a lane stages them four at a time (one
+            // 32-byte accumulator read per four entries; the wave loops while any lane has entries left), and
             // the cost follows the entries, not the columns. Every rank is staged by exactly one lane.
             const int wa = j * WIN_WORDS;
             const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
@@ -708,19 +722,38 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                     wbits &= wbits - 1u;
                     ++r;
                 }
-                while (__ballot(wbits != 0u && r < r1) != 0ull) {
-                    if (wbits != 0u && r < r1) {
-                        const int b = __builtin_ctz(wbits);
-                        wbits &= wbits - 1u;
-                        const int32_t colv = static_cast<int32_t>(col0 + wd * 32 + b);
-                        if constexpr (SH::PACKED) {
-                            const float v = static_cast<float>(acc[r - r0]);
-                            reinterpret_cast<uint2 *>(acc)[r - r0] = make_uint2(static_cast<uint32_t>(colv),
-                                                                                __float_as_uint(v));
-                        } else {
-                            stage[r - r0] = colv;
+                int n = __popc(wbits);
+                if (r + n > r1) n = r1 - r;
+                if (n < 0) n = 0;
+                const int k0 = r - r0;   // this lane's first slot
+                const int cbase = static_cast<int>(col0) + wd * 32;
+                for (int i = 0; __ballot(i < n) != 0ull; i += 4) {
+                    if (i < n) {
+                        int cv[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            cv[q] = cbase + __builtin_ctz(wbits | 0x80000000u);
+                            wbits &= wbits - 1u;
                         }
-                        ++r;
+                        if constexpr (SH::PACKED) {
+                            // the four slots may run past this lane's entries (into slots other lanes
+                            // rewrite, or the padding after CAP); those values are never used
+                            double a4[4];
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) a4[q] = acc[k0 + i + q];
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                if (i + q < n)
+                                    reinterpret_cast<uint2 *>(acc)[k0 + i + q] =
+                                        make_uint2(static_cast<uint32_t>(cv[q]),
+                                                   __float_as_uint(static_cast<float>(a4[q])));
+                            }
+                        } else {
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                if (i + q < n) stage[k0 + i + q] = cv[q];
+                            }
+                        }
                     }
                 }
             }
@@ -953,7 +986,7 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
     __shared__ int32_t s_keys[NUM ? kRunLen : 1];
     __shared__ V s_vals[NUM ? kRunLen : 1];
     __shared__ int32_t marks[NW * kMarkInts];
-    __shared__ int32_t ctot[kMaxChunks + 1];
+    __shared__ int32_t ctot[kCtotInts];
 
     int32_t *keys = reinterpret_cast<int32_t *>(pool + static_cast<int64_t>(blockIdx.x) * slab_cap * 12);
     double *vals = reinterpret_cast<double *>(keys + slab_cap);
