@@ -184,11 +184,11 @@ __device__ __forceinline__ int wave_incl_max(int v) {
 // Orders a wave's LDS accesses to different addresses (compiler and hardware).
 __device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 
-// Per-wave LDS scratch of kProductUnroll*64 ints used by for_each_product_wg to
-// locate the A entry of every product. It must hold -1 everywhere before the
-// first call; for_each_product_wg leaves it that way.
-constexpr int kProductUnroll = 2;
-constexpr int kMarkInts = kProductUnroll * kWave;
+// Per-wave LDS scratch of kMarkInts ints used by for_each_product_wg to
+// locate the A entries of blocks that span several of them. It must hold -1
+// everywhere before the first call; for_each_product_wg leaves it that way.
+constexpr int kScalarOwners = 8;      // entries per block resolved with scalar reads
+constexpr int kMarkInts = 2 * kWave;  // marks of up to two blocks
 
 // Sets this wave's mark array (kMarkInts ints) to -1.
 __device__ __forceinline__ void init_marks(int32_t *mark) {
@@ -214,19 +214,17 @@ struct TwoPhaseVisit {};
 // Long B slices (the bulk of the products on skewed inputs) take a span
 // step: kSpanBlocks blocks that all lie inside one entry are read with one
 // address computation (lane l takes products l, l+64, l+128, l+192) and
-// visited without any per-product branch. Other blocks go U at a time; a
-// block whose first and last products belong to the same entry takes that
-// entry's data from scalar registers, and only blocks that straddle entries
-// run the mark/max-scan lookup. Within a step every lane loads (a dead lane
-// from entry 0, which exists whenever a block does), so the step's loads are
-// issued back to back and waited for once.
+// visited without any per-product branch. Other blocks go U at a time in a
+// general step (U = 4 for long rows, 2 for short ones). Within a step every
+// lane loads (a dead lane from entry 0, which exists whenever a block does),
+// so the step's loads are issued back to back and waited for once.
 constexpr int kSpanBlocks = 4;
 
-template <typename V, bool VALUES, typename Visit>
+template <typename V, bool VALUES, bool LONG, typename Visit>
 __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int incl, int tot, int lb0, int lb1,
                                              const int32_t *__restrict__ b_col, const V *__restrict__ b_val,
                                              int32_t *mark, Visit &visit) {
-    constexpr int U = kProductUnroll;
+    constexpr int U = LONG ? 4 : 2;
     constexpr int SB = kSpanBlocks;
     const int ln = lane_id();
     const int excl = incl - len;
@@ -268,52 +266,105 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
                 continue;
             }
         }
-        int ob[U];
-        bool fast = true;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int base = (lb + u) * kWave;
-            const uint64_t before = __ballot(len > 0 && excl <= base);
-            ob[u] = before ? 63 - __clzll(before) : 0;
-            const int last = (base + kWave < tot ? base + kWave : tot) - 1;
-            fast = fast && (lb + u >= lb1 || __builtin_amdgcn_readlane(incl, ob[u]) > last);
-        }
-        int bidx[U];
+        // general step: U blocks
+        int ix[U];
         double aval[U];
-        if (fast) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                bidx[u] = __builtin_amdgcn_readlane(boff, ob[u]) + (lb + u) * kWave + ln;
-                aval[u] = VALUES ? readlane_d(av, ob[u]) : 0.0;
-            }
-        } else {
+        bool live[U];
+        if constexpr (LONG) {
+            // Each block resolved on its own. A block inside one entry takes
+            // that entry's data from scalar registers; a block spanning up to
+            // kScalarOwners entries assigns them to lanes with scalar reads of
+            // each entry's data (no LDS round trip); only blocks spanning more
+            // entries use the LDS marks and a max-scan.
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int base = (lb + u) * kWave;
-                if (len > 0 && excl > base && excl < base + kWave) mark[u * kWave + excl - base] = ln;
+                const int p = base + ln;
+                live[u] = lb + u < lb1 && p < tot;
+                ix[u] = 0;
+                aval[u] = 0.0;
+                if (lb + u >= lb1) continue;
+                const uint64_t bf = __ballot(len > 0 && excl <= base);
+                const int ob = bf ? 63 - __clzll(bf) : 0;
+                const int last = (base + kWave < tot ? base + kWave : tot) - 1;
+                const uint64_t bl = __ballot(len > 0 && excl <= last);
+                const int oe = bl ? 63 - __clzll(bl) : 0;
+                if (oe - ob < kScalarOwners) {
+                    int bo = __builtin_amdgcn_readlane(boff, ob);
+                    double a = VALUES ? readlane_d(av, ob) : 0.0;
+                    for (int e = ob + 1; e <= oe; ++e) {
+                        const int e_excl = __builtin_amdgcn_readlane(excl, e);
+                        const int e_len = __builtin_amdgcn_readlane(len, e);
+                        const int e_boff = __builtin_amdgcn_readlane(boff, e);
+                        const double e_av = VALUES ? readlane_d(av, e) : 0.0;
+                        if (e_len > 0 && p >= e_excl) {
+                            bo = e_boff;
+                            a = e_av;
+                        }
+                    }
+                    ix[u] = bo + p;
+                    aval[u] = a;
+                } else {
+                    if (len > 0 && excl > base && excl < base + kWave) mark[excl - base] = ln;
+                    wave_lds_fence();
+                    int m = mark[ln];
+                    mark[ln] = -1;
+                    m = wave_incl_max(m);
+                    const int o = m > ob ? m : ob;
+                    wave_lds_fence();
+                    ix[u] = __shfl(boff, o, kWave) + p;
+                    aval[u] = VALUES ? __shfl(av, o, kWave) : 0.0;
+                }
+                if (!live[u]) ix[u] = 0;
             }
-            wave_lds_fence();
-            int o[U];
+        } else {
+            // Short slices: if every block lies inside one entry, the entries'
+            // data come from scalar registers; otherwise all U blocks share one
+            // LDS mark/max-scan round.
+            int ob[U];
+            bool fast = true;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                int m = mark[u * kWave + ln];
-                mark[u * kWave + ln] = -1;
-                m = wave_incl_max(m);
-                o[u] = m > ob[u] ? m : ob[u];
+                const int base = (lb + u) * kWave;
+                const uint64_t before = __ballot(len > 0 && excl <= base);
+                ob[u] = before ? 63 - __clzll(before) : 0;
+                const int last = (base + kWave < tot ? base + kWave : tot) - 1;
+                fast = fast && (lb + u >= lb1 || __builtin_amdgcn_readlane(incl, ob[u]) > last);
             }
-            wave_lds_fence();
+            int bidx[U];
+            if (fast) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    bidx[u] = __builtin_amdgcn_readlane(boff, ob[u]) + (lb + u) * kWave + ln;
+                    aval[u] = VALUES ? readlane_d(av, ob[u]) : 0.0;
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int base = (lb + u) * kWave;
+                    if (len > 0 && excl > base && excl < base + kWave) mark[u * kWave + excl - base] = ln;
+                }
+                wave_lds_fence();
+                int o[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    int m = mark[u * kWave + ln];
+                    mark[u * kWave + ln] = -1;
+                    m = wave_incl_max(m);
+                    o[u] = m > ob[u] ? m : ob[u];
+                }
+                wave_lds_fence();
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    bidx[u] = __shfl(boff, o[u], kWave) + (lb + u) * kWave + ln;
+                    aval[u] = VALUES ? __shfl(av, o[u], kWave) : 0.0;
+                }
+            }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                bidx[u] = __shfl(boff, o[u], kWave) + (lb + u) * kWave + ln;
-                aval[u] = VALUES ? __shfl(av, o[u], kWave) : 0.0;
+                live[u] = lb + u < lb1 && (lb + u) * kWave + ln < tot;
+                ix[u] = live[u] ? bidx[u] : 0;
             }
-        }
-        bool live[U];
-        int ix[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            live[u] = lb + u < lb1 && (lb + u) * kWave + ln < tot;
-            ix[u] = live[u] ? bidx[u] : 0;
         }
         int craw[U];
         V vraw[U];
@@ -327,9 +378,17 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
             asm volatile("" : "+v"(craw[u]));
             if (VALUES) asm volatile("" : "+v"(vraw[u]));
         }
+        if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
+            int k[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (live[u]) visit(craw[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+            for (int u = 0; u < U; ++u) k[u] = live[u] ? visit.pre(craw[u]) : -1;
+#pragma unroll
+            for (int u = 0; u < U; ++u) visit.post(k[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (live[u]) visit(craw[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+            }
         }
         lb += U;
     }
@@ -349,20 +408,21 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
 // chunks of 64. For each group:
 //   1. wave w measures chunks w, w+NW, ...: its count of 64-product blocks;
 //   2. one wave scans the counts into block offsets (ctot, in LDS);
-//   3. the blocks are shared out. Static (DYNAMIC false): wave w takes the
-//      contiguous range [w*nb/NW, (w+1)*nb/NW). Dynamic: waves claim units of
-//      kUnitBlocks consecutive blocks from an LDS counter until none are
-//      left. A block costs more where slices are short (entry boundaries
-//      inside blocks) than inside a long slice, so on long rows claiming small
-//      units keeps the waves finishing together; on short rows the claims
-//      cost more than they save. Either way a wave moves forward through the
-//      chunks, keeping its current one in registers.
+//   3. the blocks are shared out. For short rows (LONG false) wave w takes
+//      the contiguous range [w*nb/NW, (w+1)*nb/NW). For long rows waves claim
+//      units of kUnitBlocks consecutive blocks from an LDS counter until none
+//      are left: a block costs more where slices are short (entry boundaries
+//      inside blocks) than inside a long slice, so claiming small units keeps
+//      the waves finishing together (on short rows the claims would cost more
+//      than they save). Either way a wave moves forward through the chunks,
+//      keeping its current one in registers.
+// LONG also selects the general-step shape (see chunk_blocks).
 // All threads of the workgroup must call it. ctot holds kCtotInts ints of LDS.
 constexpr int kMaxChunks = 256;
 constexpr int kCtotInts = kMaxChunks + 2;   // block offsets, total, claim counter
 constexpr int kUnitBlocks = 8;
 
-template <int BLOCK, typename V, bool VALUES, bool DYNAMIC = false, typename RangeF, typename Visit>
+template <int BLOCK, typename V, bool VALUES, bool LONG = false, typename RangeF, typename Visit>
 __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ a_col,
                                                     const V *__restrict__ a_val, int a_lo, int a_hi,
                                                     RangeF range, const int32_t *__restrict__ b_col,
@@ -430,11 +490,11 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                     boff = bs - (incl - len);
                 }
                 const int ee = cb1 < e ? cb1 : e;
-                chunk_blocks<V, VALUES>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark, visit);
+                chunk_blocks<V, VALUES, LONG>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark, visit);
                 b = ee;
             }
         };
-        if constexpr (DYNAMIC) {
+        if constexpr (LONG) {
             // 3. claimed units of blocks
             const int nunits = (nb + kUnitBlocks - 1) / kUnitBlocks;
             while (true) {
