@@ -394,6 +394,22 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
     }
 }
 
+// LDS copy of the first kCacheEntries A entries of a row, filled by step 1 of
+// a for_each_product_wg call (its slices in the call's range, its value) and
+// read back when step 3 loads a chunk, so a chunk costs an LDS read instead of
+// two dependent global round trips. `col` (the entries' columns) stays valid
+// for later calls on the same row once `col_ready` is set, which saves those
+// calls one round trip in step 1 too. A null `col` disables the cache.
+constexpr int kCacheChunks = 4;
+constexpr int kCacheEntries = kCacheChunks * kWave;
+struct EntryCache {
+    int32_t *col = nullptr;
+    int32_t *bs = nullptr;
+    int32_t *len = nullptr;
+    double *av = nullptr;
+    bool col_ready = false;
+};
+
 // Visits every product a * b of A entries [a_lo, a_hi) of one row: visit(col,
 // prod) with col = B.col_idx[b] and prod = A.val[a] * B.val[b] formed in double
 // (0 when VALUES is false). `range(k)` gives the slice [x, y) of B's entry
@@ -427,7 +443,7 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                                                     const V *__restrict__ a_val, int a_lo, int a_hi,
                                                     RangeF range, const int32_t *__restrict__ b_col,
                                                     const V *__restrict__ b_val, int32_t *mark, int32_t *ctot,
-                                                    Visit visit) {
+                                                    Visit visit, EntryCache cache = EntryCache{}) {
     constexpr int NW = BLOCK / kWave;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
@@ -435,13 +451,31 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
     for (int g0 = a_lo; g0 < a_hi; g0 += kMaxChunks * kWave) {
         const int g1 = (a_hi - g0) < kMaxChunks * kWave ? a_hi : g0 + kMaxChunks * kWave;
         const int nch = (g1 - g0 + kWave - 1) / kWave;
+        const bool use_cache = cache.col != nullptr && g0 == a_lo;
         // 1. blocks per chunk
         for (int c = wv; c < nch; c += NW) {
             const int a = g0 + c * kWave + ln;
+            const bool cached = use_cache && c < kCacheChunks;
+            const int ci = c * kWave + ln;
             int len = 0;
             if (a < g1) {
-                const int2 r = range(a_col[a]);
+                int k;
+                if (cached && cache.col_ready) k = cache.col[ci];
+                else k = a_col[a];
+                double av = 0.0;
+                if (VALUES && cached) av = to_d(a_val[a]);
+                const int2 r = range(k);
                 len = r.y - r.x;
+                if (cached) {
+                    if (!cache.col_ready) cache.col[ci] = k;
+                    cache.bs[ci] = r.x;
+                    cache.len[ci] = len;
+                    if (VALUES) cache.av[ci] = av;
+                }
+            } else if (cached) {
+                cache.bs[ci] = 0;
+                cache.len[ci] = 0;
+                if (VALUES) cache.av[ci] = 0.0;
             }
             const int tot = __builtin_amdgcn_readlane(wave_incl_sum(len), kWave - 1);
             if (ln == 0) ctot[c] = (tot + kWave - 1) / kWave;
@@ -479,7 +513,12 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                     int bs = 0;
                     len = 0;
                     av = 0.0;
-                    if (a < g1) {
+                    if (use_cache && c < kCacheChunks) {
+                        const int ci = c * kWave + ln;
+                        bs = cache.bs[ci];
+                        len = cache.len[ci];
+                        if (VALUES) av = cache.av[ci];
+                    } else if (a < g1) {
                         const int2 r = range(a_col[a]);
                         bs = r.x;
                         len = r.y - r.x;

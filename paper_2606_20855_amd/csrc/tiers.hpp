@@ -391,15 +391,17 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
     __shared__ int32_t ctot[kCtotInts];
+    __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
     __syncthreads();
-    for_each_product_wg<BLOCK, float, false, true>(M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1],
-                                                   BRowRange{M.b_rp}, M.b_col, nullptr, mark, ctot,
-                                                   [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); });
+    for_each_product_wg<BLOCK, float, false, true>(
+        M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1], BRowRange{M.b_rp}, M.b_col, nullptr, mark, ctot,
+        [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); },
+        EntryCache{e_col, e_bs, e_len, nullptr, false});
     __syncthreads();
     int cnt = 0;
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) cnt += __popc(bm[i]);
@@ -460,6 +462,8 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
     __shared__ int32_t ctot[kCtotInts];
+    __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
+    __shared__ double e_av[kCacheEntries];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -468,6 +472,7 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
+    EntryCache cache{e_col, e_bs, e_len, e_av, false};
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
 
@@ -590,7 +595,7 @@ struct RankShape {
     static constexpr int REGION_COLS = REGION_WORDS * 32;
     static constexpr int REGION_WINS = REGION_COLS / kRankWinCols;
     static constexpr bool PACKED = sizeof(V) == 4;
-    static constexpr int CAP = PACKED ? 10240 : 7168;
+    static constexpr int CAP = PACKED ? 10240 : 6656;
     static constexpr int STAGE = PACKED ? 1 : CAP;   // separate column stage (ints)
     static_assert(REGION_COLS % kRankWinCols == 0, "regions hold whole windows");
     static_assert(REGION_WORDS % (BLOCK / kWave * kWave) == 0, "prefix scan takes whole word rows per wave");
@@ -627,11 +632,13 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     constexpr int WIN_WORDS = kRankWinCols / 32;
     constexpr int CAP = SH::CAP;
     __shared__ uint2 bw[RW];                 // x: column bits, y: exclusive prefix within the region
-    __shared__ double acc[CAP + 4];          // 4 slots of padding for the staging reads
+    __shared__ double acc[CAP];
     __shared__ int32_t stage[SH::STAGE];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
     __shared__ int32_t ctot[kCtotInts];
+    __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
+    __shared__ double e_av[kCacheEntries];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -640,6 +647,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
+    EntryCache cache{e_col, e_bs, e_len, e_av, false};
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
@@ -652,12 +660,20 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         const int nwords = (ncw + 31) >> 5;
         for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
         __syncthreads();
-        // 1. structure
-        for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0, rg1},
-                                                   M.b_col, M.b_val, mark, ctot, [&](int col, double) {
-                                                       const int rel = static_cast<int>(col - col0);
-                                                       atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
-                                                   });
+        // 1. structure (a region covering every column takes whole B rows, whose bounds come from B's row
+        //    pointers rather than the larger window table)
+        auto mark_col = [&](int col, double) {
+            const int rel = static_cast<int>(col - col0);
+            atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
+        };
+        if (nwin <= SH::REGION_WINS)
+            for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col,
+                                                       M.b_val, mark, ctot, mark_col, cache);
+        else
+            for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi,
+                                                       BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val, mark,
+                                                       ctot, mark_col, cache);
+        cache.col_ready = true;
         // 2. exclusive popcount prefix: wave w owns words [w*RW/NW, (w+1)*RW/NW), read one 64-word row at a
         //    time (lane-contiguous, so free of bank conflicts)
         {
@@ -688,11 +704,13 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         region_total = uniform(region_total);
         __syncthreads();
         // 3. rank slices: whole windows while they fit CAP entries; a window
-        //    denser than CAP is taken in slices of CAP ranks
-        auto rank_at_window = [&](int jw) -> int {
-            return jw * WIN_WORDS < nwords ? uniform(static_cast<int>(bw[jw * WIN_WORDS].y)) : region_total;
-        };
+        //    denser than CAP is taken in slices of CAP ranks. Lane jw holds the
+        //    first rank of window jw (one LDS read for all windows), and the
+        //    greedy grouping reads them with scalar lane reads.
         const int nwr = rg1 - rg0;
+        const int win_rank = ln <= nwr && ln * WIN_WORDS < nwords ? static_cast<int>(bw[ln * WIN_WORDS].y)
+                                                                   : region_total;
+        auto rank_at_window = [&](int jw) -> int { return __builtin_amdgcn_readlane(win_rank, jw); };
         int j = 0;
         int r0 = 0;   // first rank of the current slice
         while (j < nwr) {
@@ -704,17 +722,35 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             for_each_product_wg<BLOCK, V, true, true>(
                 M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0 + j, rg0 + j2}, M.b_col, M.b_val, mark,
                 ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1});
-            // stage ranks [r0, r1) in rank order: each wave a contiguous run of the windows' words, one word
-            // per lane. A word's entries hold consecutive ranks, so a lane stages them four at a time (one
-            // 32-byte accumulator read per four entries; the wave loops while any lane has entries left), and
-            // the cost follows the entries, not the columns. Every rank is staged by exactly one lane.
+            if constexpr (SH::PACKED) {
+                // float output: round each accumulator once and keep the float in the high half of its own
+                // 8-byte slot, so the staging below only writes (it never waits on an accumulator read)
+                for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
+                    const float v = static_cast<float>(acc[i]);
+                    reinterpret_cast<uint2 *>(acc)[i].y = __float_as_uint(v);
+                }
+                __syncthreads();
+            }
+            // stage ranks [r0, r1) in rank order, one bitmap word per lane: the windows' words are cut into
+            // 64-word groups dealt round-robin to the waves (dense column ranges, where words hold many
+            // entries, are thus spread over all waves). A word's entries hold consecutive ranks; a lane stages
+            // them four per step (the wave loops while any lane has entries left), so the cost follows the
+            // entries, not the columns. Every rank is staged by exactly one lane.
             const int wa = j * WIN_WORDS;
             const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
-            const int w0w = wa + static_cast<int>(static_cast<int64_t>(wb - wa) * wv / NW);
-            const int w1w = wa + static_cast<int>(static_cast<int64_t>(wb - wa) * (wv + 1) / NW);
-            for (int wbase = w0w; wbase < w1w; wbase += kWave) {
-                const int wd = wbase + ln;
-                uint2 e = wd < w1w ? bw[wd] : make_uint2(0u, 0u);
+            // a wave holds at most RW / NW / 64 groups: read them all before staging
+            constexpr int MAXG = RW / NW / kWave;
+            uint2 ew[MAXG];
+#pragma unroll
+            for (int g = 0; g < MAXG; ++g) {
+                const int wd = wa + (g * NW + wv) * kWave + ln;
+                ew[g] = wd < wb ? bw[wd] : make_uint2(0u, 0u);
+            }
+#pragma unroll
+            for (int g = 0; g < MAXG; ++g) {
+                if (wa + (g * NW + wv) * kWave >= wb) break;
+                const int wd = wa + (g * NW + wv) * kWave + ln;
+                const uint2 e = ew[g];
                 uint32_t wbits = e.x;
                 int r = static_cast<int>(e.y);
                 // drop the entries below r0
@@ -736,17 +772,10 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                             wbits &= wbits - 1u;
                         }
                         if constexpr (SH::PACKED) {
-                            // the four slots may run past this lane's entries (into slots other lanes
-                            // rewrite, or the padding after CAP); those values are never used
-                            double a4[4];
-#pragma unroll
-                            for (int q = 0; q < 4; ++q) a4[q] = acc[k0 + i + q];
+                            // the column goes into the low half of the slot, beside the float value
 #pragma unroll
                             for (int q = 0; q < 4; ++q) {
-                                if (i + q < n)
-                                    reinterpret_cast<uint2 *>(acc)[k0 + i + q] =
-                                        make_uint2(static_cast<uint32_t>(cv[q]),
-                                                   __float_as_uint(static_cast<float>(a4[q])));
+                                if (i + q < n) reinterpret_cast<uint2 *>(acc)[k0 + i + q].x = static_cast<uint32_t>(cv[q]);
                             }
                         } else {
 #pragma unroll
