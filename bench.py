@@ -13,6 +13,10 @@ input, writing into a preallocated C. Prints one JSON line:
   cpu_baseline   the CPU oracle (single thread) on a seeded random sample of rows
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rmat18]
+       python bench.py --calibrate-copy BYTES
+The second form only copies BYTES bytes device to device three times (the
+runtime's plain copy kernel): run under rocprofv3 --pmc FETCH_SIZE or
+WRITE_SIZE, it gives the factor that turns those counters into bytes.
 """
 from __future__ import annotations
 
@@ -103,6 +107,7 @@ def main():
     ap.add_argument("--workload", default="rmat18")
     ap.add_argument("--cpu-fraction", type=float, default=0.08)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -110,6 +115,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.calibrate_copy > 0:
+        src = torch.ones(args.calibrate_copy, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps(dict(calibrate_copy_bytes=args.calibrate_copy, copies=3)), flush=True)
+        return
 
     import matgen
     from paper_2606_20855_amd import wingspan as ws

@@ -802,8 +802,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 }
                 acc[i] = 0.0;
                 if (pbase + i < seg) {
-                    c_col[cb + pbase + i] = colv;
-                    c_val[cb + pbase + i] = v;
+                    // streaming stores: C is written once, and must not push B out of the L2
+                    __builtin_nontemporal_store(colv, &c_col[cb + pbase + i]);
+                    __builtin_nontemporal_store(v, &c_val[cb + pbase + i]);
                 }
             }
             __syncthreads();
