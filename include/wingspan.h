@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define WINGSPAN_ABI_VERSION 1
+#define WINGSPAN_ABI_VERSION 2
 
 typedef enum { WINGSPAN_F32 = 0, WINGSPAN_F64 = 1 } wingspan_dtype;
 
@@ -115,6 +115,8 @@ typedef struct {
     float analysis_ms;                   /* product counting, binning, scans */
     int64_t total_products;
     int64_t c_nnz_total;
+    int64_t structure_cache_rows;        /* numeric phase only: rows whose column sets were taken
+                                            from the symbolic phase's structure cache (0: not used) */
 } wingspan_phase_stats;
 
 /* Bytes of device workspace the calls below need for this A, B and options.
@@ -136,10 +138,18 @@ wingspan_status wingspan_spgemm_symbolic(const wingspan_csr *A, const wingspan_c
 
 /* Numeric phase: fills c_col_idx_dev (int32) and c_val_dev (dtype) for the
  * structure c_row_ptr_dev produced by the symbolic phase for the same A and B
- * patterns. Depends only on c_row_ptr_dev, so it can be re-run when the
- * values of A or B change. Synchronizes `stream` once (to size its kernel
- * launches); the output kernels run asynchronously. Writes never leave a
- * row's range [c_row_ptr[i], c_row_ptr[i+1]). */
+ * patterns, so it can be re-run when the values of A or B change. Synchronizes
+ * `stream` once (to size its kernel launches); the output kernels run
+ * asynchronously. Writes never leave a row's range [c_row_ptr[i], c_row_ptr[i+1]).
+ *
+ * Structure cache: the symbolic phase keeps the column sets (bitmaps) of its
+ * densest rows in the workspace, up to 4 GiB, with a stamp naming A and B
+ * (pointers and sizes), the workspace layout and a checksum of C.row_ptr. A
+ * numeric call on the same workspace whose A, B, layout and c_row_ptr_dev
+ * match the stamp takes those column sets instead of recomputing them (it
+ * then reads B's column indices once per product instead of twice); any other
+ * call recomputes them. Calls that change A's or B's pattern in place must run
+ * the symbolic phase again, as C.row_ptr itself requires. */
 wingspan_status wingspan_spgemm_numeric(const wingspan_csr *A, const wingspan_csr *B,
                                         wingspan_dtype dtype, const int64_t *c_row_ptr_dev,
                                         int32_t *c_col_idx_dev, void *c_val_dev,

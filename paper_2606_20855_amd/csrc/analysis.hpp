@@ -248,6 +248,32 @@ __global__ void fill_i64(int64_t *p, int64_t n, int64_t v) {
     if (i < n) p[i] = v;
 }
 
+__global__ void fill_i32(int32_t *p, int64_t n, int32_t v) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// Position-weighted checksum of C.row_ptr[0..m]: sum of rp[i] * (2i + 1)
+// modulo 2^64, added into *out (which the caller zeroes).
+__global__ void __launch_bounds__(256) rowptr_checksum(const int64_t *__restrict__ rp, int64_t m, uint64_t *out) {
+    uint64_t acc = 0;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i <= m;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        acc += static_cast<uint64_t>(rp[i]) * static_cast<uint64_t>(2 * i + 1);
+    acc = wave_sum(acc);
+    if (lane_id() == 0) atomicAdd(reinterpret_cast<unsigned long long *>(out), static_cast<unsigned long long>(acc));
+}
+
+// Writes the stamp (one thread); magic 0 invalidates it.
+__global__ void write_stamp(Stamp *stamp, Stamp value) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) *stamp = value;
+}
+
+// Marks a stamp complete once its checksum has been added (one thread).
+__global__ void seal_stamp(Stamp *stamp) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) stamp->magic = kStampMagic;
+}
+
 // Flags values that could produce a zero product: exact zeros, and (for
 // double) magnitudes below 2^-537, whose products with each other could
 // underflow to zero. float products are formed in double and cannot underflow.

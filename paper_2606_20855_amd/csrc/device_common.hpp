@@ -35,6 +35,21 @@ enum : int32_t {
     kErrInvalidMatrix = 4,    // validation found a non-canonical input
 };
 
+// Record of what the last symbolic phase left in the workspace for the
+// numeric phase: the column sets (bitmaps) of dense rows. It names the inputs
+// and the layout it was made for and a checksum of C.row_ptr; the numeric
+// phase uses the bitmaps only if all of them match its own call. magic is 0
+// while a symbolic phase is running or after it failed.
+struct Stamp {
+    uint64_t magic;
+    uint64_t a_rp, a_col, b_rp, b_col;
+    int64_t a_nrows, a_ncols, a_nnz, b_nrows, b_ncols, b_nnz;
+    int64_t off_slot, off_cache, row_words, cache_rows;
+    int64_t cached_rows;   // rows that received a cache slot
+    uint64_t rp_sum;
+};
+constexpr uint64_t kStampMagic = 0x57535f5354525543ull;
+
 // Device-side control block, zeroed at the start of each phase and copied to
 // the host once the rows have been binned.
 struct Control {
@@ -45,6 +60,7 @@ struct Control {
     int32_t error_flags;
     int32_t has_zero_values;   // some A or B value could give a zero product
     int32_t pad_;
+    uint64_t rp_sum;           // numeric: checksum of the C.row_ptr it was given
     int32_t bin_count[kMaxBins];
     int32_t bin_offset[kMaxBins];
     int32_t bin_cursor[kMaxBins];

@@ -381,11 +381,16 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
 // Dense tier, symbolic: an LDS bitmap over all NWORDS*32 columns, one
 // workgroup per row. The row's entry count is the bitmap's population count.
 // ---------------------------------------------------------------------------
+// Row i of the structure cache (when cache is not null) receives the bitmap
+// of the row handled by workgroup i < cache_rows, and slot_of_row[row] = i.
 template <int NWORDS, int BLOCK>
 __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
                                                            const int32_t *__restrict__ rows,
                                                            int nwords_used,
-                                                           int32_t *__restrict__ row_nnz) {
+                                                           int32_t *__restrict__ row_nnz,
+                                                           int32_t *__restrict__ slot_of_row,
+                                                           uint32_t *__restrict__ cache, int64_t row_words,
+                                                           int64_t cache_rows) {
     constexpr int NW = BLOCK / kWave;
     __shared__ uint32_t bm[NWORDS];
     __shared__ int32_t scratch[NW];
@@ -405,6 +410,11 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     __syncthreads();
     int cnt = 0;
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) cnt += __popc(bm[i]);
+    if (cache != nullptr && blockIdx.x < cache_rows) {
+        uint32_t *dst = cache + static_cast<int64_t>(blockIdx.x) * row_words;
+        for (int i = threadIdx.x; i < nwords_used; i += BLOCK) __builtin_nontemporal_store(bm[i], &dst[i]);
+        if (threadIdx.x == 0) slot_of_row[row] = static_cast<int32_t>(blockIdx.x);
+    }
     const int total = block_sum<BLOCK>(cnt, scratch);
     if (threadIdx.x == 0) row_nnz[row] = total;
 }
@@ -462,8 +472,6 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
     __shared__ int32_t ctot[kCtotInts];
-    __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
-    __shared__ double e_av[kCacheEntries];
 
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
@@ -472,7 +480,6 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
-    EntryCache cache{e_col, e_bs, e_len, e_av, false};
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
 
@@ -620,10 +627,14 @@ struct RankAccumulate : TwoPhaseVisit {
     __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
 };
 
+// When slot_of_row is not null, a row with slot_of_row[row] >= 0 takes its
+// column bitmap from that row of the structure cache (written by the symbolic
+// phase for the same A and B) instead of running the structure pass.
 template <typename V>
 __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     Mats<V> M, const int32_t *__restrict__ rows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
-    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl) {
+    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
+    const int32_t *__restrict__ slot_of_row, const uint32_t *__restrict__ cache, int64_t row_words) {
     using SH = RankShape<V>;
     constexpr int BLOCK = SH::BLOCK;
     constexpr int NW = BLOCK / kWave;
@@ -647,7 +658,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
-    EntryCache cache{e_col, e_bs, e_len, e_av, false};
+    EntryCache ecache{e_col, e_bs, e_len, e_av, false};
+    const int slot = slot_of_row != nullptr ? uniform(slot_of_row[row]) : -1;
+    const uint32_t *cached = slot >= 0 ? cache + static_cast<int64_t>(slot) * row_words : nullptr;
     int32_t *mark = marks + wv * kMarkInts;
     init_marks(mark);
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
@@ -658,22 +671,28 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         const int64_t col0 = static_cast<int64_t>(rg0) * kRankWinCols;
         const int ncw = static_cast<int>(ncols - col0 < SH::REGION_COLS ? ncols - col0 : SH::REGION_COLS);
         const int nwords = (ncw + 31) >> 5;
-        for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
-        __syncthreads();
-        // 1. structure (a region covering every column takes whole B rows, whose bounds come from B's row
-        //    pointers rather than the larger window table)
-        auto mark_col = [&](int col, double) {
-            const int rel = static_cast<int>(col - col0);
-            atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
-        };
-        if (nwin <= SH::REGION_WINS)
-            for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col,
-                                                       M.b_val, mark, ctot, mark_col, cache);
-        else
-            for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi,
-                                                       BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val, mark,
-                                                       ctot, mark_col, cache);
-        cache.col_ready = true;
+        // 1. structure: the cached bitmap, or a structure pass (a region covering every column takes whole B
+        //    rows, whose bounds come from B's row pointers rather than the larger window table)
+        if (cached != nullptr) {
+            const uint32_t *src = cached + static_cast<int64_t>(rg0) * WIN_WORDS;
+            for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = i < nwords ? src[i] : 0u;
+            __syncthreads();
+        } else {
+            for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
+            __syncthreads();
+            auto mark_col = [&](int col, double) {
+                const int rel = static_cast<int>(col - col0);
+                atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
+            };
+            if (nwin <= SH::REGION_WINS)
+                for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col,
+                                                           M.b_val, mark, ctot, mark_col, ecache);
+            else
+                for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi,
+                                                           BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val,
+                                                           mark, ctot, mark_col, ecache);
+            ecache.col_ready = true;
+        }
         // 2. exclusive popcount prefix: wave w owns words [w*RW/NW, (w+1)*RW/NW), read one 64-word row at a
         //    time (lane-contiguous, so free of bank conflicts)
         {
@@ -721,7 +740,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             // values
             for_each_product_wg<BLOCK, V, true, true>(
                 M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0 + j, rg0 + j2}, M.b_col, M.b_val, mark,
-                ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1});
+                ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1}, ecache);
+            ecache.col_ready = true;
             if constexpr (SH::PACKED) {
                 // float output: round each accumulator once and keep the float in the high half of its own
                 // 8-byte slot, so the staging below only writes (it never waits on an accumulator read)

@@ -32,6 +32,7 @@ constexpr int kHashLog2MaxSym = 14;           // 16K int32 keys = 64 KB of LDS
 constexpr int kHashLog2MaxNum = 13;           // 8K keys + 8K doubles = 96 KB of LDS
 constexpr int64_t kBitmapMaxCols = 36864 * 32; // 144 KB LDS bitmap (plus per-wave marks)
 constexpr int kMaxWindows = 128;              // dense numeric tier: windows per row
+constexpr int64_t kStructCacheBytes = int64_t(4) << 30;   // dense-row bitmaps kept from symbolic to numeric
 constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
 constexpr int64_t kPoolBytes = int64_t(256) << 20;
 constexpr int64_t kMaxSlabCap = int64_t(1) << 27;
@@ -153,7 +154,9 @@ wingspan_status check_pair(const wingspan_csr *A, const wingspan_csr *B) {
 
 // Workspace layout, a pure function of the sizes and options.
 struct Layout {
-    size_t off_ctrl, off_pref, off_row_nnz, off_perm, off_partials, off_wtab, off_pool, total;
+    size_t off_stamp, off_ctrl, off_pref, off_row_nnz, off_perm, off_partials, off_wtab, off_pool, total;
+    size_t off_slot, off_cache;   // structure cache (cache_rows == 0: none)
+    int64_t row_words, cache_rows;
     int nwin;          // numeric dense windows per row (0: dense numeric tier unavailable)
     int wcols;         // columns per window of the window table
     bool rank_mode;    // dense numeric rows use the rank-indexed kernel
@@ -165,6 +168,8 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
     Layout L{};
     const int64_t m = A->nrows, n = B->ncols, nnz_a = A->nnz;
     size_t off = 0;
+    L.off_stamp = off;
+    off += align_up(sizeof(Stamp));
     L.off_ctrl = off;
     off += align_up(sizeof(Control));
     L.off_pref = off;
@@ -192,6 +197,19 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
     const int64_t slab_bytes = L.slab_cap * 12;
     L.nslab = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxSlabs, kPoolBytes / slab_bytes)));
     off += align_up(static_cast<size_t>(slab_bytes) * L.nslab);
+    // structure cache: the symbolic phase's column bitmaps of dense rows, reused by the rank-indexed numeric
+    // kernel; rows beyond kStructCacheBytes run their own structure pass
+    L.cache_rows = 0;
+    L.row_words = 0;
+    if (L.rank_mode && L.nwin > 0 && !o.dense_disabled && n > 0 && n <= kBitmapMaxCols && m > 0) {
+        L.row_words = (n + 31) / 32;
+        L.row_words = (L.row_words + 63) / 64 * 64;
+        L.cache_rows = std::min<int64_t>(m, kStructCacheBytes / (L.row_words * 4));
+    }
+    L.off_slot = off;
+    if (L.cache_rows > 0) off += align_up(sizeof(int32_t) * m);
+    L.off_cache = off;
+    if (L.cache_rows > 0) off += align_up(static_cast<size_t>(L.cache_rows) * L.row_words * 4);
     L.total = off;
     return L;
 }
@@ -212,7 +230,11 @@ struct Ctx {
     int64_t *partials;
     int32_t *wtab;
     char *pool;
+    Stamp *stamp;
+    int32_t *slot_of_row;
+    uint32_t *cache;
     Control host;
+    Stamp host_stamp;
 };
 
 void carve(Ctx &c, void *ws) {
@@ -224,6 +246,44 @@ void carve(Ctx &c, void *ws) {
     c.partials = reinterpret_cast<int64_t *>(c.ws + c.L.off_partials);
     c.wtab = reinterpret_cast<int32_t *>(c.ws + c.L.off_wtab);
     c.pool = c.ws + c.L.off_pool;
+    c.stamp = reinterpret_cast<Stamp *>(c.ws + c.L.off_stamp);
+    c.slot_of_row = reinterpret_cast<int32_t *>(c.ws + c.L.off_slot);
+    c.cache = reinterpret_cast<uint32_t *>(c.ws + c.L.off_cache);
+}
+
+// The stamp a symbolic phase on (A, B) with this layout leaves (magic and
+// rp_sum are filled in on the device).
+Stamp make_stamp(const Ctx &c, const wingspan_csr *A, const wingspan_csr *B, int64_t cached_rows = 0) {
+    Stamp t{};
+    t.cached_rows = cached_rows;
+    t.a_rp = reinterpret_cast<uint64_t>(A->row_ptr);
+    t.a_col = reinterpret_cast<uint64_t>(A->col_idx);
+    t.b_rp = reinterpret_cast<uint64_t>(B->row_ptr);
+    t.b_col = reinterpret_cast<uint64_t>(B->col_idx);
+    t.a_nrows = A->nrows;
+    t.a_ncols = A->ncols;
+    t.a_nnz = A->nnz;
+    t.b_nrows = B->nrows;
+    t.b_ncols = B->ncols;
+    t.b_nnz = B->nnz;
+    t.off_slot = static_cast<int64_t>(c.L.off_slot);
+    t.off_cache = static_cast<int64_t>(c.L.off_cache);
+    t.row_words = c.L.row_words;
+    t.cache_rows = c.L.cache_rows;
+    return t;
+}
+
+// Whether the numeric phase may use the structure cache: the stamp is valid,
+// was made for these inputs and this layout, and for the C.row_ptr given.
+bool stamp_matches(const Ctx &c, const wingspan_csr *A, const wingspan_csr *B) {
+    if (c.L.cache_rows <= 0) return false;
+    const Stamp &h = c.host_stamp;
+    const Stamp t = make_stamp(c, A, B);
+    return h.magic == kStampMagic && h.a_rp == t.a_rp && h.a_col == t.a_col && h.b_rp == t.b_rp &&
+           h.b_col == t.b_col && h.a_nrows == t.a_nrows && h.a_ncols == t.a_ncols && h.a_nnz == t.a_nnz &&
+           h.b_nrows == t.b_nrows && h.b_ncols == t.b_ncols && h.b_nnz == t.b_nnz && h.off_slot == t.off_slot &&
+           h.off_cache == t.off_cache && h.row_words == t.row_words && h.cache_rows == t.cache_rows &&
+           h.rp_sum == c.host.rp_sum;
 }
 
 // HIP events for optional per-tier timing, created once per thread.
@@ -278,6 +338,13 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, bo
     const int64_t words = sizeof(Control) / sizeof(int32_t);
     zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl), words);
     LAUNCH_CHECK("zero_words");
+    if (!numeric) {
+        // the structure cache is being rewritten: invalid until this phase completes
+        write_stamp<<<1, 1, 0, c.st>>>(c.stamp, Stamp{});
+    } else if (c.L.cache_rows > 0) {
+        rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, m, &c.ctrl->rp_sum);
+    }
+    LAUNCH_CHECK("stamp");
     if (c.o.validate) {
         if (A->nrows > 0)
             validate_csr<<<blocks_for(A->nrows * kWave, 256), 256, 0, c.st>>>(A->row_ptr, A->col_idx, A->nrows,
@@ -328,6 +395,8 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, bo
     LAUNCH_CHECK("binning");
     if ((s = timer_stop(c, kSlotAnalysis)) != WINGSPAN_OK) return s;
     HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+    if (numeric && c.L.cache_rows > 0)
+        HIP_TRY(hipMemcpyAsync(&c.host_stamp, c.stamp, sizeof(Stamp), hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
     const int64_t slab_limit = c.L.slab_cap / 2;
     if (c.host.spill_max_bound > slab_limit)
@@ -411,13 +480,16 @@ void launch_hash(int log2t, unsigned grid, hipStream_t st, const Mats<V> &M, con
 }
 
 void launch_bitmap(int64_t ncols, unsigned grid, hipStream_t st, const Mats<float> &M, const int32_t *rows,
-                   int32_t *row_nnz) {
+                   int32_t *row_nnz, int32_t *slot_of_row, uint32_t *cache, int64_t row_words, int64_t cache_rows) {
     const int nwords = static_cast<int>((ncols + 31) / 32);
-    if (nwords <= 2048) bitmap_sym_kernel<2048, 512><<<grid, 512, 0, st>>>(M, rows, nwords, row_nnz);
-    else if (nwords <= 8192) bitmap_sym_kernel<8192, 512><<<grid, 512, 0, st>>>(M, rows, nwords, row_nnz);
-    else if (nwords <= 16384) bitmap_sym_kernel<16384, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
-    else if (nwords <= 32768) bitmap_sym_kernel<32768, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
-    else bitmap_sym_kernel<36864, 1024><<<grid, 1024, 0, st>>>(M, rows, nwords, row_nnz);
+#define WS_BITMAP(NW, BL) \
+    bitmap_sym_kernel<NW, BL><<<grid, BL, 0, st>>>(M, rows, nwords, row_nnz, slot_of_row, cache, row_words, cache_rows)
+    if (nwords <= 2048) WS_BITMAP(2048, 512);
+    else if (nwords <= 8192) WS_BITMAP(8192, 512);
+    else if (nwords <= 16384) WS_BITMAP(16384, 1024);
+    else if (nwords <= 32768) WS_BITMAP(32768, 1024);
+    else WS_BITMAP(36864, 1024);
+#undef WS_BITMAP
 }
 
 template <int WV, typename V>
@@ -487,8 +559,16 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
     int32_t start, cnt;
     if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
+    const bool caching = c.L.cache_rows > 0;
+    const int64_t cnt_dense = cnt;
+    if (caching) {
+        fill_i32<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(c.slot_of_row, A->nrows, -1);
+        LAUNCH_CHECK("fill slots");
+    }
     if (cnt) {
-        launch_bitmap(B->ncols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.row_nnz);
+        launch_bitmap(B->ncols, static_cast<unsigned>(cnt), c.st, M, perm + start, c.row_nnz,
+                      caching ? c.slot_of_row : nullptr, caching ? c.cache : nullptr, c.L.row_words,
+                      c.L.cache_rows);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("bitmap symbolic");
     }
@@ -508,6 +588,13 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
 
     s = run_scan(c, CountIn{c.row_nnz}, A->nrows, c_rp);
     if (s != WINGSPAN_OK) return s;
+    if (caching) {
+        // the cache is complete: stamp it with the inputs, the layout and C.row_ptr's checksum
+        write_stamp<<<1, 1, 0, c.st>>>(c.stamp, make_stamp(c, A, B, std::min<int64_t>(cnt_dense, c.L.cache_rows)));
+        rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, A->nrows, &c.stamp->rp_sum);
+        seal_stamp<<<1, 1, 0, c.st>>>(c.stamp);
+        LAUNCH_CHECK("stamp");
+    }
     int64_t total = 0;
     HIP_TRY(hipMemcpyAsync(&total, c_rp + A->nrows, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
@@ -569,8 +656,11 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     // the dense tier's time covers its one kernel launch only
     if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     if (cnt && c.L.rank_mode) {
+        const bool cached = stamp_matches(c, A, B);
+        stats.structure_cache_rows = cached ? c.host_stamp.cached_rows : 0;
         dense_rank_kernel<V><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
-            M, perm + start, c.wtab, c.L.nwin, B->ncols, c_rp, c_col, c_val, c.ctrl);
+            M, perm + start, c.wtab, c.L.nwin, B->ncols, c_rp, c_col, c_val, c.ctrl,
+            cached ? c.slot_of_row : nullptr, cached ? c.cache : nullptr, c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense rank numeric");
     } else if (cnt) {

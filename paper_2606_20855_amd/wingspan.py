@@ -19,7 +19,7 @@ import numpy as np
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libwingspan.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 F32, F64 = 0, 1
 TIERS = ("tiny", "hash", "dense", "spill")
 
@@ -83,6 +83,7 @@ class wingspan_phase_stats(ctypes.Structure):
         ("analysis_ms", ctypes.c_float),
         ("total_products", ctypes.c_int64),
         ("c_nnz_total", ctypes.c_int64),
+        ("structure_cache_rows", ctypes.c_int64),
     ]
 
 
@@ -169,6 +170,7 @@ def wingspan_last_stats(phase: int) -> dict:
     out["analysis_ms"] = st.analysis_ms
     out["total_products"] = st.total_products
     out["c_nnz_total"] = st.c_nnz_total
+    out["structure_cache_rows"] = st.structure_cache_rows
     return out
 
 

@@ -44,14 +44,14 @@ def test_library_exports_every_header_function():
 
 
 def test_abi_version():
-    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 1
+    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 2
 
 
 def test_struct_layouts_match_header():
     # sizes the C side sees (x86-64 SysV)
     assert ctypes.sizeof(ws.wingspan_csr) == 48
     assert ctypes.sizeof(ws.wingspan_options) == 32
-    assert ctypes.sizeof(ws.wingspan_phase_stats) == 4 * 8 * 4 + 4 * 4 + 4 * 4 + 4 + 4 + 8 + 8
+    assert ctypes.sizeof(ws.wingspan_phase_stats) == 4 * 8 * 4 + 4 * 4 + 4 * 4 + 4 + 4 + 8 + 8 + 8
 
 
 def test_workspace_size_is_host_only_and_monotone():
@@ -65,8 +65,20 @@ def test_workspace_size_is_host_only_and_monotone():
                                                 desc(100_000, 100_000, 1_000_000), ws.F64,
                                                 ws.make_options(dense_min_nnz=-1))
     assert nodense < big
-    # empty operands are fine
+    # empty operands are fine, including a B without columns (no structure
+    # cache then: its row size would be zero)
     assert ws.wingspan_spgemm_workspace_size(desc(0, 0, 0), desc(0, 0, 0), ws.F32) > 0
+    for m, k, n in [(5, 3, 0), (0, 3, 5), (5, 0, 5), (3, 3, 3)]:
+        assert ws.wingspan_spgemm_workspace_size(desc(m, k, 0), desc(k, n, 0), ws.F32) > 0
+
+
+def test_workspace_structure_cache_is_bounded():
+    # the dense rows' bitmaps kept from symbolic to numeric take at most 4 GiB
+    n = 262_144
+    with_cache = ws.wingspan_spgemm_workspace_size(desc(n, n, 4_000_000), desc(n, n, 4_000_000), ws.F32)
+    without = ws.wingspan_spgemm_workspace_size(desc(n, n, 4_000_000), desc(n, n, 4_000_000), ws.F32,
+                                                ws.make_options(window_cols=8192))
+    assert 0 < with_cache - without <= (4 << 30) + n * 4 + 512
 
 
 @pytest.mark.parametrize("A,B,code", [
