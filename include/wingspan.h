@@ -85,9 +85,11 @@ typedef struct {
     int32_t window_cols;    /* dense-window width in columns: 1024, 4096, 8192 or 16384 */
     int32_t tiny_max;       /* largest per-row product count handled by the
                                register-sort tier (8..64); -1 disables that tier */
-    int32_t dense_min_nnz;  /* numeric: rows with at least this many output entries use
-                               the dense-window tier even if they fit an LDS hash table;
-                               -1 disables the dense tier */
+    int32_t dense_min_nnz;  /* rows with at least this many output entries (numeric) or
+                               products (symbolic) use the dense tier even if they fit an
+                               LDS hash table; -1 disables the dense tier; 0 means 2048 when
+                               the structure cache applies, else only rows too large for
+                               the LDS hash tables */
     int32_t timing;         /* 1: time each tier's kernels with HIP events on `stream`
                                (the call then synchronizes the stream before returning) */
 } wingspan_options;

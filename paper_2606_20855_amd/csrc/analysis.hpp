@@ -152,7 +152,10 @@ __device__ __forceinline__ int choose_bin(int64_t f, int64_t c, const BinCfg &cf
     }
     int l = ceil_log2(need);
     if (l < kHashLog2Min) l = kHashLog2Min;
-    const bool dense_pref = cfg.numeric && cfg.dense_ok && c >= cfg.dense_min_nnz;
+    // dense preference: numeric rows by their output entries; symbolic rows by their products (a row with c
+    // entries has at least c products, so every row the numeric phase will prefer dense goes through the
+    // symbolic bitmap kernel and leaves its column set in the structure cache)
+    const bool dense_pref = cfg.dense_ok && (cfg.numeric ? c : f) >= cfg.dense_min_nnz;
     if (!cfg.force_spill && l <= cfg.hash_log2_max && !dense_pref) return kBinHash0 + (l - kHashLog2Min);
     if (!cfg.force_spill && cfg.dense_ok) return kBinDense0 + class_of(f);
     *bound = cfg.numeric ? c : (f < cfg.ncols ? f : cfg.ncols);

@@ -674,8 +674,17 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         // 1. structure: the cached bitmap, or a structure pass (a region covering every column takes whole B
         //    rows, whose bounds come from B's row pointers rather than the larger window table)
         if (cached != nullptr) {
+            // all of a thread's words are loaded before any is stored, so the loads are in flight together
             const uint32_t *src = cached + static_cast<int64_t>(rg0) * WIN_WORDS;
-            for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = i < nwords ? src[i] : 0u;
+            constexpr int PER = RW / BLOCK;
+            uint32_t wd[PER];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int i = q * BLOCK + static_cast<int>(threadIdx.x);
+                wd[q] = i < nwords ? __builtin_nontemporal_load(&src[i]) : 0u;
+            }
+#pragma unroll
+            for (int q = 0; q < PER; ++q) bw[q * BLOCK + threadIdx.x].x = wd[q];
             __syncthreads();
         } else {
             for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;

@@ -33,6 +33,11 @@ constexpr int kHashLog2MaxNum = 13;           // 8K keys + 8K doubles = 96 KB of
 constexpr int64_t kBitmapMaxCols = 36864 * 32; // 144 KB LDS bitmap (plus per-wave marks)
 constexpr int kMaxWindows = 128;              // dense numeric tier: windows per row
 constexpr int64_t kStructCacheBytes = int64_t(4) << 30;   // dense-row bitmaps kept from symbolic to numeric
+// With the structure cache, rows from this many entries (products, in the symbolic phase) up take the
+// bitmap / rank-indexed path even when they would fit an LDS hash table: the symbolic bitmap kernel is
+// cheaper than a large LDS hash, and the rank-indexed numeric kernel, which then skips its structure
+// pass, cheaper than a numeric hash table of 2^12 slots or more.
+constexpr int64_t kCachedDenseMin = 2048;
 constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
 constexpr int64_t kPoolBytes = int64_t(256) << 20;
 constexpr int64_t kMaxSlabCap = int64_t(1) << 27;
@@ -85,6 +90,7 @@ struct Opts {
     bool wcols_explicit = false;   // window_cols given: use the column-window dense kernel
     int tiny_max = 64;
     int64_t dense_min_nnz = INT64_MAX;
+    bool dense_min_explicit = false;   // dense_min_nnz given (otherwise chosen from the layout)
 };
 
 wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
@@ -123,7 +129,10 @@ wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
         if (o->dense_min_nnz == -1) r.dense_disabled = true;
         else if (o->dense_min_nnz < -1)
             return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "options->dense_min_nnz must be >= -1");
-        else if (o->dense_min_nnz > 0) r.dense_min_nnz = o->dense_min_nnz;
+        else if (o->dense_min_nnz > 0) {
+            r.dense_min_nnz = o->dense_min_nnz;
+            r.dense_min_explicit = true;
+        }
     }
     *out = r;
     return WINGSPAN_OK;
@@ -717,6 +726,7 @@ wingspan_status setup(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, cons
         return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kAlign);
     c.st = static_cast<hipStream_t>(stream);
     carve(c, ws);
+    if (!c.o.dense_min_explicit && c.L.cache_rows > 0) c.o.dense_min_nnz = kCachedDenseMin;
     return WINGSPAN_OK;
 }
 
