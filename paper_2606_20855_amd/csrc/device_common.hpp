@@ -71,6 +71,10 @@ struct Control {
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+// Lane mask of a condition (bit l set where lane l's condition holds),
+// straight from the compare's scalar mask.
+__device__ __forceinline__ uint64_t ballot(bool b) { return __builtin_amdgcn_ballot_w64(b); }
+
 // Values every lane of the workgroup holds identically (read back from LDS
 // after a barrier) are moved to scalar registers, so loops and branches that
 // depend on them compile as uniform control flow. Barriers then never sit in
@@ -244,10 +248,13 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
     constexpr int SB = kSpanBlocks;
     const int ln = lane_id();
     const int excl = incl - len;
+    // first product of the lane's entry, or INT_MAX for an entry without products: "an entry with products
+    // starts at or before q" is then one compare
+    const int start = len > 0 ? excl : 0x7fffffff;
     for (int lb = lb0; lb < lb1;) {
         if (lb + SB <= lb1) {
             const int base = lb * kWave;
-            const uint64_t before = __ballot(len > 0 && excl <= base);
+            const uint64_t before = ballot(start <= base);
             const int o = before ? 63 - __clzll(before) : 0;
             // the entry's products reach past the span's last one (so the span is also below tot)
             if (__builtin_amdgcn_readlane(incl, o) > base + SB * kWave - 1) {
@@ -300,20 +307,19 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
                 ix[u] = 0;
                 aval[u] = 0.0;
                 if (lb + u >= lb1) continue;
-                const uint64_t bf = __ballot(len > 0 && excl <= base);
+                const uint64_t bf = ballot(start <= base);
                 const int ob = bf ? 63 - __clzll(bf) : 0;
                 const int last = (base + kWave < tot ? base + kWave : tot) - 1;
-                const uint64_t bl = __ballot(len > 0 && excl <= last);
+                const uint64_t bl = ballot(start <= last);
                 const int oe = bl ? 63 - __clzll(bl) : 0;
                 if (oe - ob < kScalarOwners) {
                     int bo = __builtin_amdgcn_readlane(boff, ob);
                     double a = VALUES ? readlane_d(av, ob) : 0.0;
                     for (int e = ob + 1; e <= oe; ++e) {
-                        const int e_excl = __builtin_amdgcn_readlane(excl, e);
-                        const int e_len = __builtin_amdgcn_readlane(len, e);
+                        const int e_start = __builtin_amdgcn_readlane(start, e);
                         const int e_boff = __builtin_amdgcn_readlane(boff, e);
                         const double e_av = VALUES ? readlane_d(av, e) : 0.0;
-                        if (e_len > 0 && p >= e_excl) {
+                        if (p >= e_start) {
                             bo = e_boff;
                             a = e_av;
                         }
@@ -342,7 +348,7 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int base = (lb + u) * kWave;
-                const uint64_t before = __ballot(len > 0 && excl <= base);
+                const uint64_t before = ballot(start <= base);
                 ob[u] = before ? 63 - __clzll(before) : 0;
                 const int last = (base + kWave < tot ? base + kWave : tot) - 1;
                 fast = fast && (lb + u >= lb1 || __builtin_amdgcn_readlane(incl, ob[u]) > last);

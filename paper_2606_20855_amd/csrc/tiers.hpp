@@ -134,7 +134,7 @@ __global__ void __launch_bounds__(256) tiny_kernel(Mats<V> M, const int32_t *__r
         }
     }
     const bool tail = key != kPadKey && (sl == S - 1 || nxt != key);
-    const uint64_t bal = __ballot(tail);
+    const uint64_t bal = ballot(tail);
     const int gbase = ln & ~(S - 1);
     const uint64_t gmask = (S == 64) ? ~0ull : (((1ull << S) - 1ull) << gbase);
     const uint64_t mine = bal & gmask;
@@ -510,7 +510,7 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
             bool set;
             if (SENT) set = static_cast<uint64_t>(__double_as_longlong(acc[loc])) != kNegZero;
             else set = (bm[loc >> 5] >> (loc & 31)) & 1u;
-            occ[c] = __ballot(set);
+            occ[c] = ballot(set);
             cnt += __popcll(occ[c]);
         }
         if (ln == 0) wave_cnt[wv] = cnt;
@@ -792,7 +792,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 if (n < 0) n = 0;
                 const int k0 = r - r0;   // this lane's first slot
                 const int cbase = static_cast<int>(col0) + wd * 32;
-                for (int i = 0; __ballot(i < n) != 0ull; i += 4) {
+                for (int i = 0; ballot(i < n) != 0ull; i += 4) {
                     if (i < n) {
                         int cv[4];
 #pragma unroll
