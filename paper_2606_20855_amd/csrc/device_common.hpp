@@ -208,11 +208,12 @@ __device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOM
 // locate the A entries of blocks that span several of them. It must hold -1
 // everywhere before the first call; for_each_product_wg leaves it that way.
 constexpr int kScalarOwners = 8;      // entries per block resolved with scalar reads
-constexpr int kMarkInts = 2 * kWave;  // marks of up to two blocks
+constexpr int kMarkInts = 2 * kWave;   // short-row iteration: marks of two blocks at once
+constexpr int kMarkIntsLong = kWave;   // long-row iteration: one block at a time
 
-// Sets this wave's mark array (kMarkInts ints) to -1.
-__device__ __forceinline__ void init_marks(int32_t *mark) {
-    for (int i = lane_id(); i < kMarkInts; i += kWave) mark[i] = -1;
+// Sets this wave's mark array (n ints) to -1.
+__device__ __forceinline__ void init_marks(int32_t *mark, int n = kMarkInts) {
+    for (int i = lane_id(); i < n; i += kWave) mark[i] = -1;
     wave_lds_fence();
 }
 

@@ -394,14 +394,14 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     constexpr int NW = BLOCK / kWave;
     __shared__ uint32_t bm[NWORDS];
     __shared__ int32_t scratch[NW];
-    __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
-    int32_t *mark = marks + wv * kMarkInts;
-    init_marks(mark);
+    int32_t *mark = marks + wv * kMarkIntsLong;
+    init_marks(mark, kMarkIntsLong);
     __syncthreads();
     for_each_product_wg<BLOCK, float, false, true>(
         M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1], BRowRange{M.b_rp}, M.b_col, nullptr, mark, ctot,
@@ -602,7 +602,7 @@ struct RankShape {
     static constexpr int REGION_COLS = REGION_WORDS * 32;
     static constexpr int REGION_WINS = REGION_COLS / kRankWinCols;
     static constexpr bool PACKED = sizeof(V) == 4;
-    static constexpr int CAP = PACKED ? 10240 : 6656;
+    static constexpr int CAP = PACKED ? 10944 : 7296;
     static constexpr int STAGE = PACKED ? 1 : CAP;   // separate column stage (ints)
     static_assert(REGION_COLS % kRankWinCols == 0, "regions hold whole windows");
     static_assert(REGION_WORDS % (BLOCK / kWave * kWave) == 0, "prefix scan takes whole word rows per wave");
@@ -646,7 +646,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ double acc[CAP];
     __shared__ int32_t stage[SH::STAGE];
     __shared__ int32_t scratch[NW];
-    __shared__ int32_t marks[NW * kMarkInts];
+    __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
     __shared__ double e_av[kCacheEntries];
@@ -661,8 +661,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     EntryCache ecache{e_col, e_bs, e_len, e_av, false};
     const int slot = slot_of_row != nullptr ? uniform(slot_of_row[row]) : -1;
     const uint32_t *cached = slot >= 0 ? cache + static_cast<int64_t>(slot) * row_words : nullptr;
-    int32_t *mark = marks + wv * kMarkInts;
-    init_marks(mark);
+    int32_t *mark = marks + wv * kMarkIntsLong;
+    init_marks(mark, kMarkIntsLong);
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
 
     int64_t out = 0;   // entries of the row emitted in earlier regions
