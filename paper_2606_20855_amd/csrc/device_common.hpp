@@ -449,17 +449,17 @@ struct EntryCache {
 //   2. one wave scans the counts into block offsets (ctot, in LDS);
 //   3. the blocks are shared out. For short rows (LONG false) wave w takes
 //      the contiguous range [w*nb/NW, (w+1)*nb/NW). For long rows waves claim
-//      units of kUnitBlocks consecutive blocks from an LDS counter until none
-//      are left: a block costs more where slices are short (entry boundaries
-//      inside blocks) than inside a long slice, so claiming small units keeps
-//      the waves finishing together (on short rows the claims would cost more
-//      than they save). Either way a wave moves forward through the chunks,
-//      keeping its current one in registers.
+//      runs of consecutive blocks from an LDS counter until none are left: a
+//      block costs more where slices are short (entry boundaries inside
+//      blocks) than inside a long slice, so claiming keeps the waves finishing
+//      together (on short rows the claims would cost more than they save).
+//      Either way a wave moves forward through the chunks, keeping its current
+//      one in registers.
 // LONG also selects the general-step shape (see chunk_blocks).
 // All threads of the workgroup must call it. ctot holds kCtotInts ints of LDS.
 constexpr int kMaxChunks = 256;
 constexpr int kCtotInts = kMaxChunks + 2;   // block offsets, total, claim counter
-constexpr int kUnitBlocks = 8;
+constexpr int kUnitBlocks = 4;
 
 template <int BLOCK, typename V, bool VALUES, bool LONG = false, typename RangeF, typename Visit>
 __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ a_col,
@@ -557,15 +557,20 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
             }
         };
         if constexpr (LONG) {
-            // 3. claimed units of blocks
-            const int nunits = (nb + kUnitBlocks - 1) / kUnitBlocks;
+            // 3. claimed runs of blocks, guided: a claim takes about 1/(2 NW) of what was left at the wave's
+            //    previous claim (a multiple of kUnitBlocks, at least kUnitBlocks), so claims are few while much
+            //    remains and small near the end, where the last wave to finish sets the pass's time
+            int seen = 0;   // claim position this wave saw last
             while (true) {
-                int u = 0;
-                if (ln == 0) u = atomicAdd(claim, 1);
-                u = uniform(u);
-                if (u >= nunits) break;
-                const int b = u * kUnitBlocks;
-                run(b, nb - b < kUnitBlocks ? nb : b + kUnitBlocks);
+                int sz = (nb - seen) / (2 * NW);
+                sz = (sz + kUnitBlocks - 1) / kUnitBlocks * kUnitBlocks;
+                if (sz < kUnitBlocks) sz = kUnitBlocks;
+                int b = 0;
+                if (ln == 0) b = atomicAdd(claim, sz);
+                b = uniform(b);
+                if (b >= nb) break;
+                seen = b + sz;
+                run(b, nb - b < sz ? nb : b + sz);
             }
         } else {
             // 3. this wave's even share of the blocks
