@@ -72,6 +72,14 @@ def er(m: int, n: int, r: int, seed, dtype=np.float64, dist: str = "pm1") -> CSR
     if r > n:
         raise ValueError("r > n")
     rng = _rng(seed)
+    if r * r > n:
+        # a row of r independent draws would almost surely repeat a column:
+        # draw each row without replacement instead
+        cols = np.stack([np.sort(rng.choice(n, size=r, replace=False)) for _ in range(m)]).astype(np.int64)
+        cols = cols.reshape(m, r)
+        rp = (np.arange(m + 1, dtype=np.int64) * r).astype(np.int32)
+        val = _values(rng, m * r, dist, dtype)
+        return CSR(m, n, rp, cols.reshape(-1).astype(np.int32), val)
     cols = np.sort(rng.integers(0, n, size=(m, r), dtype=np.int64), axis=1)
     # redraw rows that picked a column twice until every row is distinct
     while True:

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <type_traits>
+#include <utility>
 
 namespace wsp {
 
@@ -430,8 +431,17 @@ struct EntryCache {
     int32_t *bs = nullptr;
     int32_t *len = nullptr;
     double *av = nullptr;
-    bool col_ready = false;
+    bool col_ready = false;    // col holds the entries' columns
+    bool vals_ready = false;   // av holds the entries' values
 };
+
+// A range functor with a member cached(k, ci) gives the slices of entries held
+// in the entry cache from there (ci: the entry's cache index) instead of from
+// memory.
+template <typename R, typename = void>
+struct has_cached_bounds : std::false_type {};
+template <typename R>
+struct has_cached_bounds<R, std::void_t<decltype(std::declval<const R &>().cached(0, 0))>> : std::true_type {};
 
 // Visits every product a * b of A entries [a_lo, a_hi) of one row: visit(col,
 // prod) with col = B.col_idx[b] and prod = A.val[a] * B.val[b] formed in double
@@ -486,14 +496,20 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                 if (cached && cache.col_ready) k = cache.col[ci];
                 else k = a_col[a];
                 double av = 0.0;
-                if (VALUES && cached) av = to_d(a_val[a]);
-                const int2 r = range(k);
+                if (VALUES && cached && !cache.vals_ready) av = to_d(a_val[a]);
+                int2 r;
+                if constexpr (has_cached_bounds<RangeF>::value) {
+                    if (cached && cache.col_ready) r = range.cached(k, ci);
+                    else r = range(k);
+                } else {
+                    r = range(k);
+                }
                 len = r.y - r.x;
                 if (cached) {
                     if (!cache.col_ready) cache.col[ci] = k;
                     cache.bs[ci] = r.x;
                     cache.len[ci] = len;
-                    if (VALUES) cache.av[ci] = av;
+                    if (VALUES && !cache.vals_ready) cache.av[ci] = av;
                 }
             } else if (cached) {
                 cache.bs[ci] = 0;

@@ -243,13 +243,88 @@ __device__ int64_t rank_emit(const int32_t *keys, const double *vals, int T, int
     return out;
 }
 
+// Writes the entries a workgroup holds in registers (thread t: keys kk[j] and
+// sums vv[j], kEmptyKey where none) to C[cb + ...] in increasing column order
+// without sorting them. The columns [0, ncols) are covered in windows of BWW*32
+// columns; for each, the window's keys are marked in a presence bitmap, the
+// words are grouped by eight, the groups' exclusive prefix counts are taken,
+// and every entry's position is its group's offset plus the set bits before it
+// in its group. bm holds BWW words (16-byte aligned) and goff BWW/8 ints. Writes
+// never reach past C[cb + seg). Returns the number of entries (uniform).
+template <int BLOCK, int BWW, int PER, typename V>
+__device__ int64_t rank_emit_regs(const int32_t (&kk)[PER], const double (&vv)[PER], int64_t ncols, uint32_t *bm,
+                                  int32_t *goff, int32_t *scratch, int32_t *__restrict__ c_col,
+                                  V *__restrict__ c_val, int64_t cb, int64_t seg) {
+    constexpr int64_t SPAN = int64_t(BWW) * 32;
+    static_assert(BWW % 8 == 0, "whole groups of eight words");
+    int64_t out = 0;
+    for (int64_t wb = 0; wb < ncols; wb += SPAN) {
+        const int span = static_cast<int>((ncols - wb) < SPAN ? (ncols - wb) : SPAN);
+        const int ngroups = (span + 255) >> 8;
+        for (int i = threadIdx.x; i < ngroups * 8; i += BLOCK) bm[i] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int k = kk[j];
+            if (k != kEmptyKey && k >= wb && k - wb < span) {
+                const int rel = static_cast<int>(k - wb);
+                atomicOr(&bm[rel >> 5], 1u << (rel & 31));
+            }
+        }
+        __syncthreads();
+        int carry = 0;
+        for (int g0 = 0; g0 < ngroups; g0 += BLOCK) {
+            const int g = g0 + threadIdx.x;
+            int cnt = 0;
+            if (g < ngroups) {
+                const uint4 lo = reinterpret_cast<const uint4 *>(bm)[2 * g];
+                const uint4 hi = reinterpret_cast<const uint4 *>(bm)[2 * g + 1];
+                cnt = __popc(lo.x) + __popc(lo.y) + __popc(lo.z) + __popc(lo.w) + __popc(hi.x) + __popc(hi.y) +
+                      __popc(hi.z) + __popc(hi.w);
+            }
+            int tot;
+            const int ex = block_excl_scan<BLOCK>(cnt, &tot, scratch);
+            if (g < ngroups) goff[g] = carry + ex;
+            carry += tot;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int k = kk[j];
+            if (k != kEmptyKey && k >= wb && k - wb < span) {
+                const int rel = static_cast<int>(k - wb);
+                const int word = rel >> 5;
+                const uint4 lo = reinterpret_cast<const uint4 *>(bm)[(word >> 3) * 2];
+                const uint4 hi = reinterpret_cast<const uint4 *>(bm)[(word >> 3) * 2 + 1];
+                const uint32_t w8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+                const int wi = word & 7;
+                int r = goff[word >> 3];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const uint32_t m = i < wi ? 0xffffffffu : (i == wi ? (1u << (rel & 31)) - 1u : 0u);
+                    r += __popc(w8[i] & m);
+                }
+                const int64_t pos = out + r;
+                if (pos < seg) {
+                    c_col[cb + pos] = k;
+                    c_val[cb + pos] = static_cast<V>(vv[j]);
+                }
+            }
+        }
+        out += carry;
+        __syncthreads();
+    }
+    return out;
+}
+
 // ---------------------------------------------------------------------------
 // Hash tier: one workgroup per row, an LDS table of 2^LOG2T slots.
 // Symbolic keeps keys only and counts first insertions. Numeric also adds the
-// product into the slot's double, then writes the row in column order: large
-// tables by rank emission (presence bitmap + popcount ranks, no sort) when the
+// product into the slot's double, then writes the row in column order: tables
+// of 1024 slots and more by rank emission (the slots move to registers and the
+// table's memory takes the presence bitmap; popcount ranks, no sort) when the
 // column space takes at most kMaxRankWindows bitmap windows, otherwise (and
-// for small tables) by compacting the slots and bitonic-sorting them in LDS.
+// for smaller tables) by compacting the slots and bitonic-sorting them in LDS.
 // ---------------------------------------------------------------------------
 constexpr int kMaxRankWindows = 4;
 
@@ -257,8 +332,8 @@ template <int LOG2T>
 struct HashShape {
     static constexpr int T = 1 << LOG2T;
     static constexpr int BLOCK = T <= 256 ? 64 : (T <= 512 ? 128 : (T <= 2048 ? 256 : (T <= 4096 ? 512 : 1024)));
-    // bitmap words for rank emission (0: always sort)
-    static constexpr int BWW = LOG2T >= 13 ? 8192 : (LOG2T >= 11 ? 2048 : 0);
+    // bitmap words for rank emission, held in the T doubles of the table (0: always sort)
+    static constexpr int BWW = LOG2T >= 10 ? 2 * T : 0;
 };
 
 template <int LOG2T, typename V, bool NUM>
@@ -274,9 +349,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     constexpr int NW = BLOCK / kWave;
     static_assert(T >= BLOCK, "table smaller than block");
     __shared__ int32_t keys[T];
-    __shared__ double vals[NUM ? T : 1];
-    __shared__ uint32_t bm[BWW > 0 ? BWW : 1];
-    __shared__ int32_t goff[BWW > 0 ? BWW / 8 : 1];
+    __shared__ __align__(16) double vals[NUM ? T : 1];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
     __shared__ int32_t ctot[kCtotInts];
@@ -311,17 +384,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
 
     const int64_t cb = c_rp[row];
     const int64_t seg = c_rp[row + 1] - cb;
-    if constexpr (BWW > 0) {
-        const int64_t nbw = (ncols + int64_t(BWW) * 32 - 1) / (int64_t(BWW) * 32);
-        if (nbw <= kMaxRankWindows) {
-            const int64_t total = rank_emit<BLOCK, BWW, V>(keys, vals, T, 0, ncols, bm, goff, scratch, c_col,
-                                                           c_val, cb, 0, seg);
-            if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
-            return;
-        }
-    }
-
-    // compact occupied slots to the front of the table
+    // the thread's slots, in registers
     constexpr int PER = T / BLOCK;
     int kk[PER];
     double vv[PER];
@@ -333,6 +396,19 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
         vv[j] = vals[s2];
         cnt += kk[j] != kEmptyKey;
     }
+    if constexpr (BWW > 0) {
+        const int64_t nbw = (ncols + int64_t(BWW) * 32 - 1) / (int64_t(BWW) * 32);
+        if (nbw <= kMaxRankWindows) {
+            __syncthreads();   // every slot is read: the table's memory takes the bitmap and the group offsets
+            static_assert(BWW <= 2 * T && BWW / 8 <= T, "bitmap in the doubles, group offsets in the keys");
+            const int64_t total = rank_emit_regs<BLOCK, BWW, PER, V>(
+                kk, vv, ncols, reinterpret_cast<uint32_t *>(vals), keys, scratch, c_col, c_val, cb, seg);
+            if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+            return;
+        }
+    }
+
+    // compact occupied slots to the front of the table
     int total;
     int pos = block_excl_scan<BLOCK>(cnt, &total, scratch);
 #pragma unroll
@@ -602,7 +678,7 @@ struct RankShape {
     static constexpr int REGION_COLS = REGION_WORDS * 32;
     static constexpr int REGION_WINS = REGION_COLS / kRankWinCols;
     static constexpr bool PACKED = sizeof(V) == 4;
-    static constexpr int CAP = PACKED ? 10944 : 7296;
+    static constexpr int CAP = PACKED ? 10864 : 7232;
     static constexpr int STAGE = PACKED ? 1 : CAP;   // separate column stage (ints)
     static_assert(REGION_COLS % kRankWinCols == 0, "regions hold whole windows");
     static_assert(REGION_WORDS % (BLOCK / kWave * kWave) == 0, "prefix scan takes whole word rows per wave");
@@ -627,6 +703,33 @@ struct RankAccumulate : TwoPhaseVisit {
     __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
 };
 
+// Part of B row k inside the windows [w, w_end) of a rank slice. An entry held
+// in the entry cache starts the pass with its slice of the previous pass there
+// (for the first pass of a region, the whole region), and its region end in
+// e_hi: the new bounds come from those where the slice boundary allows
+// (lo_from 0: the previous start, 1: the previous end; hi_from 0: the previous
+// end, 1: the region end; 2 for either: the window table), so most passes read
+// nothing from memory for the cached entries.
+struct SliceRange {
+    const int32_t *wtab;
+    int64_t stride;
+    int w, w_end;
+    int lo_from, hi_from;
+    const int32_t *e_bs, *e_len, *e_hi;
+    __device__ __forceinline__ int2 operator()(int32_t k) const {
+        const int32_t *t = wtab + static_cast<int64_t>(k) * stride;
+        return make_int2(t[w], t[w_end]);
+    }
+    __device__ __forceinline__ int2 cached(int32_t k, int ci) const {
+        const int bs = e_bs[ci];
+        const int be = bs + e_len[ci];
+        const int32_t *t = wtab + static_cast<int64_t>(k) * stride;
+        const int lo = lo_from == 0 ? bs : lo_from == 1 ? be : t[w];
+        const int hi = hi_from == 0 ? be : hi_from == 1 ? e_hi[ci] : t[w_end];
+        return make_int2(lo, hi);
+    }
+};
+
 // When slot_of_row is not null, a row with slot_of_row[row] >= 0 takes its
 // column bitmap from that row of the structure cache (written by the symbolic
 // phase for the same A and B) instead of running the structure pass.
@@ -648,7 +751,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
-    __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
+    __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries], e_hi[kCacheEntries];
     __shared__ double e_av[kCacheEntries];
 
     const int row = rows[blockIdx.x];
@@ -672,20 +775,42 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         const int ncw = static_cast<int>(ncols - col0 < SH::REGION_COLS ? ncols - col0 : SH::REGION_COLS);
         const int nwords = (ncw + 31) >> 5;
         // 1. structure: the cached bitmap, or a structure pass (a region covering every column takes whole B
-        //    rows, whose bounds come from B's row pointers rather than the larger window table)
+        //    rows, whose bounds come from B's row pointers rather than the larger window table). Either way the
+        //    entry cache ends up holding each cached entry's column, value and part of B in the region.
+        // Wave w owns words [w*RW/NW, (w+1)*RW/NW) in the prefix scan below, read one 64-word row at a time.
+        const int wbase = wv * (RW / NW);
+        uint32_t bits[WROWS];
         if (cached != nullptr) {
-            // all of a thread's words are loaded before any is stored, so the loads are in flight together
-            const uint32_t *src = cached + static_cast<int64_t>(rg0) * WIN_WORDS;
-            constexpr int PER = RW / BLOCK;
-            uint32_t wd[PER];
-#pragma unroll
-            for (int q = 0; q < PER; ++q) {
-                const int i = q * BLOCK + static_cast<int>(threadIdx.x);
-                wd[q] = i < nwords ? __builtin_nontemporal_load(&src[i]) : 0u;
+            // the entries first (their loads then overlap the bitmap's), then the words this wave scans, all
+            // loaded before any is used
+            int k = 0, lo = 0, hi = 0;
+            double av = 0.0;
+            const int ci = static_cast<int>(threadIdx.x);
+            const bool has_entry = ci < kCacheEntries && a_lo + ci < a_hi;
+            if (has_entry) {
+                k = ecache.col_ready ? e_col[ci] : M.a_col[a_lo + ci];
+                if (!ecache.vals_ready) av = to_d(M.a_val[a_lo + ci]);
             }
+            const uint32_t *src = cached + static_cast<int64_t>(rg0) * WIN_WORDS;
 #pragma unroll
-            for (int q = 0; q < PER; ++q) bw[q * BLOCK + threadIdx.x].x = wd[q];
-            __syncthreads();
+            for (int q = 0; q < WROWS; ++q) {
+                const int i = wbase + q * kWave + ln;
+                bits[q] = i < nwords ? __builtin_nontemporal_load(&src[i]) : 0u;
+            }
+            if (has_entry) {
+                const int32_t *t = wtab + static_cast<int64_t>(k) * stride;
+                lo = t[rg0];
+                hi = t[rg1];
+            }
+            if (ci < kCacheEntries) {
+                if (!ecache.col_ready) e_col[ci] = k;
+                if (!ecache.vals_ready) e_av[ci] = av;
+                e_bs[ci] = lo;
+                e_len[ci] = hi - lo;
+                e_hi[ci] = hi;
+            }
+            ecache.col_ready = true;
+            ecache.vals_ready = true;
         } else {
             for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
             __syncthreads();
@@ -701,16 +826,19 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                                                            BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val,
                                                            mark, ctot, mark_col, ecache);
             ecache.col_ready = true;
+            // the pass left each cached entry's region part in e_bs / e_len (written by this same thread)
+            if (threadIdx.x < kCacheEntries) e_hi[threadIdx.x] = e_bs[threadIdx.x] + e_len[threadIdx.x];
+#pragma unroll
+            for (int q = 0; q < WROWS; ++q) bits[q] = bw[wbase + q * kWave + ln].x;
         }
-        // 2. exclusive popcount prefix: wave w owns words [w*RW/NW, (w+1)*RW/NW), read one 64-word row at a
-        //    time (lane-contiguous, so free of bank conflicts)
+        // 2. exclusive popcount prefix (lane-contiguous rows, so free of bank conflicts); each word is stored
+        //    with its prefix
         {
-            const int wbase = wv * (RW / NW);
             uint32_t cnt[WROWS];
             int wtot = 0;
 #pragma unroll
             for (int q = 0; q < WROWS; ++q) {
-                cnt[q] = __popc(bw[wbase + q * kWave + ln].x);
+                cnt[q] = __popc(bits[q]);
                 wtot += static_cast<int>(cnt[q]);
             }
             wtot = __builtin_amdgcn_readlane(wave_incl_sum(wtot), kWave - 1);
@@ -722,7 +850,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
 #pragma unroll
             for (int q = 0; q < WROWS; ++q) {
                 const int inc = wave_incl_sum(static_cast<int>(cnt[q]));
-                bw[wbase + q * kWave + ln].y = static_cast<uint32_t>(run + inc - static_cast<int>(cnt[q]));
+                bw[wbase + q * kWave + ln] = make_uint2(bits[q], static_cast<uint32_t>(run + inc - static_cast<int>(cnt[q])));
                 run += __builtin_amdgcn_readlane(inc, kWave - 1);
             }
         }
@@ -740,17 +868,23 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                                                                    : region_total;
         auto rank_at_window = [&](int jw) -> int { return __builtin_amdgcn_readlane(win_rank, jw); };
         int j = 0;
-        int r0 = 0;   // first rank of the current slice
+        int r0 = 0;          // first rank of the current slice
+        int pj = 0, pj2 = nwr;   // windows of the slices the entry cache holds (first: the whole region)
         while (j < nwr) {
             int j2 = j + 1;
             while (j2 < nwr && rank_at_window(j2 + 1) - r0 <= CAP) ++j2;
             const int rend_w = rank_at_window(j2);
             const int r1 = rend_w - r0 > CAP ? r0 + CAP : rend_w;    // this slice covers ranks [r0, r1)
             // values
+            const int lo_from = j == pj ? 0 : j == pj2 ? 1 : 2;
+            const int hi_from = j2 == pj2 ? 0 : j2 == nwr ? 1 : 2;
             for_each_product_wg<BLOCK, V, true, true>(
-                M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0 + j, rg0 + j2}, M.b_col, M.b_val, mark,
-                ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1}, ecache);
-            ecache.col_ready = true;
+                M.a_col, M.a_val, a_lo, a_hi,
+                SliceRange{wtab, stride, rg0 + j, rg0 + j2, lo_from, hi_from, e_bs, e_len, e_hi}, M.b_col, M.b_val,
+                mark, ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1}, ecache);
+            ecache.vals_ready = true;
+            pj = j;
+            pj2 = j2;
             if constexpr (SH::PACKED) {
                 // float output: round each accumulator once and keep the float in the high half of its own
                 // 8-byte slot, so the staging below only writes (it never waits on an accumulator read)

@@ -171,6 +171,31 @@ def test_dense_rows_across_regions(dtype, opts):
     assert num["rows"]["dense"] > 0
 
 
+@pytest.mark.parametrize("r", [25, 50, 90])
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_hash_rows_rank_emission_windows(r, dtype):
+    # hash rows of ~20r entries over 200K columns: tables of 1024, 2048 and
+    # 4096 slots write their rows in 4, 2 and 1 bitmap windows (the last one
+    # ragged)
+    dist = "pm1" if dtype == np.float64 else "open01"
+    A = matgen.er(64, 3000, r, seed=70 + r, dtype=dtype, dist=dist)
+    B = matgen.er(3000, 200_000, 20, seed=69, dtype=dtype, dist=dist)
+    got, sym, num, ref = check(A, B, None, what=f"hash windows r={r}")
+    assert num["rows"]["hash"] == 64
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_dense_rows_beyond_entry_cache(dtype):
+    # 400 A entries per row, more than the 256 whose bounds the rank kernel
+    # keeps in LDS, and ~11,600 entries per row over 300K columns: two regions,
+    # each taken in one or more rank slices
+    dist = "pm1" if dtype == np.float64 else "open01"
+    A = matgen.er(32, 3000, 400, seed=61, dtype=dtype, dist=dist)
+    B = matgen.er(3000, 300_000, 30, seed=62, dtype=dtype, dist=dist)
+    got, sym, num, ref = check(A, B, None, what="long A rows")
+    assert num["rows"]["dense"] == 32
+
+
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
 def test_rank_slices_inside_one_window(dtype):
     # ~8,600 entries per row, ~7,800 of them inside the first 8192-column

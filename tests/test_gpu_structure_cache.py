@@ -133,3 +133,24 @@ def test_other_layout_recomputes():
     got, num = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, other)
     assert num["structure_cache_rows"] == 0
     assert_matches(got, oracle.spgemm(A, A), A.val.dtype, what="other layout")
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+def test_long_rows_cached_and_fresh(dtype):
+    # rows with more A entries than the rank kernel keeps in LDS, several rank
+    # slices and two 262144-column regions: the cached bitmap and the
+    # structure pass give the same C
+    dist = "open01" if dtype == np.float32 else "pm1"
+    A = matgen.er(24, 2500, 300, seed=57, dtype=dtype, dist=dist)
+    B = matgen.er(2500, 280_000, 40, seed=58, dtype=dtype, dist=dist)
+    dA, dB = _dev(A), _dev(B)
+    wsb, nbytes = _workspace(dA, dB, {})
+    fresh, _ = _workspace(dA, dB, {})
+    c_rp, nnz = _symbolic(dA, dB, wsb, nbytes, {})
+    got, num = _numeric(dA, dB, c_rp, nnz, wsb, nbytes, {})
+    assert num["rows"]["dense"] == 24 and num["structure_cache_rows"] == 24
+    ref = oracle.spgemm(A, B)
+    assert_matches(got, ref, A.val.dtype, what="long rows, cached")
+    got2, num2 = _numeric(dA, dB, c_rp, nnz, fresh, nbytes, {})
+    assert num2["structure_cache_rows"] == 0
+    assert_matches(got2, ref, A.val.dtype, what="long rows, fresh")
