@@ -426,6 +426,104 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
 // calls one round trip in step 1 too. A null `col` disables the cache.
 constexpr int kCacheChunks = 4;
 constexpr int kCacheEntries = kCacheChunks * kWave;
+// Long rows: blocks aligned to entries. Entry e of a 64-entry chunk (lane e)
+// owns the ceil(len_e / 64) consecutive blocks from bstart_e, block k of the
+// entry taking products 64k .. 64k+63 of its slice (an entry's last block may
+// be partial). Every block thus has exactly one entry, found with one ballot,
+// and a step of kSpanBlocks full blocks of one entry is read with one address
+// computation. Processes blocks [lb0, lb1) of the chunk whose lanes hold
+// (bs, av, len, bstart, nblk). As in chunk_blocks every lane of a step loads
+// (a dead lane from its block's own entry), so the loads go out back to back.
+template <typename V, bool VALUES, typename Visit>
+__device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len, int bstart, int nblk, int lb0,
+                                                     int lb1, const int32_t *__restrict__ b_col,
+                                                     const V *__restrict__ b_val, Visit &visit) {
+    constexpr int SB = kSpanBlocks;
+    const int ln = lane_id();
+    // first block of the lane's entry, or INT_MAX for an entry without products
+    const int bfirst = nblk > 0 ? bstart : 0x7fffffff;
+    for (int lb = lb0; lb < lb1;) {
+        const uint64_t m0 = ballot(bfirst <= lb);
+        const int o = m0 ? 63 - __clzll(m0) : 0;
+        const int k = lb - __builtin_amdgcn_readlane(bstart, o);   // block of entry o
+        if (lb + SB <= lb1 && (k + SB) * kWave <= __builtin_amdgcn_readlane(len, o)) {
+            const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(bs, o)) + k * kWave;
+            const int32_t *cp = b_col + b0 + ln;
+            const V *vp = b_val + b0 + ln;
+            const double a = VALUES ? readlane_d(av, o) : 0.0;
+            int c[SB];
+            V v[SB];
+#pragma unroll
+            for (int u = 0; u < SB; ++u) {
+                c[u] = cp[u * kWave];
+                if (VALUES) v[u] = vp[u * kWave];
+            }
+            // keep the compiler from sinking a load into its use
+#pragma unroll
+            for (int u = 0; u < SB; ++u) {
+                asm volatile("" : "+v"(c[u]));
+                if (VALUES) asm volatile("" : "+v"(v[u]));
+            }
+            if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
+                int kk[SB];
+#pragma unroll
+                for (int u = 0; u < SB; ++u) kk[u] = visit.pre(c[u]);
+#pragma unroll
+                for (int u = 0; u < SB; ++u) visit.post(kk[u], VALUES ? a * to_d(v[u]) : 0.0);
+            } else {
+#pragma unroll
+                for (int u = 0; u < SB; ++u) visit(c[u], VALUES ? a * to_d(v[u]) : 0.0);
+            }
+            lb += SB;
+            continue;
+        }
+        // SB blocks, each inside one entry
+        int ix[SB];
+        double aval[SB];
+        bool live[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int b = lb + u;
+            live[u] = false;
+            ix[u] = 0;
+            aval[u] = 0.0;
+            if (b < lb1) {
+                const uint64_t m = ballot(bfirst <= b);
+                const int e = m ? 63 - __clzll(m) : 0;
+                const int p = (b - __builtin_amdgcn_readlane(bstart, e)) * kWave + ln;
+                live[u] = p < __builtin_amdgcn_readlane(len, e);
+                ix[u] = __builtin_amdgcn_readlane(bs, e) + (live[u] ? p : 0);
+                aval[u] = VALUES ? readlane_d(av, e) : 0.0;
+            }
+        }
+        int craw[SB];
+        V vraw[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            craw[u] = b_col[ix[u]];
+            if (VALUES) vraw[u] = b_val[ix[u]];
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            asm volatile("" : "+v"(craw[u]));
+            if (VALUES) asm volatile("" : "+v"(vraw[u]));
+        }
+        if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
+            int kk[SB];
+#pragma unroll
+            for (int u = 0; u < SB; ++u) kk[u] = live[u] ? visit.pre(craw[u]) : -1;
+#pragma unroll
+            for (int u = 0; u < SB; ++u) visit.post(kk[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < SB; ++u) {
+                if (live[u]) visit(craw[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+            }
+        }
+        lb += SB;
+    }
+}
+
 struct EntryCache {
     int32_t *col = nullptr;
     int32_t *bs = nullptr;
@@ -465,13 +563,17 @@ struct has_cached_bounds<R, std::void_t<decltype(std::declval<const R &>().cache
 //      together (on short rows the claims would cost more than they save).
 //      Either way a wave moves forward through the chunks, keeping its current
 //      one in registers.
-// LONG also selects the general-step shape (see chunk_blocks).
+// LONG also selects the general-step shape (see chunk_blocks). ALIGNED (for
+// visits over whole B rows, where slices are long) replaces the flattening by
+// entry-aligned blocks (see chunk_blocks_aligned): more blocks, but never a
+// block shared by two entries.
 // All threads of the workgroup must call it. ctot holds kCtotInts ints of LDS.
 constexpr int kMaxChunks = 256;
 constexpr int kCtotInts = kMaxChunks + 2;   // block offsets, total, claim counter
 constexpr int kUnitBlocks = 4;
 
-template <int BLOCK, typename V, bool VALUES, bool LONG = false, typename RangeF, typename Visit>
+template <int BLOCK, typename V, bool VALUES, bool LONG = false, bool ALIGNED = false, typename RangeF,
+          typename Visit>
 __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ a_col,
                                                     const V *__restrict__ a_val, int a_lo, int a_hi,
                                                     RangeF range, const int32_t *__restrict__ b_col,
@@ -516,8 +618,14 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                 cache.len[ci] = 0;
                 if (VALUES) cache.av[ci] = 0.0;
             }
-            const int tot = __builtin_amdgcn_readlane(wave_incl_sum(len), kWave - 1);
-            if (ln == 0) ctot[c] = (tot + kWave - 1) / kWave;
+            if constexpr (ALIGNED) {
+                // entry-aligned blocks: each entry rounds up to whole blocks
+                const int nbc = __builtin_amdgcn_readlane(wave_incl_sum((len + kWave - 1) / kWave), kWave - 1);
+                if (ln == 0) ctot[c] = nbc;
+            } else {
+                const int tot = __builtin_amdgcn_readlane(wave_incl_sum(len), kWave - 1);
+                if (ln == 0) ctot[c] = (tot + kWave - 1) / kWave;
+            }
         }
         if (threadIdx.x == 0) *claim = 0;
         __syncthreads();
@@ -537,7 +645,8 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
         const int nb = uniform(ctot[nch]);
         // a wave's chunk, held in registers, and its block range
         int c = -1, cb0 = 0, cb1 = 0;
-        int boff = 0, len = 0, incl = 0, tot = 0;
+        int boff = 0, len = 0, incl = 0, tot = 0;   // flattened blocks
+        int bs = 0, bstart = 0, nblk = 0;            // entry-aligned blocks
         double av = 0.0;
         // processes blocks [b, e) of the group, moving forward through the chunks
         auto run = [&](int b, int e) {
@@ -549,7 +658,7 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                     cb0 = uniform(ctot[c]);
                     cb1 = uniform(ctot[c + 1]);
                     const int a = g0 + c * kWave + ln;
-                    int bs = 0;
+                    bs = 0;
                     len = 0;
                     av = 0.0;
                     if (use_cache && c < kCacheChunks) {
@@ -563,12 +672,21 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                         len = r.y - r.x;
                         if (VALUES) av = to_d(a_val[a]);
                     }
-                    incl = wave_incl_sum(len);
-                    tot = __builtin_amdgcn_readlane(incl, kWave - 1);
-                    boff = bs - (incl - len);
+                    if constexpr (ALIGNED) {
+                        nblk = (len + kWave - 1) / kWave;
+                        bstart = wave_incl_sum(nblk) - nblk;
+                    } else {
+                        incl = wave_incl_sum(len);
+                        tot = __builtin_amdgcn_readlane(incl, kWave - 1);
+                        boff = bs - (incl - len);
+                    }
                 }
                 const int ee = cb1 < e ? cb1 : e;
-                chunk_blocks<V, VALUES, LONG>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark, visit);
+                if constexpr (ALIGNED)
+                    chunk_blocks_aligned<V, VALUES>(bs, av, len, bstart, nblk, b - cb0, ee - cb0, b_col, b_val, visit);
+                else
+                    chunk_blocks<V, VALUES, LONG>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark,
+                                                  visit);
                 b = ee;
             }
         };

@@ -479,7 +479,7 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     int32_t *mark = marks + wv * kMarkIntsLong;
     init_marks(mark, kMarkIntsLong);
     __syncthreads();
-    for_each_product_wg<BLOCK, float, false, true>(
+    for_each_product_wg<BLOCK, float, false, true, true>(
         M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1], BRowRange{M.b_rp}, M.b_col, nullptr, mark, ctot,
         [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); },
         EntryCache{e_col, e_bs, e_len, nullptr, false});
@@ -751,6 +751,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
+    __shared__ int32_t sclaim;   // staging's group counter
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries], e_hi[kCacheEntries];
     __shared__ double e_av[kCacheEntries];
 
@@ -767,6 +768,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     int32_t *mark = marks + wv * kMarkIntsLong;
     init_marks(mark, kMarkIntsLong);
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
+    if (threadIdx.x == 0) sclaim = 0;
 
     int64_t out = 0;   // entries of the row emitted in earlier regions
     for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
@@ -819,10 +821,10 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
             };
             if (nwin <= SH::REGION_WINS)
-                for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col,
+                for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col,
                                                            M.b_val, mark, ctot, mark_col, ecache);
             else
-                for_each_product_wg<BLOCK, V, false, true>(M.a_col, M.a_val, a_lo, a_hi,
+                for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi,
                                                            BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val,
                                                            mark, ctot, mark_col, ecache);
             ecache.col_ready = true;
@@ -894,26 +896,24 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 }
                 __syncthreads();
             }
-            // stage ranks [r0, r1) in rank order, one bitmap word per lane: the windows' words are cut into
-            // 64-word groups dealt round-robin to the waves (dense column ranges, where words hold many
-            // entries, are thus spread over all waves). A word's entries hold consecutive ranks; a lane stages
-            // them four per step (the wave loops while any lane has entries left), so the cost follows the
-            // entries, not the columns. Every rank is staged by exactly one lane.
+            // stage ranks [r0, r1) in rank order, one bitmap word per lane: the waves claim the windows' words
+            // in 64-word groups from an LDS counter, so the waves holding dense groups (many entries per word)
+            // take fewer of them and all finish together. A word's entries hold consecutive ranks; a lane
+            // stages them four per step (the wave loops while any lane has entries left), so the cost follows
+            // the entries, not the columns. Every rank is staged by exactly one lane.
             const int wa = j * WIN_WORDS;
             const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
-            // a wave holds at most RW / NW / 64 groups: read them all before staging
-            constexpr int MAXG = RW / NW / kWave;
-            uint2 ew[MAXG];
-#pragma unroll
-            for (int g = 0; g < MAXG; ++g) {
-                const int wd = wa + (g * NW + wv) * kWave + ln;
-                ew[g] = wd < wb ? bw[wd] : make_uint2(0u, 0u);
-            }
-#pragma unroll
-            for (int g = 0; g < MAXG; ++g) {
-                if (wa + (g * NW + wv) * kWave >= wb) break;
-                const int wd = wa + (g * NW + wv) * kWave + ln;
-                const uint2 e = ew[g];
+            int gnext = 0;
+            if (ln == 0) gnext = atomicAdd(&sclaim, 1);
+            gnext = uniform(gnext);
+            while (true) {
+                const int g = gnext;
+                if (wa + g * kWave >= wb) break;
+                const int wd = wa + g * kWave + ln;
+                const uint2 e = wd < wb ? bw[wd] : make_uint2(0u, 0u);
+                // the next claim is in flight while this group is staged
+                if (ln == 0) gnext = atomicAdd(&sclaim, 1);
+                gnext = uniform(gnext);
                 uint32_t wbits = e.x;
                 int r = static_cast<int>(e.y);
                 // drop the entries below r0
@@ -970,6 +970,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                     __builtin_nontemporal_store(v, &c_val[cb + pbase + i]);
                 }
             }
+            if (threadIdx.x == 0) sclaim = 0;   // every wave has left the staging loop
             __syncthreads();
             r0 = r1;
             if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
