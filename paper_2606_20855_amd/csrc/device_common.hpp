@@ -226,7 +226,9 @@ __device__ __forceinline__ double readlane_d(double x, int lane) {
 
 // A visitor deriving from TwoPhaseVisit splits a visit into k = pre(col), a
 // lookup, and post(k, prod), the update; operator()(col, prod) must equal
-// post(pre(col), prod). Span steps then issue all lookups before any update.
+// post(pre(col), prod), and post(-1, prod) must do nothing. safe_col() is a
+// column pre() accepts whatever the visit. Steps then issue all lookups before
+// any update, and dead lanes look up safe_col() (no branch around a lookup).
 struct TwoPhaseVisit {};
 
 // Processes blocks [lb0, lb1) (block = 64 consecutive products) of one
@@ -405,9 +407,9 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
         if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
             int k[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) k[u] = live[u] ? visit.pre(craw[u]) : -1;
+            for (int u = 0; u < U; ++u) k[u] = visit.pre(live[u] ? craw[u] : visit.safe_col());
 #pragma unroll
-            for (int u = 0; u < U; ++u) visit.post(k[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+            for (int u = 0; u < U; ++u) visit.post(live[u] ? k[u] : -1, VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -511,9 +513,9 @@ __device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len,
         if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
             int kk[SB];
 #pragma unroll
-            for (int u = 0; u < SB; ++u) kk[u] = live[u] ? visit.pre(craw[u]) : -1;
+            for (int u = 0; u < SB; ++u) kk[u] = visit.pre(live[u] ? craw[u] : visit.safe_col());
 #pragma unroll
-            for (int u = 0; u < SB; ++u) visit.post(kk[u], VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
+            for (int u = 0; u < SB; ++u) visit.post(live[u] ? kk[u] : -1, VALUES ? aval[u] * to_d(vraw[u]) : 0.0);
         } else {
 #pragma unroll
             for (int u = 0; u < SB; ++u) {

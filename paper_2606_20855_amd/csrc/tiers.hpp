@@ -700,6 +700,7 @@ struct RankAccumulate : TwoPhaseVisit {
     __device__ __forceinline__ void post(int k, double prod) const {
         if (k >= 0) atomicAdd(&acc[k], prod);
     }
+    __device__ __forceinline__ int safe_col() const { return col0; }
     __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
 };
 
