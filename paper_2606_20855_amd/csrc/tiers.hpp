@@ -666,6 +666,7 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
 // of windows.
 // ---------------------------------------------------------------------------
 constexpr int kRankWinCols = 8192;
+constexpr int kStageStep = 2;   // entries a lane stages per step (measured best of 1..4 and 8 on R-MAT 18)
 
 // Shape: 1024 threads, regions of 8192 bitmap words (262144 columns), and a
 // rank accumulator of CAP doubles. With float output a staged entry (column,
@@ -900,8 +901,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             // stage ranks [r0, r1) in rank order, one bitmap word per lane: the waves claim the windows' words
             // in 64-word groups from an LDS counter, so the waves holding dense groups (many entries per word)
             // take fewer of them and all finish together. A word's entries hold consecutive ranks; a lane
-            // stages them four per step (the wave loops while any lane has entries left), so the cost follows
-            // the entries, not the columns. Every rank is staged by exactly one lane.
+            // stages them kStageStep per step (the wave loops while any lane has entries left), so the cost
+            // follows the entries, not the columns. Every rank is staged by exactly one lane.
             const int wa = j * WIN_WORDS;
             const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
             int gnext = 0;
@@ -927,23 +928,23 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 if (n < 0) n = 0;
                 const int k0 = r - r0;   // this lane's first slot
                 const int cbase = static_cast<int>(col0) + wd * 32;
-                for (int i = 0; ballot(i < n) != 0ull; i += 4) {
+                for (int i = 0; ballot(i < n) != 0ull; i += kStageStep) {
                     if (i < n) {
-                        int cv[4];
+                        int cv[kStageStep];
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
+                        for (int q = 0; q < kStageStep; ++q) {
                             cv[q] = cbase + __builtin_ctz(wbits | 0x80000000u);
                             wbits &= wbits - 1u;
                         }
                         if constexpr (SH::PACKED) {
                             // the column goes into the low half of the slot, beside the float value
 #pragma unroll
-                            for (int q = 0; q < 4; ++q) {
+                            for (int q = 0; q < kStageStep; ++q) {
                                 if (i + q < n) reinterpret_cast<uint2 *>(acc)[k0 + i + q].x = static_cast<uint32_t>(cv[q]);
                             }
                         } else {
 #pragma unroll
-                            for (int q = 0; q < 4; ++q) {
+                            for (int q = 0; q < kStageStep; ++q) {
                                 if (i + q < n) stage[k0 + i + q] = cv[q];
                             }
                         }
