@@ -99,6 +99,57 @@ def cpu_baseline(A, B, fraction: float, seed: int):
     )
 
 
+def sharded_pass(ws, torch, dA, dB, nnz_c, P, steps, warmup):
+    """The single pass with sharded output on the same workload: each row of C
+    claims its pool segment when it is done (no symbolic phase). Timed with
+    HIP events on its stream, pool sized to nnz(C); the gather into plain CSR
+    is timed beside it."""
+    dev = dA.row_ptr.device
+    Ad, Bd, dt = dA.desc(), dB.desc(), dA.dtype_code
+    opts = ws.make_options(timing=1)
+    wsb, nbytes = ws.allocate_workspace(dA, dB, opts)
+    h = torch.cuda.current_stream().cuda_stream
+    m = dA.nrows
+    row_off = torch.empty(max(m, 1), dtype=torch.int64, device=dev)
+    row_nnz = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+    pool_col = torch.empty(max(nnz_c, 1), dtype=torch.int32, device=dev)
+    pool_val = torch.empty(max(nnz_c, 1), dtype=dA.val.dtype, device=dev)
+
+    def one():
+        ws.wingspan_spgemm_sharded(Ad, Bd, dt, row_off.data_ptr(), row_nnz.data_ptr(), pool_col.data_ptr(),
+                                   pool_val.data_ptr(), nnz_c, wsb.data_ptr(), nbytes, h, opts)
+        return ws.wingspan_last_stats(2)
+
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ms, tiers = [], {t: [] for t in ws.TIERS}
+    for _ in range(steps):
+        e0.record()
+        st = one()
+        e1.record()
+        e1.synchronize()
+        ms.append(e0.elapsed_time(e1))
+        for t in ws.TIERS:
+            tiers[t].append(st["kernel_ms"][t])
+    # gather into CSR
+    S = ws.ShardedCSR(m, dB.ncols, row_off[:m], row_nnz[:m], pool_col, pool_val, nnz_c)
+    ws.sharded_to_csr(S)
+    torch.cuda.synchronize()
+    e0.record()
+    C = ws.sharded_to_csr(S)
+    e1.record()
+    e1.synchronize()
+    to_csr_ms = e0.elapsed_time(e1)
+    del C
+    t = float(np.mean(ms))
+    return dict(ms=round(t, 4), ms_min=round(float(np.min(ms)), 4), GFLOPs=round(2.0 * P / (t / 1e3) / 1e9, 2),
+                tier_ms={k: round(float(np.mean(v)), 4) for k, v in tiers.items()},
+                tier_rows={k: int(st["rows"][k]) for k in ws.TIERS},
+                to_csr_ms=round(to_csr_ms, 4), pool_entries=nnz_c)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +159,7 @@ def main():
     ap.add_argument("--cpu-fraction", type=float, default=0.08)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--no-sharded", action="store_true", help="skip the single-pass (sharded output) timing")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -233,6 +285,13 @@ def main():
         numeric_tier_rows={t: int(num["rows"][t]) for t in ws.TIERS},
         numeric_tier_products={t: int(num["products"][t]) for t in ws.TIERS},
     )
+    if not args.no_sharded:
+        log("timing the single pass with sharded output")
+        del c_col, c_val
+        torch.cuda.empty_cache()
+        sh = sharded_pass(ws, torch, dA, dB, nnz_c, P, args.steps, args.warmup)
+        sh["vs_two_phase_step"] = round(ms_per_step / sh["ms"], 3)
+        out["sharded_single_pass"] = sh
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a row sample")
         out["cpu_baseline"] = cpu_baseline(A, B, args.cpu_fraction, seed=20261)

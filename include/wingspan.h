@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define WINGSPAN_ABI_VERSION 2
+#define WINGSPAN_ABI_VERSION 3
 
 typedef enum { WINGSPAN_F32 = 0, WINGSPAN_F64 = 1 } wingspan_dtype;
 
@@ -53,7 +53,8 @@ typedef enum {
     WINGSPAN_ERR_DIMENSION_MISMATCH = 2,  /* A.ncols != B.nrows */
     WINGSPAN_ERR_INDEX_OVERFLOW = 3,      /* a size does not fit the int32 index types */
     WINGSPAN_ERR_WORKSPACE_TOO_SMALL = 4, /* workspace_bytes < wingspan_spgemm_workspace_size() */
-    WINGSPAN_ERR_INSUFFICIENT_CAPACITY = 5, /* nnz(C) > c_capacity (wingspan_spgemm only) */
+    WINGSPAN_ERR_INSUFFICIENT_CAPACITY = 5, /* nnz(C) > c_capacity (wingspan_spgemm) or
+                                             > pool_capacity (wingspan_spgemm_sharded) */
     WINGSPAN_ERR_INVALID_MATRIX = 6,      /* non-canonical input detected (options->validate) */
     WINGSPAN_ERR_HIP = 7,                 /* a HIP runtime call failed; message has the HIP error */
     WINGSPAN_ERR_UNSUPPORTED = 8,         /* a row is too long for the global spill pool */
@@ -104,14 +105,15 @@ enum {
     WINGSPAN_NUM_TIERS = 4
 };
 
-/* What the last symbolic (phase 0) or numeric (phase 1) call on this thread
- * did. Products are the scalar multiplies A[i,k]*B[k,j]; kernel_ms is only
+/* What the last symbolic (phase 0), numeric (phase 1) or single-pass
+ * (phase 2, wingspan_spgemm_sharded) call on this thread did. Products are the scalar multiplies A[i,k]*B[k,j]; kernel_ms is only
  * filled when options->timing was set. */
 typedef struct {
     int64_t rows[WINGSPAN_NUM_TIERS];
     int64_t a_nnz[WINGSPAN_NUM_TIERS];
     int64_t products[WINGSPAN_NUM_TIERS];
-    int64_t c_nnz[WINGSPAN_NUM_TIERS];   /* numeric phase only */
+    int64_t c_nnz[WINGSPAN_NUM_TIERS];   /* numeric phase only (the single pass bins before
+                                            C's row counts exist: 0) */
     int32_t launches[WINGSPAN_NUM_TIERS];
     float kernel_ms[WINGSPAN_NUM_TIERS];
     float analysis_ms;                   /* product counting, binning, scans */
@@ -167,7 +169,69 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
                                 void *workspace_dev, size_t workspace_bytes,
                                 void *stream, const wingspan_options *options);
 
-/* Statistics of the last call on this thread: phase 0 = symbolic, 1 = numeric. */
+/* ------------------------------------------------------------------------
+ * Single pass with sharded output.
+ *
+ * The paper's SpGEMM (Section 5.1, Gustavson's algorithm in the SpGEMM
+ * programs figure) writes C into a shard level (Section 4.3, modifier levels
+ * for concurrency): a fiber of the output is claimed by the one thread that
+ * writes it, on its first write, and kept in that thread's own storage, so
+ * no pass has to estimate the output's sparsity beforehand (Section 5.2 notes
+ * the pass this saves). Here the fiber is a row of C and the writer the
+ * workgroup that computes it: once the row's entries are known, the row
+ * claims a contiguous segment of a caller-owned pool from a shared counter
+ * and is written there, sorted by column. Rows sit in the pool in no
+ * particular order. The result, "sharded CSR", is
+ *
+ *   row i of C = columns pool_col_dev[row_off_dev[i] .. row_off_dev[i] +
+ *                row_nnz_dev[i]) with values at the same positions of
+ *                pool_val_dev (dtype),
+ *
+ * row_off_dev int64 and row_nnz_dev int32, A.nrows entries each, written by
+ * the library (rows without entries: row_nnz 0, row_off 0). A row's columns
+ * are strictly increasing; the entries and values are those of
+ * wingspan_spgemm, to the same rounding.
+ *
+ * Workspace: the same as wingspan_spgemm_workspace_size() gives for (A, B,
+ * dtype, options). The pool holds pool_capacity entries (4 bytes of column
+ * plus one value each). The call synchronizes `stream` twice: once to size
+ * its kernel launches, once to return *pool_used.
+ *
+ * *pool_used (host) receives nnz(C), the entries the rows claimed. If it
+ * exceeds pool_capacity the call returns WINGSPAN_ERR_INSUFFICIENT_CAPACITY:
+ * row_nnz_dev is then valid, the rows that did not fit were not written, and
+ * the caller can retry with a pool of *pool_used entries (an upper bound
+ * beforehand is the sum over rows of min(products of the row, B.ncols)).
+ * Nothing is ever written past pool_capacity.
+ *
+ * Dense rows (beyond the LDS hash tables) take the rank-indexed kernel only
+ * when B.ncols <= 262144, where a row's entry count is known before its first
+ * write; wider problems send them to the global spill tier.
+ * ------------------------------------------------------------------------ */
+wingspan_status wingspan_spgemm_sharded(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                        int64_t *row_off_dev, int32_t *row_nnz_dev, int32_t *pool_col_dev,
+                                        void *pool_val_dev, int64_t pool_capacity, int64_t *pool_used,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream,
+                                        const wingspan_options *options);
+
+/* Bytes of device workspace wingspan_sharded_to_csr needs for nrows rows
+ * (256-byte aligned). Pure host code. */
+wingspan_status wingspan_sharded_to_csr_workspace_size(int64_t nrows, size_t *bytes);
+
+/* Gathers a sharded C (as written by wingspan_spgemm_sharded, with every row
+ * present in the pool) into plain CSR: c_row_ptr_dev (int64, nrows+1 entries)
+ * is the exclusive prefix sum of row_nnz_dev, and row i's entries move to
+ * [c_row_ptr[i], c_row_ptr[i+1]) of c_col_idx_dev and c_val_dev. nnz is the
+ * entry count of C (the *pool_used of the sharded call; it sizes the launch);
+ * the C arrays hold at least that many entries. Asynchronous on `stream`. */
+wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_t *row_off_dev,
+                                        const int32_t *row_nnz_dev,
+                                        const int32_t *pool_col_dev, const void *pool_val_dev, wingspan_dtype dtype,
+                                        int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream);
+
+/* Statistics of the last call on this thread: phase 0 = symbolic, 1 = numeric,
+ * 2 = single pass (wingspan_spgemm_sharded). */
 wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out);
 
 /* Message for the last non-OK status on this thread ("" if none). */

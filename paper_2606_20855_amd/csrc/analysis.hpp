@@ -256,6 +256,87 @@ __global__ void fill_i32(int32_t *p, int64_t n, int32_t v) {
     if (i < n) p[i] = v;
 }
 
+// Sharded rows to CSR: entry p of C (row r, c_rp[r] <= p < c_rp[r+1]) comes
+// from pool position row_off[r] + p - c_rp[r]. Workgroup w writes entries
+// [w*kGatherChunk, (w+1)*kGatherChunk) of C with coalesced stores: one wave
+// finds the rows holding the chunk's ends by a 64-ary search of c_rp, the
+// chunk's row pointers are staged in LDS, and each thread finds its entry's
+// row by binary search there (in c_rp itself when the chunk spans very many,
+// mostly empty, rows).
+constexpr int kGatherChunk = 4096;
+constexpr int kGatherRows = 1024;
+
+// Last row r in [0, nrows) with c_rp[r] <= p (so c_rp[r] <= p < c_rp[r+1]
+// for p < c_rp[nrows]). All 64 lanes of one wave take part.
+__device__ __forceinline__ int64_t wave_find_row(const int64_t *__restrict__ c_rp, int64_t nrows, int64_t p) {
+    int64_t lo = 0, hi = nrows - 1;   // c_rp[lo] <= p holds throughout
+    while (hi > lo) {
+        const int64_t step = (hi - lo + kWave) / kWave;   // ceil((hi - lo + 1) / 64)
+        const int64_t idx = lo + static_cast<int64_t>(lane_id()) * step;
+        const bool le = idx <= hi && c_rp[idx] <= p;
+        const uint64_t m = ballot(le);
+        const int k = 63 - __clzll(m);   // lane 0 always qualifies
+        lo = lo + k * step;
+        const int64_t h = lo + step - 1;
+        hi = h < hi ? h : hi;
+    }
+    return lo;
+}
+
+template <typename V>
+__global__ void __launch_bounds__(256) gather_rows(int64_t nrows, const int64_t *__restrict__ row_off,
+                                                   const int64_t *__restrict__ c_rp,
+                                                   const int32_t *__restrict__ pool_col,
+                                                   const V *__restrict__ pool_val, int32_t *__restrict__ c_col,
+                                                   V *__restrict__ c_val) {
+    __shared__ int64_t s_rp[kGatherRows + 1];
+    __shared__ int64_t s_off[kGatherRows];
+    __shared__ int64_t s_r[2];
+    const int64_t nnz = c_rp[nrows];
+    const int64_t p0 = static_cast<int64_t>(blockIdx.x) * kGatherChunk;
+    if (p0 >= nnz) return;   // whole workgroup leaves together
+    const int64_t p1 = nnz - p0 < kGatherChunk ? nnz : p0 + kGatherChunk;
+    if (threadIdx.x < kWave) {
+        const int64_t r0 = wave_find_row(c_rp, nrows, p0);
+        const int64_t r1 = wave_find_row(c_rp, nrows, p1 - 1);
+        if (threadIdx.x == 0) {
+            s_r[0] = r0;
+            s_r[1] = r1;
+        }
+    }
+    __syncthreads();
+    const int64_t r0 = s_r[0], r1 = s_r[1];
+    const int64_t nr = r1 - r0 + 1;
+    if (nr <= kGatherRows) {
+        for (int64_t i = threadIdx.x; i <= nr; i += blockDim.x) s_rp[i] = c_rp[r0 + i];
+        for (int64_t i = threadIdx.x; i < nr; i += blockDim.x) s_off[i] = row_off[r0 + i];
+        __syncthreads();
+        for (int64_t p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
+            int lo = 0, hi = static_cast<int>(nr) - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_rp[mid] <= p) lo = mid;
+                else hi = mid - 1;
+            }
+            const int64_t src = s_off[lo] + (p - s_rp[lo]);
+            c_col[p] = pool_col[src];
+            c_val[p] = pool_val[src];
+        }
+    } else {
+        for (int64_t p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
+            int64_t lo = r0, hi = r1;
+            while (lo < hi) {
+                const int64_t mid = (lo + hi + 1) >> 1;
+                if (c_rp[mid] <= p) lo = mid;
+                else hi = mid - 1;
+            }
+            const int64_t src = row_off[lo] + (p - c_rp[lo]);
+            c_col[p] = pool_col[src];
+            c_val[p] = pool_val[src];
+        }
+    }
+}
+
 // Position-weighted checksum of C.row_ptr[0..m]: sum of rp[i] * (2i + 1)
 // modulo 2^64, added into *out (which the caller zeroes).
 __global__ void __launch_bounds__(256) rowptr_checksum(const int64_t *__restrict__ rp, int64_t m, uint64_t *out) {

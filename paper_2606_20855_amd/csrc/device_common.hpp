@@ -34,6 +34,7 @@ enum : int32_t {
     kErrProbeExhausted = 1,   // a hash table filled up (structure larger than C.row_ptr says)
     kErrRowMismatch = 2,      // a row produced a different entry count than C.row_ptr
     kErrInvalidMatrix = 4,    // validation found a non-canonical input
+    kErrPoolLayout = 8,       // a kernel was given rows it cannot write to a pool (host routing error)
 };
 
 // Record of what the last symbolic phase left in the workspace for the
@@ -57,6 +58,7 @@ struct Control {
     int64_t total_products;
     int64_t spill_max_bound;
     int64_t c_nnz;
+    unsigned long long pool_claimed;   // single pass: pool entries the rows have claimed
     int32_t spill_next;
     int32_t error_flags;
     int32_t has_zero_values;   // some A or B value could give a zero product
@@ -71,6 +73,39 @@ struct Control {
 };
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Where a numeric kernel writes the rows of C. Without a claim counter the
+// rows go to plain CSR at C.row_ptr, which the symbolic phase computed. With
+// one (the single pass, with sharded output) a row's entry count is known only
+// once the row is computed: the row then claims that many entries of the pool
+// from the shared counter (the first and only writer of a row claims its
+// storage), records where in row_off / row_nnz, and is written there. A row
+// that would pass the pool's capacity writes nothing, but the counter still
+// grows, so it ends at the entry count of C.
+struct RowSink {
+    const int64_t *c_rp = nullptr;
+    unsigned long long *claimed = nullptr;
+    int64_t *row_off = nullptr;
+    int32_t *row_nnz = nullptr;
+    int64_t cap = 0;
+    __device__ __forceinline__ bool pooled() const { return claimed != nullptr; }
+    // Pool output: claims `count` entries for `row` and returns the first. *len
+    // is how many the row may write: count, or 0 when the pool is too small.
+    __device__ __forceinline__ int64_t claim(int row, int count, int64_t *len) const {
+        const int64_t off = static_cast<int64_t>(atomicAdd(claimed, static_cast<unsigned long long>(count)));
+        row_off[row] = off;
+        row_nnz[row] = count;
+        *len = off + count <= cap ? count : 0;
+        return off;
+    }
+};
+
+// 64-bit value of lane `src` of each group of `width` lanes.
+__device__ __forceinline__ int64_t shfl_i64(int64_t x, int src, int width) {
+    const int lo = __shfl(static_cast<int>(x), src, width);
+    const int hi = __shfl(static_cast<int>(x >> 32), src, width);
+    return static_cast<int64_t>((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo));
+}
 
 // Lane mask of a condition (bit l set where lane l's condition holds),
 // straight from the compare's scalar mask.

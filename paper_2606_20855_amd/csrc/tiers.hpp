@@ -55,8 +55,7 @@ struct Mats {
 // ---------------------------------------------------------------------------
 template <int S, typename V, bool NUM>
 __global__ void __launch_bounds__(256) tiny_kernel(Mats<V> M, const int32_t *__restrict__ rows,
-                                                   int32_t nrows, int32_t *__restrict__ row_nnz,
-                                                   const int64_t *__restrict__ c_rp,
+                                                   int32_t nrows, int32_t *__restrict__ row_nnz, RowSink out,
                                                    int32_t *__restrict__ c_col, V *__restrict__ c_val,
                                                    Control *ctrl) {
     constexpr int G = 256 / S;
@@ -144,9 +143,17 @@ __global__ void __launch_bounds__(256) tiny_kernel(Mats<V> M, const int32_t *__r
         return;
     }
     const int rank = __popcll(mine & ((1ull << ln) - 1ull));
-    const int64_t cb = c_rp[row];
-    const int64_t seg = c_rp[row + 1] - cb;
-    if (sl == 0 && count != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    int64_t cb, seg;
+    if (!out.pooled()) {
+        cb = out.c_rp[row];
+        seg = out.c_rp[row + 1] - cb;
+        if (sl == 0 && count != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    } else {
+        int64_t b = 0, l = 0;
+        if (sl == 0) b = out.claim(row, count, &l);
+        cb = shfl_i64(b, 0, S);
+        seg = shfl_i64(l, 0, S);
+    }
     if (tail && rank < seg) {
         c_col[cb + rank] = key;
         c_val[cb + rank] = static_cast<V>(val);
@@ -339,8 +346,7 @@ struct HashShape {
 template <int LOG2T, typename V, bool NUM>
 __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M, const int32_t *__restrict__ rows,
                                                                        int64_t ncols,
-                                                                       int32_t *__restrict__ row_nnz,
-                                                                       const int64_t *__restrict__ c_rp,
+                                                                       int32_t *__restrict__ row_nnz, RowSink out,
                                                                        int32_t *__restrict__ c_col,
                                                                        V *__restrict__ c_val, Control *ctrl) {
     constexpr int T = HashShape<LOG2T>::T;
@@ -353,6 +359,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkInts];
     __shared__ int32_t ctot[kCtotInts];
+    __shared__ int64_t s_claim[2];   // pool output: the row's first entry and writable length
 
     const int row = rows[blockIdx.x];
     for (int i = threadIdx.x; i < T; i += BLOCK) {
@@ -382,8 +389,18 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
     }
     __syncthreads();
 
-    const int64_t cb = c_rp[row];
-    const int64_t seg = c_rp[row + 1] - cb;
+    int64_t cb, seg;
+    if (!out.pooled()) {
+        cb = out.c_rp[row];
+        seg = out.c_rp[row + 1] - cb;
+    } else {
+        // the row's entries are its first insertions
+        const int total = block_sum<BLOCK>(inserted, scratch);
+        if (threadIdx.x == 0) s_claim[0] = out.claim(row, total, &s_claim[1]);
+        __syncthreads();
+        cb = uniform(s_claim[0]);
+        seg = uniform(s_claim[1]);
+    }
     // the thread's slots, in registers
     constexpr int PER = T / BLOCK;
     int kk[PER];
@@ -403,7 +420,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
             static_assert(BWW <= 2 * T && BWW / 8 <= T, "bitmap in the doubles, group offsets in the keys");
             const int64_t total = rank_emit_regs<BLOCK, BWW, PER, V>(
                 kk, vv, ncols, reinterpret_cast<uint32_t *>(vals), keys, scratch, c_col, c_val, cb, seg);
-            if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+            if (threadIdx.x == 0 && !out.pooled() && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
             return;
         }
     }
@@ -445,7 +462,7 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
         }
     }
 
-    if (threadIdx.x == 0 && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    if (threadIdx.x == 0 && !out.pooled() && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
     const int lim = static_cast<int64_t>(total) < seg ? total : static_cast<int>(seg);
     for (int i = threadIdx.x; i < lim; i += BLOCK) {
         c_col[cb + i] = keys[i];
@@ -738,7 +755,7 @@ struct SliceRange {
 template <typename V>
 __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     Mats<V> M, const int32_t *__restrict__ rows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
-    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
+    RowSink out, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
     const int32_t *__restrict__ slot_of_row, const uint32_t *__restrict__ cache, int64_t row_words) {
     using SH = RankShape<V>;
     constexpr int BLOCK = SH::BLOCK;
@@ -754,13 +771,24 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
     __shared__ int32_t sclaim;   // staging's group counter
+    __shared__ int64_t s_claim[2];   // pool output: the row's first entry and writable length
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries], e_hi[kCacheEntries];
     __shared__ double e_av[kCacheEntries];
 
+    // pool output needs a row's entry count before its first write: one region only
+    if (out.pooled() && nwin > SH::REGION_WINS) {
+        if (threadIdx.x == 0) atomicOr(&ctrl->error_flags, kErrPoolLayout);
+        return;
+    }
     const int row = rows[blockIdx.x];
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
-    const int64_t cb = c_rp[row];
-    const int64_t seg = c_rp[row + 1] - cb;
+    // CSR output: the row's place from C.row_ptr. Pool output: claimed once the region's entry count is
+    // known
+    int64_t cb = 0, seg = 0;
+    if (!out.pooled()) {
+        cb = out.c_rp[row];
+        seg = out.c_rp[row + 1] - cb;
+    }
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
@@ -772,7 +800,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
     if (threadIdx.x == 0) sclaim = 0;
 
-    int64_t out = 0;   // entries of the row emitted in earlier regions
+    int64_t done = 0;   // entries of the row emitted in earlier regions
     for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
         const int rg1 = nwin - rg0 < SH::REGION_WINS ? nwin : rg0 + SH::REGION_WINS;
         const int64_t col0 = static_cast<int64_t>(rg0) * kRankWinCols;
@@ -862,7 +890,12 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
 #pragma unroll
         for (int i = 0; i < NW; ++i) region_total += scratch[i];
         region_total = uniform(region_total);
+        if (out.pooled() && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
         __syncthreads();
+        if (out.pooled()) {
+            cb = uniform(s_claim[0]);
+            seg = uniform(s_claim[1]);
+        }
         // 3. rank slices: whole windows while they fit CAP entries; a window
         //    denser than CAP is taken in slices of CAP ranks. Lane jw holds the
         //    first rank of window jw (one LDS read for all windows), and the
@@ -953,7 +986,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             }
             __syncthreads();
             // copy the slice to C with coalesced stores, clearing the accumulator
-            const int64_t pbase = out + r0;
+            const int64_t pbase = done + r0;
             for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
                 int32_t colv;
                 V v;
@@ -977,9 +1010,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             r0 = r1;
             if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
         }
-        out += region_total;
+        done += region_total;
     }
-    if (threadIdx.x == 0 && out != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    if (threadIdx.x == 0 && !out.pooled() && done != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
 }
 
 // ---------------------------------------------------------------------------
@@ -1090,17 +1123,17 @@ __device__ void merge_sort_segment(int32_t *__restrict__ col, V *__restrict__ va
 template <typename V, bool NUM>
 __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64_t *__restrict__ pref,
                                           int64_t ncols, int32_t *__restrict__ keys, double *__restrict__ vals,
-                                          int32_t *__restrict__ row_nnz, const int64_t *__restrict__ c_rp,
+                                          int32_t *__restrict__ row_nnz, const RowSink &out,
                                           int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
                                           int32_t *scratch, int32_t *s_keys, V *s_vals, int32_t *mark,
-                                          int32_t *ctot) {
+                                          int32_t *ctot, int64_t *s_claim) {
     constexpr int BLOCK = kSpillBlock;
     constexpr int NW = BLOCK / kWave;
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
     int64_t bound;
-    if (NUM) {
-        bound = c_rp[row + 1] - c_rp[row];
+    if (NUM && !out.pooled()) {
+        bound = out.c_rp[row + 1] - out.c_rp[row];
     } else {
         const int64_t f = pref[a_hi] - pref[a_lo];
         bound = f < ncols ? f : ncols;
@@ -1142,8 +1175,18 @@ __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64
         __threadfence();
         __syncthreads();
         // compact the table into the row of C (slot order), then sort it there
-        const int64_t cb = c_rp[row];
-        const int64_t seg = c_rp[row + 1] - cb;
+        int64_t cb, seg;
+        if (!out.pooled()) {
+            cb = out.c_rp[row];
+            seg = out.c_rp[row + 1] - cb;
+        } else {
+            // the row's entries are its first insertions
+            const int total = block_sum<BLOCK>(inserted, scratch);
+            if (threadIdx.x == 0) s_claim[0] = out.claim(row, total, &s_claim[1]);
+            __syncthreads();
+            cb = uniform(s_claim[0]);
+            seg = uniform(s_claim[1]);
+        }
         int running = 0;
         for (int64_t s0 = 0; s0 < T; s0 += BLOCK) {
             const int64_t s = s0 + threadIdx.x;
@@ -1162,7 +1205,7 @@ __device__ __forceinline__ void spill_row(const Mats<V> &M, int row, const int64
             }
             running += tot;
         }
-        if (threadIdx.x == 0 && running != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+        if (threadIdx.x == 0 && !out.pooled() && running != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
         __syncthreads();
         const int len = uniform(static_cast<int64_t>(running) < seg ? running : static_cast<int>(seg));
         merge_sort_segment<V>(c_col + cb, c_val + cb, len, keys, reinterpret_cast<V *>(vals), s_keys, s_vals);
@@ -1174,10 +1217,11 @@ template <typename V, bool NUM>
 __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
     Mats<V> M, const int32_t *__restrict__ rows, int32_t nrows, const int64_t *__restrict__ pref,
     int64_t ncols, char *__restrict__ pool, int64_t slab_cap, int32_t *__restrict__ row_nnz,
-    const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col, V *__restrict__ c_val,
+    RowSink out, int32_t *__restrict__ c_col, V *__restrict__ c_val,
     Control *ctrl) {
     constexpr int NW = kSpillBlock / kWave;
     __shared__ int32_t s_row;
+    __shared__ int64_t s_claim[2];   // pool output: the row's first entry and writable length
     __shared__ int32_t scratch[NW];
     __shared__ int32_t s_keys[NUM ? kRunLen : 1];
     __shared__ V s_vals[NUM ? kRunLen : 1];
@@ -1199,8 +1243,8 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
         const int ri = uniform(s_row);
         __syncthreads();
         if (ri >= nrows) break;
-        spill_row<V, NUM>(M, rows[ri], pref, ncols, keys, vals, row_nnz, c_rp, c_col, c_val, ctrl, scratch,
-                          s_keys, s_vals, mark, ctot);
+        spill_row<V, NUM>(M, rows[ri], pref, ncols, keys, vals, row_nnz, out, c_col, c_val, ctrl, scratch,
+                          s_keys, s_vals, mark, ctot, s_claim);
     }
 }
 

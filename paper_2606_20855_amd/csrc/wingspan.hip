@@ -45,7 +45,7 @@ constexpr int kMaxSlabs = 256;
 constexpr size_t kAlign = 256;
 
 thread_local std::string g_err;
-thread_local wingspan_phase_stats g_stats[2];
+thread_local wingspan_phase_stats g_stats[3];   // symbolic, numeric, single pass
 
 wingspan_status fail(wingspan_status s, const char *fmt, ...) {
     char buf[512];
@@ -339,18 +339,25 @@ unsigned blocks_for(int64_t n, int per) { return static_cast<unsigned>((n + per 
 
 // Product counts, optional validation, and binning. Ends with the control
 // block on the host.
-wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, bool numeric,
-                        const int64_t *c_rp, bool have_pref) {
+// What the analysis prepares: the symbolic phase (bins by products, LDS
+// tables of keys), the numeric phase (bins by C's exact row counts), or the
+// single pass with sharded output (bins by products, LDS tables of keys and
+// doubles; row_nnz_out receives 0 for the rows without products).
+enum AnalysisMode { kModeSymbolic = 0, kModeNumeric = 1, kModeSharded = 2 };
+
+wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, AnalysisMode mode,
+                        const int64_t *c_rp, bool have_pref, int32_t *row_nnz_out = nullptr) {
     wingspan_status s;
+    const bool numeric = mode == kModeNumeric;
     if ((s = timer_start(c, kSlotAnalysis)) != WINGSPAN_OK) return s;
     const int64_t m = A->nrows;
     const int64_t words = sizeof(Control) / sizeof(int32_t);
     zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl), words);
     LAUNCH_CHECK("zero_words");
-    if (!numeric) {
+    if (mode == kModeSymbolic) {
         // the structure cache is being rewritten: invalid until this phase completes
         write_stamp<<<1, 1, 0, c.st>>>(c.stamp, Stamp{});
-    } else if (c.L.cache_rows > 0) {
+    } else if (numeric && c.L.cache_rows > 0) {
         rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, m, &c.ctrl->rp_sum);
     }
     LAUNCH_CHECK("stamp");
@@ -391,11 +398,21 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, bo
     cfg.numeric = numeric;
     cfg.tiny_max = c.o.tiny_max;
     cfg.force_spill = c.o.force_spill;
-    cfg.hash_log2_max = numeric ? c.o.hash_log2_max_num : c.o.hash_log2_max_sym;
-    cfg.dense_ok = numeric ? (c.L.nwin > 0) : (!c.o.dense_disabled && B->ncols <= kBitmapMaxCols);
+    cfg.hash_log2_max = mode == kModeSymbolic ? c.o.hash_log2_max_sym : c.o.hash_log2_max_num;
     cfg.dense_min_nnz = c.o.dense_min_nnz;
+    if (mode == kModeNumeric) {
+        cfg.dense_ok = c.L.nwin > 0;
+    } else if (mode == kModeSymbolic) {
+        cfg.dense_ok = !c.o.dense_disabled && B->ncols <= kBitmapMaxCols;
+    } else {
+        // the rank kernel writes a pool row once its count is known: rows of one region only (others spill)
+        cfg.dense_ok = c.L.rank_mode && c.L.nwin > 0 && c.L.nwin <= RankShape<float>::REGION_WINS;
+        // without a structure cache the LDS hash is the cheaper tier wherever it fits
+        cfg.dense_min_nnz = c.o.dense_min_explicit ? c.o.dense_min_nnz : INT64_MAX;
+    }
     if (m > 0) {
-        bin_count<<<blocks_for(m, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, m, cfg, c.ctrl, c.row_nnz);
+        bin_count<<<blocks_for(m, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, m, cfg, c.ctrl,
+                                                         row_nnz_out ? row_nnz_out : c.row_nnz);
         bin_offsets<<<1, 1, 0, c.st>>>(c.ctrl, c.pref, A->nnz);
         bin_scatter<<<blocks_for(m, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, m, cfg, c.ctrl, c.perm);
     } else {
@@ -450,28 +467,27 @@ void bin_range(const Ctx &c, int b0, int nb, int32_t *start, int32_t *count) {
 // ---------------------------------------------------------------------------
 template <typename V, bool NUM>
 void launch_tiny(int s_idx, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows,
-                 int32_t cnt, int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val,
-                 Control *ctrl) {
+                 int32_t cnt, int32_t *row_nnz, RowSink out, int32_t *c_col, V *c_val, Control *ctrl) {
     switch (s_idx) {
-        case 0: tiny_kernel<8, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 1: tiny_kernel<16, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        case 2: tiny_kernel<32, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
-        default: tiny_kernel<64, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, c_rp, c_col, c_val, ctrl); break;
+        case 0: tiny_kernel<8, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, out, c_col, c_val, ctrl); break;
+        case 1: tiny_kernel<16, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, out, c_col, c_val, ctrl); break;
+        case 2: tiny_kernel<32, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, out, c_col, c_val, ctrl); break;
+        default: tiny_kernel<64, V, NUM><<<grid, 256, 0, st>>>(M, rows, cnt, row_nnz, out, c_col, c_val, ctrl); break;
     }
 }
 
 template <int LOG2T, typename V, bool NUM>
 void launch_hash_t(unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows, int64_t ncols,
-                   int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
-    hash_kernel<LOG2T, V, NUM><<<grid, HashShape<LOG2T>::BLOCK, 0, st>>>(M, rows, ncols, row_nnz, c_rp, c_col,
+                   int32_t *row_nnz, RowSink out, int32_t *c_col, V *c_val, Control *ctrl) {
+    hash_kernel<LOG2T, V, NUM><<<grid, HashShape<LOG2T>::BLOCK, 0, st>>>(M, rows, ncols, row_nnz, out, c_col,
                                                                         c_val, ctrl);
 }
 
 template <typename V, bool NUM>
 void launch_hash(int log2t, unsigned grid, hipStream_t st, const Mats<V> &M, const int32_t *rows, int64_t ncols,
-                 int32_t *row_nnz, const int64_t *c_rp, int32_t *c_col, V *c_val, Control *ctrl) {
+                 int32_t *row_nnz, RowSink out, int32_t *c_col, V *c_val, Control *ctrl) {
 #define WS_HASH_CASE(L) \
-    case L: launch_hash_t<L, V, NUM>(grid, st, M, rows, ncols, row_nnz, c_rp, c_col, c_val, ctrl); break;
+    case L: launch_hash_t<L, V, NUM>(grid, st, M, rows, ncols, row_nnz, out, c_col, c_val, ctrl); break;
     switch (log2t) {
         WS_HASH_CASE(6)
         WS_HASH_CASE(7)
@@ -482,7 +498,7 @@ void launch_hash(int log2t, unsigned grid, hipStream_t st, const Mats<V> &M, con
         WS_HASH_CASE(12)
         WS_HASH_CASE(13)
         default:
-            if constexpr (!NUM) launch_hash_t<14, V, NUM>(grid, st, M, rows, ncols, row_nnz, c_rp, c_col, c_val, ctrl);
+            if constexpr (!NUM) launch_hash_t<14, V, NUM>(grid, st, M, rows, ncols, row_nnz, out, c_col, c_val, ctrl);
             break;
     }
 #undef WS_HASH_CASE
@@ -531,7 +547,7 @@ void launch_dense(int wcols, bool sentinel, unsigned grid, hipStream_t st, const
 // ---------------------------------------------------------------------------
 wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, int64_t *c_rp,
                               int64_t *c_nnz) {
-    wingspan_status s = analyze(c, A, B, false, nullptr, false);
+    wingspan_status s = analyze(c, A, B, kModeSymbolic, nullptr, false);
     if (s != WINGSPAN_OK) return s;
     fill_stats(c, 0);
     wingspan_phase_stats &stats = g_stats[0];
@@ -546,7 +562,7 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
         if (!cnt) continue;
         const int S = 8 << i;
         launch_tiny<float, false>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b],
-                                  cnt, c.row_nnz, nullptr, nullptr, nullptr, c.ctrl);
+                                  cnt, c.row_nnz, RowSink{}, nullptr, nullptr, c.ctrl);
         stats.launches[WINGSPAN_TIER_TINY]++;
     }
     LAUNCH_CHECK("tiny symbolic");
@@ -558,7 +574,7 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
         const int32_t cnt = c.host.bin_count[b];
         if (!cnt) continue;
         launch_hash<float, false>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M,
-                                  perm + c.host.bin_offset[b], B->ncols, c.row_nnz, nullptr, nullptr, nullptr,
+                                  perm + c.host.bin_offset[b], B->ncols, c.row_nnz, RowSink{}, nullptr, nullptr,
                                   c.ctrl);
         stats.launches[WINGSPAN_TIER_HASH]++;
     }
@@ -588,7 +604,7 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
     if (cnt) {
         const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
         spill_kernel<float, false><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols,
-                                                                  c.pool, c.L.slab_cap, c.row_nnz, nullptr,
+                                                                  c.pool, c.L.slab_cap, c.row_nnz, RowSink{},
                                                                   nullptr, nullptr, c.ctrl);
         stats.launches[WINGSPAN_TIER_SPILL]++;
         LAUNCH_CHECK("spill symbolic");
@@ -615,7 +631,7 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
 template <typename V>
 wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, const int64_t *c_rp,
                              int32_t *c_col, V *c_val, bool have_pref) {
-    wingspan_status s = analyze(c, A, B, true, c_rp, have_pref);
+    wingspan_status s = analyze(c, A, B, kModeNumeric, c_rp, have_pref);
     if (s != WINGSPAN_OK) return s;
     fill_stats(c, 1);
     wingspan_phase_stats &stats = g_stats[1];
@@ -628,6 +644,8 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     const Mats<V> M{A->row_ptr, A->col_idx, static_cast<const V *>(A->val),
                     B->row_ptr, B->col_idx, static_cast<const V *>(B->val)};
     const int32_t *perm = c.perm;
+    RowSink sink;
+    sink.c_rp = c_rp;
 
     if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
     for (int i = 0; i < kNumTiny; ++i) {
@@ -636,7 +654,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         if (!cnt) continue;
         const int S = 8 << i;
         launch_tiny<V, true>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b], cnt,
-                             nullptr, c_rp, c_col, c_val, c.ctrl);
+                             nullptr, sink, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_TINY]++;
     }
     LAUNCH_CHECK("tiny numeric");
@@ -648,7 +666,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         const int32_t cnt = c.host.bin_count[b];
         if (!cnt) continue;
         launch_hash<V, true>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M, perm + c.host.bin_offset[b],
-                             B->ncols, nullptr, c_rp, c_col, c_val, c.ctrl);
+                             B->ncols, nullptr, sink, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_HASH]++;
     }
     LAUNCH_CHECK("hash numeric");
@@ -668,7 +686,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         const bool cached = stamp_matches(c, A, B);
         stats.structure_cache_rows = cached ? c.host_stamp.cached_rows : 0;
         dense_rank_kernel<V><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
-            M, perm + start, c.wtab, c.L.nwin, B->ncols, c_rp, c_col, c_val, c.ctrl,
+            M, perm + start, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl,
             cached ? c.slot_of_row : nullptr, cached ? c.cache : nullptr, c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense rank numeric");
@@ -685,7 +703,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt) {
         const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
         spill_kernel<V, true><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols, c.pool,
-                                                             c.L.slab_cap, nullptr, c_rp, c_col, c_val, c.ctrl);
+                                                             c.L.slab_cap, nullptr, sink, c_col, c_val, c.ctrl);
         stats.launches[WINGSPAN_TIER_SPILL]++;
         LAUNCH_CHECK("spill numeric");
     }
@@ -699,6 +717,103 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
             return fail(WINGSPAN_ERR_INCONSISTENT, "C.row_ptr does not match the structure of A*B (flags %d)",
                         flags);
     }
+    return WINGSPAN_OK;
+}
+
+// Single pass with sharded output: rows binned by products, each tier's
+// numeric kernel claims a row's pool segment once the row's entry count is
+// known and writes the sorted row there.
+template <typename V>
+wingspan_status sharded_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, int64_t *row_off,
+                             int32_t *row_nnz, int32_t *pool_col, V *pool_val, int64_t cap, int64_t *used) {
+    const int64_t m = A->nrows;
+    // rows without products are written by the analysis (row_nnz = 0); their offsets here
+    if (m > 0) {
+        fill_i64<<<blocks_for(m, 256), 256, 0, c.st>>>(row_off, m, 0);
+        LAUNCH_CHECK("fill offsets");
+    }
+    wingspan_status s = analyze(c, A, B, kModeSharded, nullptr, false, row_nnz);
+    if (s != WINGSPAN_OK) return s;
+    fill_stats(c, 2);
+    wingspan_phase_stats &stats = g_stats[2];
+    const Mats<V> M{A->row_ptr, A->col_idx, static_cast<const V *>(A->val),
+                    B->row_ptr, B->col_idx, static_cast<const V *>(B->val)};
+    const int32_t *perm = c.perm;
+    RowSink sink;
+    sink.claimed = &c.ctrl->pool_claimed;
+    sink.row_off = row_off;
+    sink.row_nnz = row_nnz;
+    sink.cap = cap;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+    for (int i = 0; i < kNumTiny; ++i) {
+        const int b = kBinTiny0 + i;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        const int S = 8 << i;
+        launch_tiny<V, true>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b], cnt,
+                             nullptr, sink, pool_col, pool_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_TINY]++;
+    }
+    LAUNCH_CHECK("tiny single pass");
+    if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+    for (int i = 0; i < kNumHash; ++i) {
+        const int b = kBinHash0 + i;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        launch_hash<V, true>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M, perm + c.host.bin_offset[b],
+                             B->ncols, nullptr, sink, pool_col, pool_val, c.ctrl);
+        stats.launches[WINGSPAN_TIER_HASH]++;
+    }
+    LAUNCH_CHECK("hash single pass");
+    if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+
+    int32_t start, cnt;
+    bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
+    if (cnt) {
+        const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
+        build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows, c.L.nwin,
+                                                                       c.L.wcols, c.wtab);
+        LAUNCH_CHECK("build_window_table");
+    }
+    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+    if (cnt) {
+        // binning sends dense rows here only in rank mode with one region; the column bitmaps come from the
+        // kernel's own structure pass
+        dense_rank_kernel<V><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+            M, perm + start, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr, nullptr,
+            c.L.row_words);
+        stats.launches[WINGSPAN_TIER_DENSE]++;
+        LAUNCH_CHECK("dense rank single pass");
+    }
+    if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
+    bin_range(c, kBinSpill0, kNumClasses, &start, &cnt);
+    if (cnt) {
+        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
+        spill_kernel<V, true><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols, c.pool,
+                                                             c.L.slab_cap, nullptr, sink, pool_col, pool_val,
+                                                             c.ctrl);
+        stats.launches[WINGSPAN_TIER_SPILL]++;
+        LAUNCH_CHECK("spill single pass");
+    }
+    if ((s = timer_stop(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
+
+    HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (c.host.error_flags & kErrProbeExhausted)
+        return fail(WINGSPAN_ERR_INCONSISTENT, "a row's hash table filled up (flags %d)", c.host.error_flags);
+    if (c.host.error_flags & kErrPoolLayout)
+        return fail(WINGSPAN_ERR_INCONSISTENT, "a dense row spans several regions (flags %d)", c.host.error_flags);
+    const int64_t total = static_cast<int64_t>(c.host.pool_claimed);
+    *used = total;
+    stats.c_nnz_total = total;
+    if (total > cap)
+        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "C has %lld entries but the pool holds %lld",
+                    (long long)total, (long long)cap);
     return WINGSPAN_OK;
 }
 
@@ -742,7 +857,7 @@ int wingspan_abi_version(void) { return WINGSPAN_ABI_VERSION; }
 const char *wingspan_last_error(void) { return g_err.c_str(); }
 
 wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out) {
-    if ((phase != 0 && phase != 1) || !out) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bad phase or NULL out");
+    if (phase < 0 || phase > 2 || !out) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bad phase or NULL out");
     *out = g_stats[phase];
     return WINGSPAN_OK;
 }
@@ -833,6 +948,85 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
         return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_col_idx_dev or c_val_dev is NULL");
     return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, workspace_dev, workspace_bytes,
                          stream, options, true, c);
+}
+
+wingspan_status wingspan_spgemm_sharded(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                        int64_t *row_off_dev, int32_t *row_nnz_dev, int32_t *pool_col_dev,
+                                        void *pool_val_dev, int64_t pool_capacity, int64_t *pool_used,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream,
+                                        const wingspan_options *options) {
+    g_err.clear();
+    wingspan_status s = check_pair(A, B);
+    if (s != WINGSPAN_OK) return s;
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (!pool_used) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "pool_used is NULL");
+    if (pool_capacity < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "pool_capacity is negative");
+    if (A->nrows > 0 && (!row_off_dev || !row_nnz_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "row_off_dev or row_nnz_dev is NULL");
+    if (pool_capacity > 0 && (!pool_col_dev || !pool_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "pool_col_dev or pool_val_dev is NULL");
+    Ctx c{};
+    if ((s = setup(c, A, B, options, workspace_dev, workspace_bytes, stream)) != WINGSPAN_OK) return s;
+    if ((s = timer_begin(c.o.timing)) != WINGSPAN_OK) return s;
+    c.dtype_f64 = dtype == WINGSPAN_F64 ? 1 : 0;
+    if (dtype == WINGSPAN_F32)
+        s = sharded_impl<float>(c, A, B, row_off_dev, row_nnz_dev, pool_col_dev, static_cast<float *>(pool_val_dev),
+                                pool_capacity, pool_used);
+    else
+        s = sharded_impl<double>(c, A, B, row_off_dev, row_nnz_dev, pool_col_dev,
+                                 static_cast<double *>(pool_val_dev), pool_capacity, pool_used);
+    const wingspan_status t = finish_timing(2);
+    return s != WINGSPAN_OK ? s : t;
+}
+
+wingspan_status wingspan_sharded_to_csr_workspace_size(int64_t nrows, size_t *bytes) {
+    g_err.clear();
+    if (!bytes) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    if (nrows < 0 || nrows > INT32_MAX - 1) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "nrows out of range");
+    const int64_t tiles = (nrows + 1 + kScanTile - 1) / kScanTile + 2;
+    *bytes = align_up(sizeof(int64_t) * tiles);
+    return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_t *row_off_dev, const int32_t *row_nnz_dev,
+                                        const int32_t *pool_col_dev, const void *pool_val_dev, wingspan_dtype dtype,
+                                        int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream) {
+    g_err.clear();
+    size_t need = 0;
+    wingspan_status s = wingspan_sharded_to_csr_workspace_size(nrows, &need);
+    if (s != WINGSPAN_OK) return s;
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    if (nnz < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "nnz is negative");
+    if (nnz > 0 && (!pool_col_dev || !pool_val_dev || !c_col_idx_dev || !c_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "a pool or C array is NULL");
+    if (nrows > 0 && (!row_off_dev || !row_nnz_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "row_off_dev or row_nnz_dev is NULL");
+    if (workspace_bytes < need)
+        return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+    if (!workspace_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(workspace_dev) % kAlign != 0)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kAlign);
+    Ctx c{};
+    c.st = static_cast<hipStream_t>(stream);
+    c.partials = static_cast<int64_t *>(workspace_dev);
+    if ((s = run_scan(c, CountIn{row_nnz_dev}, nrows, c_row_ptr_dev)) != WINGSPAN_OK) return s;
+    if (nrows > 0 && nnz > 0) {
+        const unsigned grid = static_cast<unsigned>((nnz + kGatherChunk - 1) / kGatherChunk);
+        if (dtype == WINGSPAN_F32)
+            gather_rows<float><<<grid, 256, 0, c.st>>>(nrows, row_off_dev, c_row_ptr_dev, pool_col_dev,
+                                                       static_cast<const float *>(pool_val_dev), c_col_idx_dev,
+                                                       static_cast<float *>(c_val_dev));
+        else
+            gather_rows<double><<<grid, 256, 0, c.st>>>(nrows, row_off_dev, c_row_ptr_dev, pool_col_dev,
+                                                        static_cast<const double *>(pool_val_dev), c_col_idx_dev,
+                                                        static_cast<double *>(c_val_dev));
+        LAUNCH_CHECK("gather_rows");
+    }
+    return WINGSPAN_OK;
 }
 
 }  // extern "C"

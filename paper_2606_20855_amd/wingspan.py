@@ -19,7 +19,7 @@ import numpy as np
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libwingspan.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 F32, F64 = 0, 1
 TIERS = ("tiny", "hash", "dense", "spill")
 
@@ -116,6 +116,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wingspan_spgemm_numeric.restype = i32
     lib.wingspan_spgemm.argtypes = [csr_p, csr_p, i32, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
     lib.wingspan_spgemm.restype = i32
+    lib.wingspan_spgemm_sharded.argtypes = [csr_p, csr_p, i32, vp, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
+    lib.wingspan_spgemm_sharded.restype = i32
+    lib.wingspan_sharded_to_csr_workspace_size.argtypes = [i64, P(sz)]
+    lib.wingspan_sharded_to_csr_workspace_size.restype = i32
+    lib.wingspan_sharded_to_csr.argtypes = [i64, i64, vp, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
+    lib.wingspan_sharded_to_csr.restype = i32
     _lib = lib
     return lib
 
@@ -128,6 +134,9 @@ EXPORTED = (
     "wingspan_spgemm_symbolic",
     "wingspan_spgemm_numeric",
     "wingspan_spgemm",
+    "wingspan_spgemm_sharded",
+    "wingspan_sharded_to_csr_workspace_size",
+    "wingspan_sharded_to_csr",
 )
 
 
@@ -204,6 +213,32 @@ def wingspan_spgemm(A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int
                                   c_capacity, ctypes.byref(nnz), workspace, workspace_bytes, stream or None,
                                   _opt_ptr(options)))
     return nnz.value
+
+
+def wingspan_spgemm_sharded(A: wingspan_csr, B: wingspan_csr, dtype: int, row_off: int, row_nnz: int,
+                            pool_col: int, pool_val: int, pool_capacity: int, workspace: int,
+                            workspace_bytes: int, stream: int = 0, options=None, check: bool = True):
+    """Returns (status, pool_used). With check=True a non-OK status raises."""
+    used = ctypes.c_int64(0)
+    st = load().wingspan_spgemm_sharded(ctypes.byref(A), ctypes.byref(B), dtype, row_off, row_nnz, pool_col,
+                                        pool_val, pool_capacity, ctypes.byref(used), workspace, workspace_bytes,
+                                        stream or None, _opt_ptr(options))
+    if check:
+        _check(st)
+    return st, used.value
+
+
+def wingspan_sharded_to_csr_workspace_size(nrows: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().wingspan_sharded_to_csr_workspace_size(nrows, ctypes.byref(n)))
+    return n.value
+
+
+def wingspan_sharded_to_csr(nrows: int, nnz: int, row_off: int, row_nnz: int, pool_col: int, pool_val: int,
+                            dtype: int, c_row_ptr: int, c_col_idx: int, c_val: int, workspace: int,
+                            workspace_bytes: int, stream: int = 0) -> None:
+    _check(load().wingspan_sharded_to_csr(nrows, nnz, row_off, row_nnz, pool_col, pool_val, dtype, c_row_ptr,
+                                          c_col_idx, c_val, workspace, workspace_bytes, stream or None))
 
 
 # ---------------------------------------------------------------------------
@@ -295,3 +330,65 @@ def spgemm(A: DeviceCSR, B: DeviceCSR, options=None, stream=None, workspace=None
     wingspan_spgemm_numeric(Ad, Bd, A.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
                             ws.data_ptr(), nbytes, h, options)
     return DeviceCSR(A.nrows, B.ncols, c_rp, c_col[:nnz], c_val[:nnz])
+
+
+@dataclass
+class ShardedCSR:
+    """C in sharded form: row i is pool_col[row_off[i]:row_off[i]+row_nnz[i]]
+    (values at the same positions of pool_val); rows in no particular order."""
+    nrows: int
+    ncols: int
+    row_off: "object"
+    row_nnz: "object"
+    pool_col: "object"
+    pool_val: "object"
+    nnz: int
+
+
+def spgemm_sharded(A: DeviceCSR, B: DeviceCSR, options=None, stream=None, workspace=None,
+                   pool_capacity: Optional[int] = None) -> ShardedCSR:
+    """C = A * B in one pass with sharded output. Without pool_capacity the
+    pool starts at nnz(A)+nnz(B)+64 entries and is regrown to the exact size if
+    that is too small (the call is then run again)."""
+    import torch
+    if A.val.dtype != B.val.dtype:
+        raise TypeError("A and B must share a value dtype")
+    dev = A.row_ptr.device
+    if workspace is None:
+        ws, nbytes = allocate_workspace(A, B, options)
+    else:
+        ws, nbytes = workspace, workspace.numel()
+    h = _stream_handle(stream)
+    Ad, Bd = A.desc(), B.desc()
+    row_off = torch.empty(max(A.nrows, 1), dtype=torch.int64, device=dev)
+    row_nnz = torch.empty(max(A.nrows, 1), dtype=torch.int32, device=dev)
+    cap = pool_capacity if pool_capacity is not None else A.nnz + B.nnz + 64
+    for _ in range(2):
+        pool_col = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+        pool_val = torch.empty(max(cap, 1), dtype=A.val.dtype, device=dev)
+        st, used = wingspan_spgemm_sharded(Ad, Bd, A.dtype_code, row_off.data_ptr(), row_nnz.data_ptr(),
+                                           pool_col.data_ptr(), pool_val.data_ptr(), cap, ws.data_ptr(), nbytes,
+                                           h, options, check=False)
+        if st == STATUS_CODE["WINGSPAN_ERR_INSUFFICIENT_CAPACITY"] and pool_capacity is None:
+            cap = used
+            continue
+        _check(st)
+        return ShardedCSR(A.nrows, B.ncols, row_off[:A.nrows], row_nnz[:A.nrows], pool_col, pool_val, used)
+    raise RuntimeError("pool sizing did not converge")
+
+
+def sharded_to_csr(S: ShardedCSR, stream=None) -> DeviceCSR:
+    """Gather a sharded C into plain CSR (int64 row_ptr)."""
+    import torch
+    dev = S.row_off.device
+    h = _stream_handle(stream)
+    nbytes = wingspan_sharded_to_csr_workspace_size(S.nrows)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    c_rp = torch.empty(S.nrows + 1, dtype=torch.int64, device=dev)
+    c_col = torch.empty(max(S.nnz, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(S.nnz, 1), dtype=S.pool_val.dtype, device=dev)
+    dt = F32 if S.pool_val.dtype == torch.float32 else F64
+    wingspan_sharded_to_csr(S.nrows, S.nnz, S.row_off.data_ptr(), S.row_nnz.data_ptr(), S.pool_col.data_ptr(),
+                            S.pool_val.data_ptr(), dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                            ws.data_ptr(), nbytes, h)
+    return DeviceCSR(S.nrows, S.ncols, c_rp, c_col[:S.nnz], c_val[:S.nnz])

@@ -44,7 +44,7 @@ def test_library_exports_every_header_function():
 
 
 def test_abi_version():
-    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 2
+    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 3
 
 
 def test_struct_layouts_match_header():
@@ -99,6 +99,8 @@ def test_descriptor_errors(A, B, code):
     assert got2 == code
     got3, _ = status_of(ws.wingspan_spgemm_numeric, A, B, ws.F64, FAKE, FAKE, FAKE, FAKE, 1 << 40, 0)
     assert got3 == code
+    got4, _ = status_of(ws.wingspan_spgemm_sharded, A, B, ws.F64, FAKE, FAKE, FAKE, FAKE, 10, FAKE, 1 << 40, 0)
+    assert got4 == code
 
 
 def test_null_nnz_zero_pointers_allowed():
@@ -155,8 +157,9 @@ def test_null_outputs():
     assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
 
 
-def test_last_stats_bad_phase():
-    got, _ = status_of(ws.wingspan_last_stats, 2)
+@pytest.mark.parametrize("phase", [-1, 3])
+def test_last_stats_bad_phase(phase):
+    got, _ = status_of(ws.wingspan_last_stats, phase)
     assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
 
 
@@ -166,3 +169,47 @@ def test_error_message_is_thread_local_and_cleared():
     assert "A.ncols" in ws.wingspan_last_error()
     ws.wingspan_spgemm_workspace_size(desc(3, 4, 1), desc(4, 4, 1), ws.F32)
     assert ws.wingspan_last_error() == ""
+
+
+def sharded(A, B, dtype=None, row_off=FAKE, row_nnz=FAKE, pool_col=FAKE, pool_val=FAKE, cap=10, wsp=FAKE,
+            wsb=1 << 40, options=None):
+    return ws.wingspan_spgemm_sharded(A, B, ws.F64 if dtype is None else dtype, row_off, row_nnz, pool_col,
+                                      pool_val, cap, wsp, wsb, 0, options)
+
+
+def test_sharded_argument_errors():
+    A, B = desc(10, 10, 5), desc(10, 10, 5)
+    for kw in [dict(dtype=3), dict(cap=-1), dict(row_off=0), dict(row_nnz=0), dict(pool_col=0), dict(pool_val=0),
+               dict(wsp=0), dict(wsp=FAKE + 8)]:
+        got, msg = status_of(sharded, A, B, **kw)
+        assert got == "WINGSPAN_ERR_INVALID_ARGUMENT" and msg, kw
+    need = ws.wingspan_spgemm_workspace_size(A, B, ws.F64)
+    got, msg = status_of(sharded, A, B, wsb=need - 1)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL" and str(need) in msg
+    got, _ = status_of(sharded, A, B, options=ws.make_options(max_lds_slots=100))
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    # an empty pool may be NULL (the call then only counts); empty A may pass NULL row arrays: these get past
+    # the argument checks and stop at the workspace check
+    got, _ = status_of(sharded, A, B, pool_col=0, pool_val=0, cap=0, wsb=need - 1)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"
+    E = desc(0, 10, 0, col=0, val=0)
+    got, _ = status_of(sharded, E, B, row_off=0, row_nnz=0, wsb=0)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"
+
+
+def test_sharded_to_csr_workspace_and_errors():
+    sizes = [ws.wingspan_sharded_to_csr_workspace_size(n) for n in (0, 1, 1000, 10 ** 6)]
+    assert all(b > 0 and b % 256 == 0 for b in sizes) and sizes == sorted(sizes)
+    got, _ = status_of(ws.wingspan_sharded_to_csr_workspace_size, -1)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    need = ws.wingspan_sharded_to_csr_workspace_size(10)
+    args = dict(nrows=10, nnz=5, row_off=FAKE, row_nnz=FAKE, pool_col=FAKE, pool_val=FAKE, dtype=ws.F32,
+                c_row_ptr=FAKE, c_col_idx=FAKE, c_val=FAKE, workspace=FAKE, workspace_bytes=need)
+    for kw, code in [(dict(dtype=5), "WINGSPAN_ERR_INVALID_ARGUMENT"), (dict(c_row_ptr=0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                     (dict(row_off=0), "WINGSPAN_ERR_INVALID_ARGUMENT"), (dict(nrows=-3), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                     (dict(nnz=-1), "WINGSPAN_ERR_INVALID_ARGUMENT"), (dict(pool_col=0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                     (dict(c_val=0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                     (dict(workspace_bytes=need - 1), "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"),
+                     (dict(workspace=FAKE + 8), "WINGSPAN_ERR_INVALID_ARGUMENT")]:
+        got, _ = status_of(ws.wingspan_sharded_to_csr, **{**args, **kw})
+        assert got == code, kw

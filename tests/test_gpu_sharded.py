@@ -1,0 +1,196 @@
+"""The single pass with sharded output (wingspan_spgemm_sharded): every row of
+C claims its own pool segment once its entries are known, with no symbolic
+phase. The rows, gathered into CSR, must equal the oracle's C (structure bit
+for bit, values within the tolerance), and the pool itself must hold each
+row sorted, in its own segment, never past the capacity."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import matgen
+import oracle
+from gpu_util import assert_matches
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(M):
+    from paper_2606_20855_amd import wingspan as ws
+    return ws.DeviceCSR.from_host(M, "cuda:0")
+
+
+def run_sharded(A, B, options=None, pool_capacity=None):
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    print(f"sharded: A {A.nrows}x{A.ncols} nnz={A.nnz} B {B.nrows}x{B.ncols} nnz={B.nnz} "
+          f"dtype={A.val.dtype} options={options}", flush=True)
+    dA = _dev(A)
+    dB = dA if B is A else _dev(B)
+    S = ws.spgemm_sharded(dA, dB, options=options, pool_capacity=pool_capacity)
+    st = ws.wingspan_last_stats(2)
+    C = ws.sharded_to_csr(S)
+    torch.cuda.synchronize()
+    return S, C.to_host(), st
+
+
+def check_pool(S, ref):
+    """Each row lies in its own segment of the pool, sorted; segments are
+    disjoint and together exactly fill [0, nnz(C))."""
+    off = S.row_off.cpu().numpy().astype(np.int64)
+    cnt = S.row_nnz.cpu().numpy().astype(np.int64)
+    assert np.array_equal(cnt, np.diff(ref.row_ptr)), "row_nnz differs from the oracle's row lengths"
+    assert int(cnt.sum()) == S.nnz == ref.nnz
+    live = cnt > 0
+    o, n = off[live], cnt[live]
+    order = np.argsort(o, kind="stable")
+    o, n = o[order], n[order]
+    if len(o):
+        assert o[0] == 0 and np.all(o[1:] == o[:-1] + n[:-1]), "pool segments are not a partition"
+        assert int(o[-1] + n[-1]) == S.nnz
+    col = S.pool_col[:max(S.nnz, 0)].cpu().numpy()
+    for i in np.nonzero(live)[0][:2000]:
+        seg = col[off[i]:off[i] + cnt[i]]
+        assert np.array_equal(seg, ref.col_idx[ref.row_ptr[i]:ref.row_ptr[i + 1]]), f"row {i}"
+
+
+def check(A, B, options=None, what=""):
+    S, got, st = run_sharded(A, B, options)
+    ref = oracle.spgemm(A, B)
+    assert_matches(got, ref, A.val.dtype, what=what or f"sharded {options}")
+    check_pool(S, ref)
+    assert st["total_products"] == int(ref.products.sum())
+    assert st["c_nnz_total"] == ref.nnz
+    return S, st, ref
+
+
+@pytest.mark.parametrize("shape", [(0, 0, 0), (0, 5, 3), (4, 0, 6), (5, 6, 0), (1, 1, 1), (3, 2, 7)])
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_degenerate_shapes(shape, dtype):
+    m, k, n = shape
+    A = matgen.random_sparse(m, k, 0.7, 11, dtype)
+    B = matgen.random_sparse(k, n, 0.7, 12, dtype)
+    check(A, B, what=f"shape {shape}")
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+@pytest.mark.parametrize("shape,density", [((60, 70, 80), 0.1), ((200, 150, 300), 0.05), ((33, 1000, 17), 0.2)])
+def test_random(shape, density, dtype):
+    m, k, n = shape
+    A = matgen.random_sparse(m, k, density, 13, dtype, empty_rows=0.2)
+    B = matgen.random_sparse(k, n, density, 14, dtype)
+    check(A, B)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+@pytest.mark.parametrize("opts", [None, dict(tiny_max=-1), dict(max_lds_slots=64), dict(force_spill=1),
+                                  dict(max_lds_slots=64, dense_min_nnz=-1)])
+def test_tiers_rmat(opts, dtype):
+    # R-MAT scale 11: rows from a handful of products to thousands, so every
+    # tier writes to the pool; max_lds_slots=64 sends most rows to the rank
+    # kernel, dense_min_nnz=-1 (no dense tier) to the spill tier
+    A = matgen.rmat(11, 16, seed=61, dtype=dtype, dist="open01" if dtype == np.float32 else "pm1")
+    S, st, ref = check(A, A, opts, what=f"rmat11 {opts}")
+    if opts and opts.get("max_lds_slots") == 64 and "dense_min_nnz" not in opts:
+        assert st["rows"]["dense"] > 0
+    if opts and (opts.get("force_spill") or opts.get("dense_min_nnz") == -1):
+        assert st["rows"]["spill"] > 0
+
+
+def test_laplacian_bit_exact():
+    A = matgen.laplacian2d(64)
+    S, got, st = run_sharded(A, A)
+    ref = oracle.spgemm(A, A)
+    assert np.array_equal(got.row_ptr, ref.row_ptr) and np.array_equal(got.col_idx, ref.col_idx)
+    assert np.array_equal(got.val, ref.val.astype(got.val.dtype))
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_arrowhead_dense_rows(dtype):
+    # every row of A*A is full (4096 entries): rank kernel rows written to the pool
+    n = 4096
+    A = matgen.arrowhead(n, dtype)
+    S, got, st = run_sharded(A, A, dict(max_lds_slots=1024))
+    assert st["rows"]["dense"] > 0
+    assert got.row_ptr[-1] == n * n
+    assert np.array_equal(got.col_idx.reshape(n, n), np.tile(np.arange(n, dtype=np.int32), (n, 1)))
+    E = np.ones((n, n))
+    E[0, :] = 2
+    E[:, 0] = 2
+    E[np.arange(n), np.arange(n)] = 2
+    E[0, 0] = n
+    assert np.array_equal(got.val.reshape(n, n), E)
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_wide_rows_spill_to_pool(dtype):
+    # 300K columns: more than one rank region, so the single pass sends the
+    # long rows to the spill tier, which claims after its count
+    dist = "pm1" if dtype == np.float64 else "open01"
+    A = matgen.er(24, 2500, 300, seed=63, dtype=dtype, dist=dist)
+    B = matgen.er(2500, 300_000, 30, seed=64, dtype=dtype, dist=dist)
+    S, st, ref = check(A, B, what="wide rows")
+    assert st["rows"]["dense"] == 0 and st["rows"]["spill"] > 0
+
+
+def test_same_structure_as_two_phase():
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(10, 16, seed=65, dtype=np.float32)
+    dA = _dev(A)
+    two = ws.spgemm(dA, dA).to_host()
+    S = ws.spgemm_sharded(dA, dA)
+    one = ws.sharded_to_csr(S).to_host()
+    assert np.array_equal(one.row_ptr, two.row_ptr) and np.array_equal(one.col_idx, two.col_idx)
+    ref = oracle.spgemm(A, A)
+    assert_matches(one, ref, A.val.dtype, what="single pass vs two phase")
+
+
+def test_pool_too_small_reports_size_and_writes_nothing_past_it():
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(10, 16, seed=66, dtype=np.float64, dist="pm1")
+    ref = oracle.spgemm(A, A)
+    dA = _dev(A)
+    nbytes = ws.wingspan_spgemm_workspace_size(dA.desc(), dA.desc(), ws.F64)
+    wsb = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    m = A.nrows
+    row_off = torch.empty(m, dtype=torch.int64, device="cuda:0")
+    row_nnz = torch.empty(m, dtype=torch.int32, device="cuda:0")
+    cap = ref.nnz // 3
+    guard = 4096
+    pool_col = torch.full((cap + guard,), -7, dtype=torch.int32, device="cuda:0")
+    pool_val = torch.full((cap + guard,), 3.5, dtype=torch.float64, device="cuda:0")
+    st, used = ws.wingspan_spgemm_sharded(dA.desc(), dA.desc(), ws.F64, row_off.data_ptr(), row_nnz.data_ptr(),
+                                          pool_col.data_ptr(), pool_val.data_ptr(), cap, wsb.data_ptr(), nbytes,
+                                          0, None, check=False)
+    torch.cuda.synchronize()
+    assert ws.STATUS[st] == "WINGSPAN_ERR_INSUFFICIENT_CAPACITY"
+    assert used == ref.nnz
+    assert np.array_equal(row_nnz.cpu().numpy(), np.diff(ref.row_ptr))
+    assert torch.all(pool_col[cap:] == -7) and torch.all(pool_val[cap:] == 3.5)
+    # the rows that fit were written in full
+    off = row_off.cpu().numpy()
+    cnt = row_nnz.cpu().numpy()
+    col = pool_col.cpu().numpy()
+    fit = np.nonzero((cnt > 0) & (off + cnt <= cap))[0]
+    assert len(fit) > 0
+    for i in fit[:500]:
+        assert np.array_equal(col[off[i]:off[i] + cnt[i]], ref.col_idx[ref.row_ptr[i]:ref.row_ptr[i + 1]])
+    # retry at the reported size
+    S = ws.spgemm_sharded(dA, dA, pool_capacity=used)
+    got = ws.sharded_to_csr(S).to_host()
+    assert_matches(got, ref, np.float64, what="after retry")
+
+
+def test_rerun_reuses_buffers():
+    # a second call over the same outputs and workspace gives the same C
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(10, 8, seed=67, dtype=np.float32)
+    dA = _dev(A)
+    wsb, nbytes = ws.allocate_workspace(dA, dA)
+    S1 = ws.spgemm_sharded(dA, dA, workspace=wsb)
+    c1 = ws.sharded_to_csr(S1).to_host()
+    S2 = ws.spgemm_sharded(dA, dA, workspace=wsb, pool_capacity=S1.nnz)
+    c2 = ws.sharded_to_csr(S2).to_host()
+    assert np.array_equal(c1.row_ptr, c2.row_ptr) and np.array_equal(c1.col_idx, c2.col_idx)
+    assert_matches(c2, oracle.spgemm(A, A), A.val.dtype, what="rerun")
