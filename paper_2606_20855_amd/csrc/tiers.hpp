@@ -752,7 +752,9 @@ struct SliceRange {
 // When slot_of_row is not null, a row with slot_of_row[row] >= 0 takes its
 // column bitmap from that row of the structure cache (written by the symbolic
 // phase for the same A and B) instead of running the structure pass.
-template <typename V>
+// POOL selects the output: CSR at C.row_ptr, or pool segments claimed through
+// the sink (compiled apart, so the CSR kernel carries none of the pool state).
+template <typename V, bool POOL>
 __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     Mats<V> M, const int32_t *__restrict__ rows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
     RowSink out, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
@@ -776,7 +778,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ double e_av[kCacheEntries];
 
     // pool output needs a row's entry count before its first write: one region only
-    if (out.pooled() && nwin > SH::REGION_WINS) {
+    if (POOL && nwin > SH::REGION_WINS) {
         if (threadIdx.x == 0) atomicOr(&ctrl->error_flags, kErrPoolLayout);
         return;
     }
@@ -785,7 +787,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     // CSR output: the row's place from C.row_ptr. Pool output: claimed once the region's entry count is
     // known
     int64_t cb = 0, seg = 0;
-    if (!out.pooled()) {
+    if (!POOL) {
         cb = out.c_rp[row];
         seg = out.c_rp[row + 1] - cb;
     }
@@ -890,9 +892,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
 #pragma unroll
         for (int i = 0; i < NW; ++i) region_total += scratch[i];
         region_total = uniform(region_total);
-        if (out.pooled() && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
+        if (POOL && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
         __syncthreads();
-        if (out.pooled()) {
+        if (POOL) {
             cb = uniform(s_claim[0]);
             seg = uniform(s_claim[1]);
         }
@@ -1012,7 +1014,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         }
         done += region_total;
     }
-    if (threadIdx.x == 0 && !out.pooled() && done != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+    if (threadIdx.x == 0 && !POOL && done != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
 }
 
 // ---------------------------------------------------------------------------

@@ -685,7 +685,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt && c.L.rank_mode) {
         const bool cached = stamp_matches(c, A, B);
         stats.structure_cache_rows = cached ? c.host_stamp.cached_rows : 0;
-        dense_rank_kernel<V><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+        dense_rank_kernel<V, false><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
             M, perm + start, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl,
             cached ? c.slot_of_row : nullptr, cached ? c.cache : nullptr, c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
@@ -782,7 +782,7 @@ wingspan_status sharded_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt) {
         // binning sends dense rows here only in rank mode with one region; the column bitmaps come from the
         // kernel's own structure pass
-        dense_rank_kernel<V><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+        dense_rank_kernel<V, true><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
             M, perm + start, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr, nullptr,
             c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
