@@ -230,6 +230,41 @@ wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_
                                         int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
                                         void *workspace_dev, size_t workspace_bytes, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Elementwise operations on two CSR matrices of one shape (the paper's
+ * sparse linear algebra evaluation, Section 5.2: SpAdd and the Hadamard
+ * product).
+ *
+ *   WINGSPAN_OP_ADD:      C = A + B, stored on the union of A's and B's
+ *                         coordinates; a coordinate stored on both sides takes
+ *                         a + b and stays stored even when that is zero.
+ *   WINGSPAN_OP_HADAMARD: C = A .* B, stored on the intersection, a * b.
+ *
+ * Values are formed in double and rounded once to dtype, so they equal the
+ * exact sum or product correctly rounded (bit for bit the same on any
+ * hardware). Rows of C have strictly increasing columns. C.row_ptr is int64.
+ *
+ * wingspan_elementwise_structure writes c_row_ptr_dev (A.nrows+1 entries) and
+ * *c_nnz (host); it synchronizes `stream` once, to return *c_nnz. A.val and
+ * B.val are not read. wingspan_elementwise_values then fills c_col_idx_dev
+ * (int32) and c_val_dev for that c_row_ptr_dev and the same A and B patterns
+ * (so it can be re-run for new values); it is asynchronous. Both take the
+ * workspace wingspan_elementwise_workspace_size gives (pure host code, a
+ * function of the sizes only).
+ * ------------------------------------------------------------------------ */
+typedef enum { WINGSPAN_OP_ADD = 0, WINGSPAN_OP_HADAMARD = 1 } wingspan_ew_op;
+
+wingspan_status wingspan_elementwise_workspace_size(const wingspan_csr *A, const wingspan_csr *B, size_t *bytes);
+
+wingspan_status wingspan_elementwise_structure(wingspan_ew_op op, const wingspan_csr *A, const wingspan_csr *B,
+                                               int64_t *c_row_ptr_dev, int64_t *c_nnz, void *workspace_dev,
+                                               size_t workspace_bytes, void *stream);
+
+wingspan_status wingspan_elementwise_values(wingspan_ew_op op, const wingspan_csr *A, const wingspan_csr *B,
+                                            wingspan_dtype dtype, const int64_t *c_row_ptr_dev,
+                                            int32_t *c_col_idx_dev, void *c_val_dev, void *workspace_dev,
+                                            size_t workspace_bytes, void *stream);
+
 /* Statistics of the last call on this thread: phase 0 = symbolic, 1 = numeric,
  * 2 = single pass (wingspan_spgemm_sharded). */
 wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out);

@@ -17,6 +17,7 @@ from .generators import (
     permutation,
     diagonal,
     random_sparse,
+    shuffled_copy,
 )
 
 __all__ = [
@@ -32,4 +33,5 @@ __all__ = [
     "permutation",
     "diagonal",
     "random_sparse",
+    "shuffled_copy",
 ]

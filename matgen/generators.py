@@ -151,6 +151,20 @@ def arrowhead(n: int, dtype=np.float64) -> CSR:
     return CSR(n, n, rp, ci, np.ones(len(ci), dtype=dtype))
 
 
+def shuffled_copy(M: CSR, seed) -> CSR:
+    """M with its rows and columns relabelled by two seeded random
+    permutations (B[p(i), q(j)] = M[i, j]): the same values and degree
+    distribution on a different pattern."""
+    rng = _rng(seed)
+    p = rng.permutation(M.nrows).astype(np.int64)
+    q = rng.permutation(M.ncols).astype(np.int64)
+    rows = np.repeat(np.arange(M.nrows, dtype=np.int64), np.diff(M.row_ptr))
+    keys = p[rows] * max(M.ncols, 1) + q[M.col_idx.astype(np.int64)]
+    order = np.argsort(keys, kind="stable")
+    rp, ci = _csr_from_sorted_keys(keys[order], M.nrows, M.ncols)
+    return CSR(M.nrows, M.ncols, rp, ci, M.val[order].copy())
+
+
 def identity(n: int, dtype=np.float64) -> CSR:
     return CSR(n, n, np.arange(n + 1, dtype=np.int32), np.arange(n, dtype=np.int32),
                np.ones(n, dtype=dtype))

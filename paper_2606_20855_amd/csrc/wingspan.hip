@@ -20,6 +20,7 @@
 #include "analysis.hpp"
 #include "device_common.hpp"
 #include "tiers.hpp"
+#include "elementwise.hpp"
 
 using namespace wsp;
 
@@ -845,6 +846,92 @@ wingspan_status setup(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, cons
     return WINGSPAN_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Elementwise operations (SpAdd, Hadamard): workspace layout and checks.
+// ---------------------------------------------------------------------------
+struct EwLayout {
+    size_t off_dups, off_rank, off_pos, off_partials, total;
+};
+
+EwLayout ew_plan(const wingspan_csr *A, const wingspan_csr *B) {
+    EwLayout L{};
+    const int64_t m = std::max<int64_t>(A->nrows, 1), na = std::max<int64_t>(A->nnz, 1);
+    size_t off = 0;
+    L.off_dups = off;
+    off += align_up(sizeof(int32_t) * m);
+    L.off_rank = off;
+    off += align_up(sizeof(int32_t) * na);
+    L.off_pos = off;
+    off += align_up(sizeof(int64_t) * (na + 1));
+    L.off_partials = off;
+    const int64_t n = std::max<int64_t>({A->nnz, B->nnz, A->nrows + 1});
+    off += align_up(sizeof(int64_t) * ((n + kScanTile - 1) / kScanTile + 2));
+    L.total = off;
+    return L;
+}
+
+wingspan_status ew_check(int op, const wingspan_csr *A, const wingspan_csr *B) {
+    if (op != WINGSPAN_OP_ADD && op != WINGSPAN_OP_HADAMARD)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "op must be WINGSPAN_OP_ADD or WINGSPAN_OP_HADAMARD");
+    wingspan_status s = check_csr_desc(A, "A");
+    if (s != WINGSPAN_OK) return s;
+    if ((s = check_csr_desc(B, "B")) != WINGSPAN_OK) return s;
+    if (A->nrows != B->nrows || A->ncols != B->ncols)
+        return fail(WINGSPAN_ERR_DIMENSION_MISMATCH, "A is %lldx%lld but B is %lldx%lld", (long long)A->nrows,
+                    (long long)A->ncols, (long long)B->nrows, (long long)B->ncols);
+    return WINGSPAN_OK;
+}
+
+wingspan_status ew_workspace(const wingspan_csr *A, const wingspan_csr *B, void *ws, size_t ws_bytes,
+                             EwLayout *L) {
+    *L = ew_plan(A, B);
+    if (ws_bytes < L->total)
+        return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", ws_bytes, L->total);
+    if (!ws) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kAlign);
+    return WINGSPAN_OK;
+}
+
+unsigned ew_grid(int64_t nnz) { return static_cast<unsigned>((nnz + kEwChunk - 1) / kEwChunk); }
+
+template <typename V>
+wingspan_status ew_values_impl(Ctx &c, int op, const wingspan_csr *A, const wingspan_csr *B, const EwLayout &L,
+                               const int64_t *c_rp, int32_t *c_col, V *c_val) {
+    const int m = static_cast<int>(A->nrows);
+    const V *av = static_cast<const V *>(A->val), *bv = static_cast<const V *>(B->val);
+    if (m == 0) return WINGSPAN_OK;
+    int32_t *rank = reinterpret_cast<int32_t *>(c.ws + L.off_rank);
+    int64_t *pos = reinterpret_cast<int64_t *>(c.ws + L.off_pos);
+    if (op == WINGSPAN_OP_ADD) {
+        // A's ranks in B and the prefix count of the columns both store, then each side writes its entries
+        if (A->nnz > 0)
+            ew_match<<<ew_grid(A->nnz), kEwBlock, 0, c.st>>>(A->row_ptr, A->col_idx, B->row_ptr, B->col_idx, m,
+                                                             A->nnz, nullptr, rank);
+        LAUNCH_CHECK("elementwise match");
+        wingspan_status s = run_scan(c, EwDupIn{rank}, A->nnz, pos);
+        if (s != WINGSPAN_OK) return s;
+        if (A->nnz > 0)
+            ew_add_a<V><<<ew_grid(A->nnz), kEwBlock, 0, c.st>>>(A->row_ptr, A->col_idx, av, B->row_ptr, bv, m,
+                                                                A->nnz, rank, pos, c_rp, c_col, c_val);
+        if (B->nnz > 0)
+            ew_add_b<V><<<ew_grid(B->nnz), kEwBlock, 0, c.st>>>(A->row_ptr, A->col_idx, B->row_ptr, B->col_idx, bv,
+                                                                m, B->nnz, pos, c_rp, c_col, c_val);
+        LAUNCH_CHECK("elementwise sum");
+        return WINGSPAN_OK;
+    }
+    if (A->nnz == 0 || B->nnz == 0) return WINGSPAN_OK;   // the product is empty
+    ew_match<<<ew_grid(A->nnz), kEwBlock, 0, c.st>>>(A->row_ptr, A->col_idx, B->row_ptr, B->col_idx, m, A->nnz,
+                                                     nullptr, rank);
+    LAUNCH_CHECK("elementwise match");
+    wingspan_status s = run_scan(c, EwDupIn{rank}, A->nnz, pos);
+    if (s != WINGSPAN_OK) return s;
+    ew_mul_write<V><<<ew_grid(A->nnz), kEwBlock, 0, c.st>>>(A->row_ptr, A->col_idx, av, B->row_ptr, bv, m, A->nnz,
+                                                            rank, pos, c_col, c_val);
+    LAUNCH_CHECK("elementwise product");
+    return WINGSPAN_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1027,6 +1114,71 @@ wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_
         LAUNCH_CHECK("gather_rows");
     }
     return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_elementwise_workspace_size(const wingspan_csr *A, const wingspan_csr *B, size_t *bytes) {
+    g_err.clear();
+    if (!bytes) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    wingspan_status s = ew_check(WINGSPAN_OP_ADD, A, B);
+    if (s != WINGSPAN_OK) return s;
+    *bytes = ew_plan(A, B).total;
+    return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_elementwise_structure(wingspan_ew_op op, const wingspan_csr *A, const wingspan_csr *B,
+                                               int64_t *c_row_ptr_dev, int64_t *c_nnz, void *workspace_dev,
+                                               size_t workspace_bytes, void *stream) {
+    g_err.clear();
+    wingspan_status s = ew_check(op, A, B);
+    if (s != WINGSPAN_OK) return s;
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    if (!c_nnz) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_nnz is NULL");
+    EwLayout L;
+    if ((s = ew_workspace(A, B, workspace_dev, workspace_bytes, &L)) != WINGSPAN_OK) return s;
+    Ctx c{};
+    c.st = static_cast<hipStream_t>(stream);
+    c.ws = static_cast<char *>(workspace_dev);
+    c.partials = reinterpret_cast<int64_t *>(c.ws + L.off_partials);
+    int32_t *dups = reinterpret_cast<int32_t *>(c.ws + L.off_dups);
+    const int m = static_cast<int>(A->nrows);
+    if (m > 0) {
+        fill_i32<<<blocks_for(m, 256), 256, 0, c.st>>>(dups, m, 0);
+        if (A->nnz > 0 && B->nnz > 0)
+            ew_match<<<ew_grid(A->nnz), kEwBlock, 0, c.st>>>(A->row_ptr, A->col_idx, B->row_ptr, B->col_idx, m,
+                                                             A->nnz, dups, nullptr);
+        LAUNCH_CHECK("elementwise match");
+    }
+    if ((s = run_scan(c, EwCountIn{A->row_ptr, B->row_ptr, dups, static_cast<int>(op)}, m, c_row_ptr_dev)) !=
+        WINGSPAN_OK)
+        return s;
+    int64_t total = 0;
+    HIP_TRY(hipMemcpyAsync(&total, c_row_ptr_dev + m, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    *c_nnz = total;
+    return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_elementwise_values(wingspan_ew_op op, const wingspan_csr *A, const wingspan_csr *B,
+                                            wingspan_dtype dtype, const int64_t *c_row_ptr_dev,
+                                            int32_t *c_col_idx_dev, void *c_val_dev, void *workspace_dev,
+                                            size_t workspace_bytes, void *stream) {
+    g_err.clear();
+    wingspan_status s = ew_check(op, A, B);
+    if (s != WINGSPAN_OK) return s;
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    if ((A->nnz > 0 || B->nnz > 0) && (!c_col_idx_dev || !c_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_col_idx_dev or c_val_dev is NULL");
+    EwLayout L;
+    if ((s = ew_workspace(A, B, workspace_dev, workspace_bytes, &L)) != WINGSPAN_OK) return s;
+    Ctx c{};
+    c.st = static_cast<hipStream_t>(stream);
+    c.ws = static_cast<char *>(workspace_dev);
+    c.partials = reinterpret_cast<int64_t *>(c.ws + L.off_partials);
+    if (dtype == WINGSPAN_F32)
+        return ew_values_impl<float>(c, op, A, B, L, c_row_ptr_dev, c_col_idx_dev, static_cast<float *>(c_val_dev));
+    return ew_values_impl<double>(c, op, A, B, L, c_row_ptr_dev, c_col_idx_dev, static_cast<double *>(c_val_dev));
 }
 
 }  // extern "C"

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_PKG, "libwingspan.so")
 
 ABI_VERSION = 3
 F32, F64 = 0, 1
+OP_ADD, OP_HADAMARD = 0, 1
 TIERS = ("tiny", "hash", "dense", "spill")
 
 STATUS = {
@@ -122,6 +123,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wingspan_sharded_to_csr_workspace_size.restype = i32
     lib.wingspan_sharded_to_csr.argtypes = [i64, i64, vp, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
     lib.wingspan_sharded_to_csr.restype = i32
+    lib.wingspan_elementwise_workspace_size.argtypes = [csr_p, csr_p, P(sz)]
+    lib.wingspan_elementwise_workspace_size.restype = i32
+    lib.wingspan_elementwise_structure.argtypes = [i32, csr_p, csr_p, vp, P(i64), vp, sz, vp]
+    lib.wingspan_elementwise_structure.restype = i32
+    lib.wingspan_elementwise_values.argtypes = [i32, csr_p, csr_p, i32, vp, vp, vp, vp, sz, vp]
+    lib.wingspan_elementwise_values.restype = i32
     _lib = lib
     return lib
 
@@ -137,6 +144,9 @@ EXPORTED = (
     "wingspan_spgemm_sharded",
     "wingspan_sharded_to_csr_workspace_size",
     "wingspan_sharded_to_csr",
+    "wingspan_elementwise_workspace_size",
+    "wingspan_elementwise_structure",
+    "wingspan_elementwise_values",
 )
 
 
@@ -239,6 +249,27 @@ def wingspan_sharded_to_csr(nrows: int, nnz: int, row_off: int, row_nnz: int, po
                             workspace_bytes: int, stream: int = 0) -> None:
     _check(load().wingspan_sharded_to_csr(nrows, nnz, row_off, row_nnz, pool_col, pool_val, dtype, c_row_ptr,
                                           c_col_idx, c_val, workspace, workspace_bytes, stream or None))
+
+
+def wingspan_elementwise_workspace_size(A: wingspan_csr, B: wingspan_csr) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().wingspan_elementwise_workspace_size(ctypes.byref(A), ctypes.byref(B), ctypes.byref(n)))
+    return n.value
+
+
+def wingspan_elementwise_structure(op: int, A: wingspan_csr, B: wingspan_csr, c_row_ptr: int, workspace: int,
+                                   workspace_bytes: int, stream: int = 0) -> int:
+    nnz = ctypes.c_int64(0)
+    _check(load().wingspan_elementwise_structure(op, ctypes.byref(A), ctypes.byref(B), c_row_ptr, ctypes.byref(nnz),
+                                                 workspace, workspace_bytes, stream or None))
+    return nnz.value
+
+
+def wingspan_elementwise_values(op: int, A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int,
+                                c_col_idx: int, c_val: int, workspace: int, workspace_bytes: int,
+                                stream: int = 0) -> None:
+    _check(load().wingspan_elementwise_values(op, ctypes.byref(A), ctypes.byref(B), dtype, c_row_ptr, c_col_idx,
+                                              c_val, workspace, workspace_bytes, stream or None))
 
 
 # ---------------------------------------------------------------------------
@@ -392,3 +423,23 @@ def sharded_to_csr(S: ShardedCSR, stream=None) -> DeviceCSR:
                             S.pool_val.data_ptr(), dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
                             ws.data_ptr(), nbytes, h)
     return DeviceCSR(S.nrows, S.ncols, c_rp, c_col[:S.nnz], c_val[:S.nnz])
+
+
+def elementwise(op: str, A: DeviceCSR, B: DeviceCSR, stream=None) -> DeviceCSR:
+    """C = A + B (op "add") or C = A .* B (op "hadamard") on the GPU."""
+    import torch
+    if A.val.dtype != B.val.dtype:
+        raise TypeError("A and B must share a value dtype")
+    code = {"add": OP_ADD, "hadamard": OP_HADAMARD}[op]
+    dev = A.row_ptr.device
+    Ad, Bd = A.desc(), B.desc()
+    nbytes = wingspan_elementwise_workspace_size(Ad, Bd)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    h = _stream_handle(stream)
+    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device=dev)
+    nnz = wingspan_elementwise_structure(code, Ad, Bd, c_rp.data_ptr(), ws.data_ptr(), nbytes, h)
+    c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(nnz, 1), dtype=A.val.dtype, device=dev)
+    wingspan_elementwise_values(code, Ad, Bd, A.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                                ws.data_ptr(), nbytes, h)
+    return DeviceCSR(A.nrows, A.ncols, c_rp, c_col[:nnz], c_val[:nnz])

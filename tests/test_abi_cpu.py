@@ -213,3 +213,28 @@ def test_sharded_to_csr_workspace_and_errors():
                      (dict(workspace=FAKE + 8), "WINGSPAN_ERR_INVALID_ARGUMENT")]:
         got, _ = status_of(ws.wingspan_sharded_to_csr, **{**args, **kw})
         assert got == code, kw
+
+
+def test_elementwise_argument_errors():
+    A, B = desc(10, 12, 5), desc(10, 12, 7)
+    need = ws.wingspan_elementwise_workspace_size(A, B)
+    assert need > 0 and need % 256 == 0
+    assert ws.wingspan_elementwise_workspace_size(desc(10, 12, 5000), B) > need
+    got, _ = status_of(ws.wingspan_elementwise_workspace_size, A, desc(10, 13, 7))
+    assert got == "WINGSPAN_ERR_DIMENSION_MISMATCH"
+    got, _ = status_of(ws.wingspan_elementwise_structure, ws.OP_ADD, A, desc(11, 12, 7), FAKE, FAKE, need, 0)
+    assert got == "WINGSPAN_ERR_DIMENSION_MISMATCH"
+    for args, code in [((5, A, B, FAKE, FAKE, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((ws.OP_ADD, A, B, 0, FAKE, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((ws.OP_ADD, A, B, FAKE, FAKE, need - 1, 0), "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"),
+                       ((ws.OP_HADAMARD, A, B, FAKE, 0, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((ws.OP_HADAMARD, A, B, FAKE, FAKE + 8, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT")]:
+        got, _ = status_of(ws.wingspan_elementwise_structure, *args)
+        assert got == code, args
+    for args, code in [((ws.OP_ADD, A, B, 9, FAKE, FAKE, FAKE, FAKE, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((ws.OP_ADD, A, B, ws.F32, FAKE, 0, FAKE, FAKE, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((ws.OP_ADD, A, B, ws.F32, 0, FAKE, FAKE, FAKE, need, 0), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((ws.OP_HADAMARD, A, B, ws.F64, FAKE, FAKE, FAKE, FAKE, need - 256, 0),
+                        "WINGSPAN_ERR_WORKSPACE_TOO_SMALL")]:
+        got, _ = status_of(ws.wingspan_elementwise_values, *args)
+        assert got == code, args
