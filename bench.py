@@ -11,8 +11,12 @@ input, writing into a preallocated C. Prints one JSON line:
              algorithmic bytes and its HIP-event time on the library's stream
   numeric_phase  algorithmic bytes of the numeric phase / its time
   cpu_baseline   the CPU oracle (single thread) on a seeded random sample of rows
+  sharded_single_pass  the single pass with sharded output on the same workload
+  elementwise    SpAdd and the Hadamard product (B = A, and B a shuffled copy)
+                 on the R-MAT scale-20 matrix, against HBM bandwidth
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rmat18]
+       python bench.py --elementwise-only [--ew-workload rmat20]
        python bench.py --calibrate-copy BYTES
 The second form only copies BYTES bytes device to device three times (the
 runtime's plain copy kernel): run under rocprofv3 --pmc FETCH_SIZE or
@@ -150,6 +154,61 @@ def sharded_pass(ws, torch, dA, dB, nnz_c, P, steps, warmup):
                 to_csr_ms=round(to_csr_ms, 4), pool_entries=nnz_c)
 
 
+def ew_alg_bytes(m, na, nb, nc, s, op):
+    """Least HBM bytes of C = A op B in CSR: both row pointers and column
+    arrays read once, C's row pointer (int64), columns and values written once;
+    the sum reads every value, the product only those of the common entries."""
+    vals = s * (na + nb) if op == "add" else 2 * s * nc
+    return 2 * 4 * (m + 1) + 4 * (na + nb) + vals + 8 * (m + 1) + (4 + s) * nc
+
+
+def elementwise_pass(ws, torch, workload, dev, steps, warmup, seed):
+    """SpAdd and the Hadamard product on a workload's A, in the identity case
+    (B = A) and the shuffled case (B = A with rows and columns relabelled by
+    seeded permutations). Each op is timed whole (structure with its count
+    read back, then values) and values alone, with HIP events on its stream."""
+    import matgen
+    A = matgen.config(workload)[0]
+    dA = ws.DeviceCSR.from_host(A, dev)
+    h = torch.cuda.current_stream().cuda_stream
+    s = A.val.dtype.itemsize
+    m = A.nrows
+    Bs = matgen.shuffled_copy(A, seed)
+    dBs = ws.DeviceCSR.from_host(Bs, dev)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    out = {}
+    for case, dB in (("identity", dA), ("shuffled", dBs)):
+        Ad, Bd = dA.desc(), dB.desc()
+        nbytes = ws.wingspan_elementwise_workspace_size(Ad, Bd)
+        wsb = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+        c_rp = torch.empty(m + 1, dtype=torch.int64, device=dev)
+        for op, code in (("add", ws.OP_ADD), ("hadamard", ws.OP_HADAMARD)):
+            nc = ws.wingspan_elementwise_structure(code, Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h)
+            c_col = torch.empty(max(nc, 1), dtype=torch.int32, device=dev)
+            c_val = torch.empty(max(nc, 1), dtype=dA.val.dtype, device=dev)
+
+            def run():
+                e[0].record()
+                ws.wingspan_elementwise_structure(code, Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h)
+                e[1].record()
+                ws.wingspan_elementwise_values(code, Ad, Bd, dA.dtype_code, c_rp.data_ptr(), c_col.data_ptr(),
+                                               c_val.data_ptr(), wsb.data_ptr(), nbytes, h)
+                e[2].record()
+                e[2].synchronize()
+                return e[0].elapsed_time(e[2]), e[1].elapsed_time(e[2])
+
+            for _ in range(warmup):
+                run()
+            tot, val = zip(*[run() for _ in range(steps)])
+            t = float(np.mean(tot))
+            b = ew_alg_bytes(m, dA.nnz, dB.nnz, nc, s, op)
+            out[f"{op}_{case}"] = dict(ms=round(t, 4), values_ms=round(float(np.mean(val)), 4), nnz_c=nc,
+                                       alg_bytes=b, GBps=round(b / (t / 1e3) / 1e9, 1),
+                                       frac=round(b / (t / 1e3) / 1e9 / HBM_PEAK_GBPS, 4))
+            del c_col, c_val
+    return dict(workload=f"{workload} A: m={A.nrows}, nnz={A.nnz}, {A.val.dtype}", **out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -160,6 +219,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     ap.add_argument("--no-sharded", action="store_true", help="skip the single-pass (sharded output) timing")
+    ap.add_argument("--no-elementwise", action="store_true", help="skip the SpAdd / Hadamard timing")
+    ap.add_argument("--ew-workload", default="rmat20", help="the matrix A of the SpAdd / Hadamard timing")
+    ap.add_argument("--elementwise-only", action="store_true",
+                    help="time only SpAdd / Hadamard and print their JSON object")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -183,6 +246,10 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.elementwise_only:
+        ew = elementwise_pass(ws, torch, args.ew_workload, dev, args.steps, args.warmup, seed=20262)
+        print(json.dumps(dict(elementwise=ew, steps=args.steps, warmup=args.warmup)), flush=True)
+        return
     cfg = matgen.CONFIGS[args.workload]
     t0 = time.time()
     A, B = matgen.config(args.workload)
@@ -292,6 +359,9 @@ def main():
         sh = sharded_pass(ws, torch, dA, dB, nnz_c, P, args.steps, args.warmup)
         sh["vs_two_phase_step"] = round(ms_per_step / sh["ms"], 3)
         out["sharded_single_pass"] = sh
+    if not args.no_elementwise:
+        log("timing SpAdd and the Hadamard product (identity and shuffled B)")
+        out["elementwise"] = elementwise_pass(ws, torch, args.ew_workload, dev, args.steps, args.warmup, seed=20262)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a row sample")
         out["cpu_baseline"] = cpu_baseline(A, B, args.cpu_fraction, seed=20261)

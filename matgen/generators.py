@@ -160,7 +160,7 @@ def shuffled_copy(M: CSR, seed) -> CSR:
     q = rng.permutation(M.ncols).astype(np.int64)
     rows = np.repeat(np.arange(M.nrows, dtype=np.int64), np.diff(M.row_ptr))
     keys = p[rows] * max(M.ncols, 1) + q[M.col_idx.astype(np.int64)]
-    order = np.argsort(keys, kind="stable")
+    order = np.argsort(keys)   # the keys are distinct, so any sort gives this order
     rp, ci = _csr_from_sorted_keys(keys[order], M.nrows, M.ncols)
     return CSR(M.nrows, M.ncols, rp, ci, M.val[order].copy())
 

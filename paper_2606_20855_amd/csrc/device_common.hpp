@@ -62,7 +62,7 @@ struct Control {
     int32_t spill_next;
     int32_t error_flags;
     int32_t has_zero_values;   // some A or B value could give a zero product
-    int32_t pad_;
+    int32_t rank_next;         // the rank kernel's row claims
     uint64_t rp_sum;           // numeric: checksum of the C.row_ptr it was given
     int32_t bin_count[kMaxBins];
     int32_t bin_offset[kMaxBins];

@@ -749,16 +749,56 @@ struct SliceRange {
     }
 };
 
-// When slot_of_row is not null, a row with slot_of_row[row] >= 0 takes its
-// column bitmap from that row of the structure cache (written by the symbolic
-// phase for the same A and B) instead of running the structure pass.
+// A row of the rank kernel, gathered beforehand so that a workgroup fetches
+// the next row's description with one load.
+struct RankRow {
+    int32_t row, a_lo, a_hi;
+    int32_t slot;     // the row's structure cache row, or -1
+    int64_t cb, seg;  // CSR output: C.row_ptr[row] and the row's entry count
+};
+static_assert(sizeof(RankRow) == 32, "two 16-byte loads");
+
+__global__ void __launch_bounds__(256) rank_rows(const int32_t *__restrict__ rows, int n,
+                                                 const int32_t *__restrict__ a_rp, const int64_t *__restrict__ c_rp,
+                                                 const int32_t *__restrict__ slot_of_row, RankRow *__restrict__ out) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int row = rows[i];
+    RankRow r;
+    r.row = row;
+    r.a_lo = a_rp[row];
+    r.a_hi = a_rp[row + 1];
+    r.slot = slot_of_row != nullptr ? slot_of_row[row] : -1;
+    r.cb = c_rp != nullptr ? c_rp[row] : 0;
+    r.seg = c_rp != nullptr ? c_rp[row + 1] - r.cb : 0;
+    out[i] = r;
+}
+
+// A zero the compiler cannot see through: an address offset by it is not
+// uniform, so the load is a vector load. Prefetches must be vector loads:
+// a scalar load counts with the LDS operations, and every barrier and LDS wait
+// would then wait for it too.
+__device__ __forceinline__ int opaque_zero() {
+    int z = 0;
+    asm volatile("" : "+v"(z));
+    return z;
+}
+
+// Rank-indexed dense rows. The grid is persistent (one workgroup per CU, the
+// LDS allows no more): workgroups claim rows from a counter in the order of
+// `rr` (heaviest first), one row ahead, and while a row's last slice is staged
+// and copied they load the next row's description, its cached bitmap words and
+// its entry-cache entries, so a row starts without a round trip to memory.
+// When `cache` is not null, a row with slot >= 0 takes its column bitmap from
+// that row of the structure cache (written by the symbolic phase for the same
+// A and B) instead of running the structure pass.
 // POOL selects the output: CSR at C.row_ptr, or pool segments claimed through
 // the sink (compiled apart, so the CSR kernel carries none of the pool state).
 template <typename V, bool POOL>
 __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
-    Mats<V> M, const int32_t *__restrict__ rows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
+    Mats<V> M, const RankRow *__restrict__ rr, int nrows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
     RowSink out, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
-    const int32_t *__restrict__ slot_of_row, const uint32_t *__restrict__ cache, int64_t row_words) {
+    const uint32_t *__restrict__ cache, int64_t row_words) {
     using SH = RankShape<V>;
     constexpr int BLOCK = SH::BLOCK;
     constexpr int NW = BLOCK / kWave;
@@ -773,6 +813,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
     __shared__ int32_t sclaim;   // staging's group counter
+    __shared__ int32_t s_next;   // the claimed next row
     __shared__ int64_t s_claim[2];   // pool output: the row's first entry and writable length
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries], e_hi[kCacheEntries];
     __shared__ double e_av[kCacheEntries];
@@ -782,239 +823,331 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         if (threadIdx.x == 0) atomicOr(&ctrl->error_flags, kErrPoolLayout);
         return;
     }
-    const int row = rows[blockIdx.x];
-    const int a_lo = M.a_rp[row], a_hi = M.a_rp[row + 1];
-    // CSR output: the row's place from C.row_ptr. Pool output: claimed once the region's entry count is
-    // known
-    int64_t cb = 0, seg = 0;
-    if (!POOL) {
-        cb = out.c_rp[row];
-        seg = out.c_rp[row + 1] - cb;
-    }
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
-    EntryCache ecache{e_col, e_bs, e_len, e_av, false};
-    const int slot = slot_of_row != nullptr ? uniform(slot_of_row[row]) : -1;
-    const uint32_t *cached = slot >= 0 ? cache + static_cast<int64_t>(slot) * row_words : nullptr;
+    const int rg1_first = nwin < SH::REGION_WINS ? nwin : SH::REGION_WINS;   // end of the first region
     int32_t *mark = marks + wv * kMarkIntsLong;
     init_marks(mark, kMarkIntsLong);
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
-    if (threadIdx.x == 0) sclaim = 0;
+    if (threadIdx.x == 0) {
+        sclaim = 0;
+        s_next = atomicAdd(&ctrl->rank_next, 1);
+    }
+    __syncthreads();
+    const int idx = uniform(s_next);
+    if (idx >= nrows) return;   // the whole workgroup
 
-    int64_t done = 0;   // entries of the row emitted in earlier regions
-    for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
-        const int rg1 = nwin - rg0 < SH::REGION_WINS ? nwin : rg0 + SH::REGION_WINS;
-        const int64_t col0 = static_cast<int64_t>(rg0) * kRankWinCols;
-        const int ncw = static_cast<int>(ncols - col0 < SH::REGION_COLS ? ncols - col0 : SH::REGION_COLS);
-        const int nwords = (ncw + 31) >> 5;
-        // 1. structure: the cached bitmap, or a structure pass (a region covering every column takes whole B
-        //    rows, whose bounds come from B's row pointers rather than the larger window table). Either way the
-        //    entry cache ends up holding each cached entry's column, value and part of B in the region.
-        // Wave w owns words [w*RW/NW, (w+1)*RW/NW) in the prefix scan below, read one 64-word row at a time.
-        const int wbase = wv * (RW / NW);
-        uint32_t bits[WROWS];
-        if (cached != nullptr) {
-            // the entries first (their loads then overlap the bitmap's), then the words this wave scans, all
-            // loaded before any is used
-            int k = 0, lo = 0, hi = 0;
-            double av = 0.0;
-            const int ci = static_cast<int>(threadIdx.x);
-            const bool has_entry = ci < kCacheEntries && a_lo + ci < a_hi;
-            if (has_entry) {
-                k = ecache.col_ready ? e_col[ci] : M.a_col[a_lo + ci];
-                if (!ecache.vals_ready) av = to_d(M.a_val[a_lo + ci]);
-            }
-            const uint32_t *src = cached + static_cast<int64_t>(rg0) * WIN_WORDS;
-#pragma unroll
-            for (int q = 0; q < WROWS; ++q) {
-                const int i = wbase + q * kWave + ln;
-                bits[q] = i < nwords ? __builtin_nontemporal_load(&src[i]) : 0u;
-            }
-            if (has_entry) {
-                const int32_t *t = wtab + static_cast<int64_t>(k) * stride;
-                lo = t[rg0];
-                hi = t[rg1];
-            }
-            if (ci < kCacheEntries) {
-                if (!ecache.col_ready) e_col[ci] = k;
-                if (!ecache.vals_ready) e_av[ci] = av;
-                e_bs[ci] = lo;
-                e_len[ci] = hi - lo;
-                e_hi[ci] = hi;
-            }
-            ecache.col_ready = true;
-            ecache.vals_ready = true;
-        } else {
-            for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
-            __syncthreads();
-            auto mark_col = [&](int col, double) {
-                const int rel = static_cast<int>(col - col0);
-                atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
-            };
-            if (nwin <= SH::REGION_WINS)
-                for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi, BRowRange{M.b_rp}, M.b_col,
-                                                           M.b_val, mark, ctot, mark_col, ecache);
-            else
-                for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi,
-                                                           BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val,
-                                                           mark, ctot, mark_col, ecache);
-            ecache.col_ready = true;
-            // the pass left each cached entry's region part in e_bs / e_len (written by this same thread)
-            if (threadIdx.x < kCacheEntries) e_hi[threadIdx.x] = e_bs[threadIdx.x] + e_len[threadIdx.x];
-#pragma unroll
-            for (int q = 0; q < WROWS; ++q) bits[q] = bw[wbase + q * kWave + ln].x;
+    // The first region of a cached row, as the row start consumes it: the words this thread scans (wave w owns
+    // words [w*RW/NW, (w+1)*RW/NW), one 64-word row at a time) and, for cache entry ci = threadIdx.x, the
+    // entry's column, value and part of B in the region. Loaded for the first row here, for later rows while
+    // the row before them finishes.
+    const int wbase = wv * (RW / NW);
+    const int ci = static_cast<int>(threadIdx.x);
+    uint32_t bits[WROWS];
+    int pk = 0, plo = 0, phi = 0;
+    double pav = 0.0;
+    auto fetch_words = [&](int a_lo, int a_hi, int slot) {
+        const uint32_t *src = cache + static_cast<int64_t>(slot) * row_words;
+        const int nw0 = static_cast<int>((ncols < SH::REGION_COLS ? ncols : SH::REGION_COLS) + 31) >> 5;
+        pk = 0;
+        pav = 0.0;
+        if (ci < kCacheEntries && a_lo + ci < a_hi) {
+            pk = M.a_col[a_lo + ci];
+            pav = to_d(M.a_val[a_lo + ci]);
         }
-        // 2. exclusive popcount prefix (lane-contiguous rows, so free of bank conflicts); each word is stored
-        //    with its prefix
-        {
-            uint32_t cnt[WROWS];
-            int wtot = 0;
 #pragma unroll
-            for (int q = 0; q < WROWS; ++q) {
-                cnt[q] = __popc(bits[q]);
-                wtot += static_cast<int>(cnt[q]);
-            }
-            wtot = __builtin_amdgcn_readlane(wave_incl_sum(wtot), kWave - 1);
-            if (ln == 0) scratch[wv] = wtot;
-            __syncthreads();
-            int run = 0;
-#pragma unroll
-            for (int i = 0; i < NW; ++i) run += i < wv ? scratch[i] : 0;
-#pragma unroll
-            for (int q = 0; q < WROWS; ++q) {
-                const int inc = wave_incl_sum(static_cast<int>(cnt[q]));
-                bw[wbase + q * kWave + ln] = make_uint2(bits[q], static_cast<uint32_t>(run + inc - static_cast<int>(cnt[q])));
-                run += __builtin_amdgcn_readlane(inc, kWave - 1);
-            }
+        for (int q = 0; q < WROWS; ++q) {
+            const int i = wbase + q * kWave + ln;
+            bits[q] = i < nw0 ? __builtin_nontemporal_load(&src[i]) : 0u;
         }
-        int region_total = 0;
-#pragma unroll
-        for (int i = 0; i < NW; ++i) region_total += scratch[i];
-        region_total = uniform(region_total);
-        if (POOL && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
-        __syncthreads();
-        if (POOL) {
-            cb = uniform(s_claim[0]);
-            seg = uniform(s_claim[1]);
+    };
+    auto fetch_bounds = [&](int a_lo, int a_hi) {
+        plo = 0;
+        phi = 0;
+        if (ci < kCacheEntries && a_lo + ci < a_hi) {
+            const int32_t *t = wtab + static_cast<int64_t>(pk) * stride;
+            plo = t[0];
+            phi = t[rg1_first];
         }
-        // 3. rank slices: whole windows while they fit CAP entries; a window
-        //    denser than CAP is taken in slices of CAP ranks. Lane jw holds the
-        //    first rank of window jw (one LDS read for all windows), and the
-        //    greedy grouping reads them with scalar lane reads.
-        const int nwr = rg1 - rg0;
-        const int win_rank = ln <= nwr && ln * WIN_WORDS < nwords ? static_cast<int>(bw[ln * WIN_WORDS].y)
-                                                                   : region_total;
-        auto rank_at_window = [&](int jw) -> int { return __builtin_amdgcn_readlane(win_rank, jw); };
-        int j = 0;
-        int r0 = 0;          // first rank of the current slice
-        int pj = 0, pj2 = nwr;   // windows of the slices the entry cache holds (first: the whole region)
-        while (j < nwr) {
-            int j2 = j + 1;
-            while (j2 < nwr && rank_at_window(j2 + 1) - r0 <= CAP) ++j2;
-            const int rend_w = rank_at_window(j2);
-            const int r1 = rend_w - r0 > CAP ? r0 + CAP : rend_w;    // this slice covers ranks [r0, r1)
-            // values
-            const int lo_from = j == pj ? 0 : j == pj2 ? 1 : 2;
-            const int hi_from = j2 == pj2 ? 0 : j2 == nwr ? 1 : 2;
-            for_each_product_wg<BLOCK, V, true, true>(
-                M.a_col, M.a_val, a_lo, a_hi,
-                SliceRange{wtab, stride, rg0 + j, rg0 + j2, lo_from, hi_from, e_bs, e_len, e_hi}, M.b_col, M.b_val,
-                mark, ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1}, ecache);
-            ecache.vals_ready = true;
-            pj = j;
-            pj2 = j2;
-            if constexpr (SH::PACKED) {
-                // float output: round each accumulator once and keep the float in the high half of its own
-                // 8-byte slot, so the staging below only writes (it never waits on an accumulator read)
-                for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
-                    const float v = static_cast<float>(acc[i]);
-                    reinterpret_cast<uint2 *>(acc)[i].y = __float_as_uint(v);
+    };
+    int row = uniform(rr[idx].row), a_lo = uniform(rr[idx].a_lo), a_hi = uniform(rr[idx].a_hi);
+    int slot = cache != nullptr ? uniform(rr[idx].slot) : -1;
+    int64_t row_cb = POOL ? 0 : uniform(rr[idx].cb), row_seg = POOL ? 0 : uniform(rr[idx].seg);
+    if (slot >= 0) {
+        fetch_words(a_lo, a_hi, slot);
+        fetch_bounds(a_lo, a_hi);
+    }
+    int claimed = 0;   // thread 0: the row after the next one
+    while (true) {
+        if (threadIdx.x == 0) claimed = atomicAdd(&ctrl->rank_next, 1);
+        // CSR output: the row's place from C.row_ptr. Pool output: claimed once the region's entry count is
+        // known
+        int64_t cb = row_cb, seg = row_seg;
+        EntryCache ecache{e_col, e_bs, e_len, e_av, false};
+        const uint32_t *cached = slot >= 0 ? cache + static_cast<int64_t>(slot) * row_words : nullptr;
+        int nidx = nrows;
+        bool fetched = false;   // the next row's description is in row .. row_seg
+        int4 n_lo = make_int4(0, 0, 0, -1);   // the next row's description, in flight until the last slice
+        longlong2 n_hi = make_longlong2(0, 0);
+        // the current row is done with its description: the next row's replaces it
+        auto take_next = [&]() {
+            row = uniform(n_lo.x);
+            a_lo = uniform(n_lo.y);
+            a_hi = uniform(n_lo.z);
+            slot = cache != nullptr ? uniform(n_lo.w) : -1;
+            row_cb = POOL ? 0 : uniform(static_cast<int64_t>(n_hi.x));
+            row_seg = POOL ? 0 : uniform(static_cast<int64_t>(n_hi.y));
+        };
+
+        int64_t done = 0;   // entries of the row emitted in earlier regions
+        for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
+            const int rg1 = nwin - rg0 < SH::REGION_WINS ? nwin : rg0 + SH::REGION_WINS;
+            const int64_t col0 = static_cast<int64_t>(rg0) * kRankWinCols;
+            const int ncw = static_cast<int>(ncols - col0 < SH::REGION_COLS ? ncols - col0 : SH::REGION_COLS);
+            const int nwords = (ncw + 31) >> 5;
+            // 1. structure: the cached bitmap, or a structure pass (a region covering every column takes whole
+            //    B rows, whose bounds come from B's row pointers rather than the larger window table). Either
+            //    way the entry cache ends up holding each cached entry's column, value and part of B in the
+            //    region.
+            if (cached != nullptr) {
+                int k = 0, lo = 0, hi = 0;
+                double av = 0.0;
+                const bool has_entry = ci < kCacheEntries && a_lo + ci < a_hi;
+                if (rg0 == 0) {
+                    // prefetched
+                    k = pk;
+                    av = pav;
+                    lo = plo;
+                    hi = phi;
+                } else {
+                    // later regions: the entries first (their loads then overlap the bitmap's), then the words
+                    // this wave scans, all loaded before any is used
+                    if (has_entry) k = e_col[ci];
+                    const uint32_t *src = cached + static_cast<int64_t>(rg0) * WIN_WORDS;
+#pragma unroll
+                    for (int q = 0; q < WROWS; ++q) {
+                        const int i = wbase + q * kWave + ln;
+                        bits[q] = i < nwords ? __builtin_nontemporal_load(&src[i]) : 0u;
+                    }
+                    if (has_entry) {
+                        const int32_t *t = wtab + static_cast<int64_t>(k) * stride;
+                        lo = t[rg0];
+                        hi = t[rg1];
+                    }
                 }
+                if (ci < kCacheEntries) {
+                    if (rg0 == 0) {
+                        e_col[ci] = k;
+                        e_av[ci] = av;
+                    }
+                    e_bs[ci] = lo;
+                    e_len[ci] = hi - lo;
+                    e_hi[ci] = hi;
+                }
+                ecache.col_ready = true;
+                ecache.vals_ready = true;
+            } else {
+                for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
                 __syncthreads();
+                auto mark_col = [&](int col, double) {
+                    const int rel = static_cast<int>(col - col0);
+                    atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
+                };
+                if (nwin <= SH::REGION_WINS)
+                    for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi,
+                                                                     BRowRange{M.b_rp}, M.b_col, M.b_val, mark,
+                                                                     ctot, mark_col, ecache);
+                else
+                    for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi,
+                                                                     BWindowRange{wtab, stride, rg0, rg1}, M.b_col,
+                                                                     M.b_val, mark, ctot, mark_col, ecache);
+                ecache.col_ready = true;
+                // the pass left each cached entry's region part in e_bs / e_len (written by this same thread)
+                if (threadIdx.x < kCacheEntries) e_hi[threadIdx.x] = e_bs[threadIdx.x] + e_len[threadIdx.x];
+#pragma unroll
+                for (int q = 0; q < WROWS; ++q) bits[q] = bw[wbase + q * kWave + ln].x;
             }
-            // stage ranks [r0, r1) in rank order, one bitmap word per lane: the waves claim the windows' words
-            // in 64-word groups from an LDS counter, so the waves holding dense groups (many entries per word)
-            // take fewer of them and all finish together. A word's entries hold consecutive ranks; a lane
-            // stages them kStageStep per step (the wave loops while any lane has entries left), so the cost
-            // follows the entries, not the columns. Every rank is staged by exactly one lane.
-            const int wa = j * WIN_WORDS;
-            const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
-            int gnext = 0;
-            if (ln == 0) gnext = atomicAdd(&sclaim, 1);
-            gnext = uniform(gnext);
-            while (true) {
-                const int g = gnext;
-                if (wa + g * kWave >= wb) break;
-                const int wd = wa + g * kWave + ln;
-                const uint2 e = wd < wb ? bw[wd] : make_uint2(0u, 0u);
-                // the next claim is in flight while this group is staged
+            // 2. exclusive popcount prefix (lane-contiguous rows, so free of bank conflicts); each word is
+            //    stored with its prefix
+            {
+                uint32_t cnt[WROWS];
+                int wtot = 0;
+#pragma unroll
+                for (int q = 0; q < WROWS; ++q) {
+                    cnt[q] = __popc(bits[q]);
+                    wtot += static_cast<int>(cnt[q]);
+                }
+                wtot = __builtin_amdgcn_readlane(wave_incl_sum(wtot), kWave - 1);
+                if (ln == 0) scratch[wv] = wtot;
+                if (threadIdx.x == 0 && rg0 == 0) s_next = claimed;
+                __syncthreads();
+                int run = 0;
+#pragma unroll
+                for (int i = 0; i < NW; ++i) run += i < wv ? scratch[i] : 0;
+#pragma unroll
+                for (int q = 0; q < WROWS; ++q) {
+                    const int inc = wave_incl_sum(static_cast<int>(cnt[q]));
+                    bw[wbase + q * kWave + ln] =
+                        make_uint2(bits[q], static_cast<uint32_t>(run + inc - static_cast<int>(cnt[q])));
+                    run += __builtin_amdgcn_readlane(inc, kWave - 1);
+                }
+            }
+            if (rg0 == 0) {
+                // the next row's description: in flight through this row's value passes
+                nidx = uniform(s_next);
+                if (nidx < nrows) {
+                    const int z = opaque_zero();
+                    const int4 *d = reinterpret_cast<const int4 *>(rr + nidx) + z;
+                    n_lo = d[0];
+                    n_hi = reinterpret_cast<const longlong2 *>(d)[1];
+                }
+            }
+            int region_total = 0;
+#pragma unroll
+            for (int i = 0; i < NW; ++i) region_total += scratch[i];
+            region_total = uniform(region_total);
+            if (POOL && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
+            __syncthreads();
+            if (POOL) {
+                cb = uniform(s_claim[0]);
+                seg = uniform(s_claim[1]);
+            }
+            // 3. rank slices: whole windows while they fit CAP entries; a window denser than CAP is taken in
+            //    slices of CAP ranks. Lane jw holds the first rank of window jw (one LDS read for all windows),
+            //    and the greedy grouping reads them with scalar lane reads.
+            const int nwr = rg1 - rg0;
+            const int win_rank = ln <= nwr && ln * WIN_WORDS < nwords ? static_cast<int>(bw[ln * WIN_WORDS].y)
+                                                                       : region_total;
+            auto rank_at_window = [&](int jw) -> int { return __builtin_amdgcn_readlane(win_rank, jw); };
+            int j = 0;
+            int r0 = 0;              // first rank of the current slice
+            int pj = 0, pj2 = nwr;   // windows of the slices the entry cache holds (first: the whole region)
+            while (j < nwr) {
+                int j2 = j + 1;
+                while (j2 < nwr && rank_at_window(j2 + 1) - r0 <= CAP) ++j2;
+                const int rend_w = rank_at_window(j2);
+                const int r1 = rend_w - r0 > CAP ? r0 + CAP : rend_w;   // this slice covers ranks [r0, r1)
+                // the row's last slice: the next row's loads go out while it is staged and copied
+                const bool prefetch = rg1 == nwin && j2 == nwr && r1 == rend_w && nidx < nrows;
+                // values
+                const int lo_from = j == pj ? 0 : j == pj2 ? 1 : 2;
+                const int hi_from = j2 == pj2 ? 0 : j2 == nwr ? 1 : 2;
+                for_each_product_wg<BLOCK, V, true, true>(
+                    M.a_col, M.a_val, a_lo, a_hi,
+                    SliceRange{wtab, stride, rg0 + j, rg0 + j2, lo_from, hi_from, e_bs, e_len, e_hi}, M.b_col,
+                    M.b_val, mark, ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1}, ecache);
+                ecache.vals_ready = true;
+                pj = j;
+                pj2 = j2;
+                if (prefetch) {
+                    take_next();
+                    fetched = true;
+                    if (slot >= 0) fetch_words(a_lo, a_hi, slot);
+                }
+                if constexpr (SH::PACKED) {
+                    // float output: round each accumulator once and keep the float in the high half of its own
+                    // 8-byte slot, so the staging below only writes (it never waits on an accumulator read)
+                    for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
+                        const float v = static_cast<float>(acc[i]);
+                        reinterpret_cast<uint2 *>(acc)[i].y = __float_as_uint(v);
+                    }
+                    __syncthreads();
+                }
+                // stage ranks [r0, r1) in rank order, one bitmap word per lane: the waves claim the windows'
+                // words in 64-word groups from an LDS counter, so the waves holding dense groups (many entries
+                // per word) take fewer of them and all finish together. A word's entries hold consecutive ranks;
+                // a lane stages them kStageStep per step (the wave loops while any lane has entries left), so
+                // the cost follows the entries, not the columns. Every rank is staged by exactly one lane.
+                const int wa = j * WIN_WORDS;
+                const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
+                int gnext = 0;
                 if (ln == 0) gnext = atomicAdd(&sclaim, 1);
                 gnext = uniform(gnext);
-                uint32_t wbits = e.x;
-                int r = static_cast<int>(e.y);
-                // drop the entries below r0
-                while (wbits != 0u && r < r0) {
-                    wbits &= wbits - 1u;
-                    ++r;
-                }
-                int n = __popc(wbits);
-                if (r + n > r1) n = r1 - r;
-                if (n < 0) n = 0;
-                const int k0 = r - r0;   // this lane's first slot
-                const int cbase = static_cast<int>(col0) + wd * 32;
-                for (int i = 0; ballot(i < n) != 0ull; i += kStageStep) {
-                    if (i < n) {
-                        int cv[kStageStep];
-#pragma unroll
-                        for (int q = 0; q < kStageStep; ++q) {
-                            cv[q] = cbase + __builtin_ctz(wbits | 0x80000000u);
-                            wbits &= wbits - 1u;
-                        }
-                        if constexpr (SH::PACKED) {
-                            // the column goes into the low half of the slot, beside the float value
+                while (true) {
+                    const int g = gnext;
+                    if (wa + g * kWave >= wb) break;
+                    const int wd = wa + g * kWave + ln;
+                    const uint2 e = wd < wb ? bw[wd] : make_uint2(0u, 0u);
+                    // the next claim is in flight while this group is staged
+                    if (ln == 0) gnext = atomicAdd(&sclaim, 1);
+                    gnext = uniform(gnext);
+                    uint32_t wbits = e.x;
+                    int r = static_cast<int>(e.y);
+                    // drop the entries below r0
+                    while (wbits != 0u && r < r0) {
+                        wbits &= wbits - 1u;
+                        ++r;
+                    }
+                    int n = __popc(wbits);
+                    if (r + n > r1) n = r1 - r;
+                    if (n < 0) n = 0;
+                    const int k0 = r - r0;   // this lane's first slot
+                    const int cbase = static_cast<int>(col0) + wd * 32;
+                    for (int i = 0; ballot(i < n) != 0ull; i += kStageStep) {
+                        if (i < n) {
+                            int cv[kStageStep];
 #pragma unroll
                             for (int q = 0; q < kStageStep; ++q) {
-                                if (i + q < n) reinterpret_cast<uint2 *>(acc)[k0 + i + q].x = static_cast<uint32_t>(cv[q]);
+                                cv[q] = cbase + __builtin_ctz(wbits | 0x80000000u);
+                                wbits &= wbits - 1u;
                             }
-                        } else {
+                            if constexpr (SH::PACKED) {
+                                // the column goes into the low half of the slot, beside the float value
 #pragma unroll
-                            for (int q = 0; q < kStageStep; ++q) {
-                                if (i + q < n) stage[k0 + i + q] = cv[q];
+                                for (int q = 0; q < kStageStep; ++q) {
+                                    if (i + q < n)
+                                        reinterpret_cast<uint2 *>(acc)[k0 + i + q].x = static_cast<uint32_t>(cv[q]);
+                                }
+                            } else {
+#pragma unroll
+                                for (int q = 0; q < kStageStep; ++q) {
+                                    if (i + q < n) stage[k0 + i + q] = cv[q];
+                                }
                             }
                         }
                     }
                 }
-            }
-            __syncthreads();
-            // copy the slice to C with coalesced stores, clearing the accumulator
-            const int64_t pbase = done + r0;
-            for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
-                int32_t colv;
-                V v;
-                if constexpr (SH::PACKED) {
-                    const uint2 e = reinterpret_cast<const uint2 *>(acc)[i];
-                    colv = static_cast<int32_t>(e.x);
-                    v = static_cast<V>(__uint_as_float(e.y));
-                } else {
-                    colv = stage[i];
-                    v = static_cast<V>(acc[i]);
+                __syncthreads();
+                if (prefetch && slot >= 0) fetch_bounds(a_lo, a_hi);
+                // copy the slice to C with coalesced stores, clearing the accumulator
+                const int64_t pbase = done + r0;
+                for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
+                    int32_t colv;
+                    V v;
+                    if constexpr (SH::PACKED) {
+                        const uint2 e = reinterpret_cast<const uint2 *>(acc)[i];
+                        colv = static_cast<int32_t>(e.x);
+                        v = static_cast<V>(__uint_as_float(e.y));
+                    } else {
+                        colv = stage[i];
+                        v = static_cast<V>(acc[i]);
+                    }
+                    acc[i] = 0.0;
+                    if (pbase + i < seg) {
+                        // streaming stores: C is written once, and must not push B out of the L2
+                        __builtin_nontemporal_store(colv, &c_col[cb + pbase + i]);
+                        __builtin_nontemporal_store(v, &c_val[cb + pbase + i]);
+                    }
                 }
-                acc[i] = 0.0;
-                if (pbase + i < seg) {
-                    // streaming stores: C is written once, and must not push B out of the L2
-                    __builtin_nontemporal_store(colv, &c_col[cb + pbase + i]);
-                    __builtin_nontemporal_store(v, &c_val[cb + pbase + i]);
-                }
+                if (threadIdx.x == 0) sclaim = 0;   // every wave has left the staging loop
+                __syncthreads();
+                r0 = r1;
+                if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
             }
-            if (threadIdx.x == 0) sclaim = 0;   // every wave has left the staging loop
-            __syncthreads();
-            r0 = r1;
-            if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
+            done += region_total;
         }
-        done += region_total;
+        if (threadIdx.x == 0 && !POOL && done != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+        if (nidx >= nrows) break;
+        if (!fetched) {
+            // the last slice always prefetches; this keeps the loop right should it not
+            take_next();
+            if (slot >= 0) {
+                fetch_words(a_lo, a_hi, slot);
+                fetch_bounds(a_lo, a_hi);
+            }
+        }
     }
-    if (threadIdx.x == 0 && !POOL && done != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
 }
 
 // ---------------------------------------------------------------------------

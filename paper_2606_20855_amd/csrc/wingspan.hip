@@ -164,7 +164,7 @@ wingspan_status check_pair(const wingspan_csr *A, const wingspan_csr *B) {
 
 // Workspace layout, a pure function of the sizes and options.
 struct Layout {
-    size_t off_stamp, off_ctrl, off_pref, off_row_nnz, off_perm, off_partials, off_wtab, off_pool, total;
+    size_t off_stamp, off_ctrl, off_pref, off_row_nnz, off_perm, off_rrows, off_partials, off_wtab, off_pool, total;
     size_t off_slot, off_cache;   // structure cache (cache_rows == 0: none)
     int64_t row_words, cache_rows;
     int nwin;          // numeric dense windows per row (0: dense numeric tier unavailable)
@@ -188,6 +188,8 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
     off += align_up(sizeof(int32_t) * std::max<int64_t>(m, 1));
     L.off_perm = off;
     off += align_up(sizeof(int32_t) * std::max<int64_t>(m, 1));
+    L.off_rrows = off;
+    off += align_up(sizeof(RankRow) * std::max<int64_t>(m, 1));
     L.off_partials = off;
     const int64_t tiles = (std::max<int64_t>(nnz_a, m + 1) + kScanTile - 1) / kScanTile + 2;
     off += align_up(sizeof(int64_t) * tiles);
@@ -237,6 +239,7 @@ struct Ctx {
     int64_t *pref;
     int32_t *row_nnz;
     int32_t *perm;
+    RankRow *rrows;
     int64_t *partials;
     int32_t *wtab;
     char *pool;
@@ -253,6 +256,7 @@ void carve(Ctx &c, void *ws) {
     c.pref = reinterpret_cast<int64_t *>(c.ws + c.L.off_pref);
     c.row_nnz = reinterpret_cast<int32_t *>(c.ws + c.L.off_row_nnz);
     c.perm = reinterpret_cast<int32_t *>(c.ws + c.L.off_perm);
+    c.rrows = reinterpret_cast<RankRow *>(c.ws + c.L.off_rrows);
     c.partials = reinterpret_cast<int64_t *>(c.ws + c.L.off_partials);
     c.wtab = reinterpret_cast<int32_t *>(c.ws + c.L.off_wtab);
     c.pool = c.ws + c.L.off_pool;
@@ -453,6 +457,21 @@ void fill_stats(const Ctx &c, int phase) {
         st.c_nnz[t] += c.host.stat_cnnz[b];
     }
     st.total_products = c.host.total_products;
+}
+
+// Workgroups of the persistent rank kernel: one per compute unit of the
+// current device (its LDS use allows no second), or fewer when there are fewer
+// rows.
+unsigned rank_grid(int32_t rows) {
+    static int cus[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+    if (cus[dev] <= 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return static_cast<unsigned>(std::min<int32_t>(rows, cus[dev]));
 }
 
 // Contiguous range of perm covering bins [b0, b0+nb).
@@ -686,9 +705,12 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt && c.L.rank_mode) {
         const bool cached = stamp_matches(c, A, B);
         stats.structure_cache_rows = cached ? c.host_stamp.cached_rows : 0;
-        dense_rank_kernel<V, false><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
-            M, perm + start, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl,
-            cached ? c.slot_of_row : nullptr, cached ? c.cache : nullptr, c.L.row_words);
+        rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, c_rp,
+                                                            cached ? c.slot_of_row : nullptr, c.rrows);
+        LAUNCH_CHECK("rank rows");
+        dense_rank_kernel<V, false><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+            M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl, cached ? c.cache : nullptr,
+            c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense rank numeric");
     } else if (cnt) {
@@ -783,9 +805,11 @@ wingspan_status sharded_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt) {
         // binning sends dense rows here only in rank mode with one region; the column bitmaps come from the
         // kernel's own structure pass
-        dense_rank_kernel<V, true><<<static_cast<unsigned>(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
-            M, perm + start, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr, nullptr,
-            c.L.row_words);
+        rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, nullptr, nullptr,
+                                                            c.rrows);
+        LAUNCH_CHECK("rank rows");
+        dense_rank_kernel<V, true><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+            M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr, c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense rank single pass");
     }
