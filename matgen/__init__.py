@@ -18,6 +18,8 @@ from .generators import (
     diagonal,
     random_sparse,
     shuffled_copy,
+    sparse_vector,
+    transpose,
 )
 
 __all__ = [
@@ -34,4 +36,6 @@ __all__ = [
     "diagonal",
     "random_sparse",
     "shuffled_copy",
+    "sparse_vector",
+    "transpose",
 ]

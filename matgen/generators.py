@@ -165,6 +165,25 @@ def shuffled_copy(M: CSR, seed) -> CSR:
     return CSR(M.nrows, M.ncols, rp, ci, M.val[order].copy())
 
 
+def transpose(M: CSR) -> CSR:
+    """The CSR arrays of M's transpose (equivalently, M in compressed
+    columns): the same entries, grouped by column, rows ascending."""
+    rows = np.repeat(np.arange(M.nrows, dtype=np.int64), np.diff(M.row_ptr))
+    keys = M.col_idx.astype(np.int64) * max(M.nrows, 1) + rows
+    order = np.argsort(keys)   # distinct keys
+    rp, ci = _csr_from_sorted_keys(keys[order], M.ncols, M.nrows)
+    return CSR(M.ncols, M.nrows, rp, ci, M.val[order].copy())
+
+
+def sparse_vector(n: int, density: float, seed, dtype=np.float64, dist: str = "pm1"):
+    """A seeded sparse vector of length n: round(density * n) distinct
+    indices drawn uniformly (returned sorted, int32) and their values."""
+    rng = _rng(seed)
+    k = int(round(density * n))
+    idx = np.sort(rng.choice(n, size=k, replace=False)).astype(np.int32) if k > 0 else np.zeros(0, np.int32)
+    return idx, _values(rng, k, dist, dtype)
+
+
 def identity(n: int, dtype=np.float64) -> CSR:
     return CSR(n, n, np.arange(n + 1, dtype=np.int32), np.arange(n, dtype=np.int32),
                np.ones(n, dtype=dtype))
