@@ -14,6 +14,7 @@ input, writing into a preallocated C. Prints one JSON line:
   sharded_single_pass  the single pass with sharded output on the same workload
   elementwise    SpAdd and the Hadamard product (B = A, and B a shuffled copy)
                  on the R-MAT scale-20 matrix, against HBM bandwidth
+  spmspv         y = A x on the same matrix with x 10% stored
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rmat18]
        python bench.py --elementwise-only [--ew-workload rmat20]
@@ -162,13 +163,12 @@ def ew_alg_bytes(m, na, nb, nc, s, op):
     return 2 * 4 * (m + 1) + 4 * (na + nb) + vals + 8 * (m + 1) + (4 + s) * nc
 
 
-def elementwise_pass(ws, torch, workload, dev, steps, warmup, seed):
+def elementwise_pass(ws, torch, A, workload, dev, steps, warmup, seed):
     """SpAdd and the Hadamard product on a workload's A, in the identity case
     (B = A) and the shuffled case (B = A with rows and columns relabelled by
     seeded permutations). Each op is timed whole (structure with its count
     read back, then values) and values alone, with HIP events on its stream."""
     import matgen
-    A = matgen.config(workload)[0]
     dA = ws.DeviceCSR.from_host(A, dev)
     h = torch.cuda.current_stream().cuda_stream
     s = A.val.dtype.itemsize
@@ -209,6 +209,54 @@ def elementwise_pass(ws, torch, workload, dev, steps, warmup, seed):
     return dict(workload=f"{workload} A: m={A.nrows}, nnz={A.nnz}, {A.val.dtype}", **out)
 
 
+def sv_alg_bytes(nx, P, ny, s):
+    """Least HBM bytes of y = A x with A in compressed columns: x's entries,
+    the column-pointer pair of each, the selected columns' entries, and y's
+    entries written once."""
+    return (4 + s) * nx + 8 * nx + (4 + s) * P + (4 + s) * ny
+
+
+def spmspv_pass(ws, torch, A, workload, dev, steps, warmup, seed, density=0.1):
+    """y = A x on a workload's A (given by its columns) for a seeded x with
+    `density` of its entries stored (the paper's x is 90% sparse). The whole
+    call is timed with HIP events on its stream (clearing the map, the
+    product count read back, scatter, coalescing, y's count read back)."""
+    import matgen
+    At = matgen.transpose(A)
+    dAt = ws.DeviceCSR.from_host(At, dev)
+    xi, xv = matgen.sparse_vector(A.ncols, density, seed, A.val.dtype)
+    x_idx = torch.from_numpy(xi).to(dev)
+    x_val = torch.from_numpy(xv).to(dev)
+    h = torch.cuda.current_stream().cuda_stream
+    Atd = dAt.desc()
+    nbytes = ws.wingspan_spmspv_workspace_size(Atd, len(xi))
+    wsb = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    m = A.nrows
+    y_idx = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+    y_val = torch.empty(max(m, 1), dtype=dAt.val.dtype, device=dev)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def run():
+        e[0].record()
+        _, n = ws.wingspan_spmspv(Atd, dAt.dtype_code, x_idx.data_ptr(), x_val.data_ptr(), len(xi), y_idx.data_ptr(),
+                                  y_val.data_ptr(), m, wsb.data_ptr(), nbytes, h)
+        e[1].record()
+        e[1].synchronize()
+        return e[0].elapsed_time(e[1]), n
+
+    for _ in range(warmup):
+        run()
+    res = [run() for _ in range(max(steps, 5))]
+    t = float(np.mean([r[0] for r in res]))
+    ny = res[-1][1]
+    colen = np.diff(At.row_ptr.astype(np.int64))
+    P = int(colen[xi].sum())
+    b = sv_alg_bytes(len(xi), P, ny, A.val.dtype.itemsize)
+    return dict(workload=f"{workload} A: m={A.nrows}, nnz={A.nnz}, {A.val.dtype}; x {density:.0%} stored",
+                nnz_x=len(xi), products=P, nnz_y=ny, ms=round(t, 4), ms_min=round(min(r[0] for r in res), 4),
+                alg_bytes=b, GBps=round(b / (t / 1e3) / 1e9, 1), frac=round(b / (t / 1e3) / 1e9 / HBM_PEAK_GBPS, 4))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -222,7 +270,8 @@ def main():
     ap.add_argument("--no-elementwise", action="store_true", help="skip the SpAdd / Hadamard timing")
     ap.add_argument("--ew-workload", default="rmat20", help="the matrix A of the SpAdd / Hadamard timing")
     ap.add_argument("--elementwise-only", action="store_true",
-                    help="time only SpAdd / Hadamard and print their JSON object")
+                    help="time only SpAdd / Hadamard and SpMSpV and print their JSON objects")
+    ap.add_argument("--no-spmspv", action="store_true", help="skip the SpMSpV timing")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -247,8 +296,13 @@ def main():
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     if args.elementwise_only:
-        ew = elementwise_pass(ws, torch, args.ew_workload, dev, args.steps, args.warmup, seed=20262)
-        print(json.dumps(dict(elementwise=ew, steps=args.steps, warmup=args.warmup)), flush=True)
+        A2 = matgen.config(args.ew_workload)[0]
+        out = dict(steps=args.steps, warmup=args.warmup)
+        out["elementwise"] = elementwise_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup,
+                                              seed=20262)
+        if not args.no_spmspv:
+            out["spmspv"] = spmspv_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup, seed=20263)
+        print(json.dumps(out), flush=True)
         return
     cfg = matgen.CONFIGS[args.workload]
     t0 = time.time()
@@ -359,9 +413,15 @@ def main():
         sh = sharded_pass(ws, torch, dA, dB, nnz_c, P, args.steps, args.warmup)
         sh["vs_two_phase_step"] = round(ms_per_step / sh["ms"], 3)
         out["sharded_single_pass"] = sh
-    if not args.no_elementwise:
-        log("timing SpAdd and the Hadamard product (identity and shuffled B)")
-        out["elementwise"] = elementwise_pass(ws, torch, args.ew_workload, dev, args.steps, args.warmup, seed=20262)
+    if not (args.no_elementwise and args.no_spmspv):
+        A2 = matgen.config(args.ew_workload)[0]
+        if not args.no_elementwise:
+            log("timing SpAdd and the Hadamard product (identity and shuffled B)")
+            out["elementwise"] = elementwise_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup,
+                                                  seed=20262)
+        if not args.no_spmspv:
+            log("timing SpMSpV (x 10% stored)")
+            out["spmspv"] = spmspv_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup, seed=20263)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a row sample")
         out["cpu_baseline"] = cpu_baseline(A, B, args.cpu_fraction, seed=20261)

@@ -265,6 +265,38 @@ wingspan_status wingspan_elementwise_values(wingspan_ew_op op, const wingspan_cs
                                             int32_t *c_col_idx_dev, void *c_val_dev, void *workspace_dev,
                                             size_t workspace_bytes, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Sparse matrix times sparse vector, y = A x (the paper's sparse linear
+ * algebra evaluation, Section 5.2: SpMSpV, with a sparse x and a bytemap as
+ * the output's root).
+ *
+ * A (m x n) is given by its columns: At is the CSR descriptor of A's
+ * transpose (At->nrows = n, At->ncols = m; row j of At holds column j of A,
+ * rows ascending). x has length n and is given by nnz_x strictly increasing
+ * int32 indices x_idx_dev in [0, n) and their values x_val_dev, of the value
+ * type dtype, which At.val shares. The call reads only the columns of A that
+ * x selects.
+ *
+ * y (length m) is stored at i exactly when column j of A has an entry in row
+ * i for some stored x_j, even where the sum is zero (the pattern is
+ * structural); then y_i = sum over those j of A[i, j] * x_j, accumulated in
+ * double (atomically, so the summation order varies between calls) and
+ * rounded once to dtype. y_idx_dev (int32, strictly increasing) and y_val_dev
+ * receive y's entries; *y_nnz (host) receives their count. If it exceeds y_cap
+ * (y_cap = m always suffices) the call returns
+ * WINGSPAN_ERR_INSUFFICIENT_CAPACITY with *y_nnz valid and only the first
+ * y_cap entries written. x indices out of order or out of range give
+ * WINGSPAN_ERR_INVALID_MATRIX, with y not written. The call synchronizes
+ * `stream` once, to return *y_nnz. The workspace, of the size
+ * wingspan_spmspv_workspace_size gives (pure host code), holds the bytemap.
+ * ------------------------------------------------------------------------ */
+wingspan_status wingspan_spmspv_workspace_size(const wingspan_csr *At, int64_t nnz_x, size_t *bytes);
+
+wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, const int32_t *x_idx_dev,
+                                const void *x_val_dev, int64_t nnz_x, int32_t *y_idx_dev, void *y_val_dev,
+                                int64_t y_cap, int64_t *y_nnz, void *workspace_dev, size_t workspace_bytes,
+                                void *stream);
+
 /* Statistics of the last call on this thread: phase 0 = symbolic, 1 = numeric,
  * 2 = single pass (wingspan_spgemm_sharded). */
 wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out);

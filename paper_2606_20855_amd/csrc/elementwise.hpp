@@ -17,7 +17,7 @@
 
 namespace wsp {
 
-constexpr int kEwChunk = 4096;   // entries per workgroup
+constexpr int kEwChunk = 1024;   // entries per workgroup
 constexpr int kEwRows = 1024;    // rows a chunk stages in LDS
 constexpr int kEwBlock = 256;
 enum EwOp { kEwAdd = 0, kEwMul = 1 };

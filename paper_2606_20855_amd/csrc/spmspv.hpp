@@ -1,0 +1,167 @@
+// Sparse matrix times sparse vector, y = A x (paper, Section 5.2: SpMSpV with
+// a merged bytemap as the output's root). A comes in compressed columns (the
+// CSR arrays of its transpose, At: row j of At is column j of A), so the
+// products of a stored x_j are the entries of one row of At, read with
+// coalesced loads, and only the columns x selects are touched.
+//
+// The output is a bytemap over y's m positions (a stored flag per position
+// and a double accumulator), which every thread updates: the paper guards it
+// with a merge level (a copy per thread, recombined at the end); here the
+// hardware's global double atomics recombine the updates as they happen, and
+// the flags mark the positions written. The map is then coalesced into the
+// sorted sparse y by a scan of the flags.
+//
+// Products are processed flat: product q belongs to the x entry t with
+// pref[t] <= q < pref[t+1] (pref: exclusive prefix of the selected columns'
+// lengths), so long and short columns balance by themselves.
+#pragma once
+
+#include "device_common.hpp"
+
+namespace wsp {
+
+constexpr int kSvChunk = 512;    // products per workgroup
+constexpr int kSvStage = 512;    // x entries a chunk stages in LDS
+constexpr int kSvBlock = 256;
+
+// Length of the column of A that x entry t selects. It also checks x: an
+// index outside [0, n), or not above the one before it, sets
+// kErrInvalidMatrix in *err (and counts 0, so nothing reads past At).
+struct SvLenIn {
+    const int32_t *at_rp, *x_idx;
+    int64_t n;
+    int32_t *err;
+    __device__ __forceinline__ int64_t operator()(int64_t t) const {
+        const int j = x_idx[t];
+        const bool bad = j < 0 || j >= n || (t > 0 && x_idx[t - 1] >= j);
+        if (bad) {
+            atomicOr(err, kErrInvalidMatrix);
+            return 0;
+        }
+        return static_cast<int64_t>(at_rp[j + 1] - at_rp[j]);
+    }
+};
+
+// Clears the map (flags as int32 words, accumulators) and the error word.
+__global__ void __launch_bounds__(256) sv_clear(int32_t *__restrict__ flag_words, int64_t nwords,
+                                                int64_t *__restrict__ yval_bits, int64_t m, int32_t *err) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < nwords) flag_words[i] = 0;
+    if (i < m) yval_bits[i] = 0;
+    if (i == 0) *err = 0;
+}
+
+// 1 where y is stored.
+struct SvFlagIn {
+    const uint8_t *flag;
+    __device__ __forceinline__ int64_t operator()(int64_t i) const { return flag[i] != 0 ? 1 : 0; }
+};
+
+// Last t in [0, nnz_x) with pref[t] <= q; all 64 lanes of one wave take part.
+__device__ __forceinline__ int wave_find_entry(const int64_t *__restrict__ pref, int nnz_x, int64_t q) {
+    int lo = 0, hi = nnz_x - 1;   // pref[lo] <= q holds throughout (pref[0] = 0)
+    while (hi > lo) {
+        const int step = (hi - lo + kWave) / kWave;
+        const int idx = lo + lane_id() * step;
+        const bool le = idx <= hi && pref[idx] <= q;
+        const uint64_t m = ballot(le);
+        lo = lo + (63 - __clzll(m)) * step;
+        const int h = lo + step - 1;
+        hi = h < hi ? h : hi;
+    }
+    return lo;
+}
+
+// Scatters the P = pref[nnz_x] products into the map: yval[i] += A[i, j] * x_j
+// and flag[i] = 1 for each selected entry (i, j). Workgroups take chunks of
+// kSvChunk products, grid-stride, reading P (and the check of x, which stops
+// everything) from device memory, so the host need not wait for them. A
+// chunk's x entries are staged in LDS when they number at most kSvStage: their
+// first product, their column's start in At minus that, and x_j. Values are
+// multiplied and accumulated in double.
+template <typename V>
+__global__ void __launch_bounds__(kSvBlock) sv_scatter(const int32_t *__restrict__ at_rp,
+                                                       const int32_t *__restrict__ at_row,
+                                                       const V *__restrict__ at_val,
+                                                       const int32_t *__restrict__ x_idx,
+                                                       const V *__restrict__ x_val, int nnz_x,
+                                                       const int64_t *__restrict__ pref, const int32_t *err,
+                                                       uint8_t *__restrict__ flag, double *__restrict__ yval) {
+    __shared__ int64_t s_pref[kSvStage + 1];
+    __shared__ int64_t s_base[kSvStage];
+    __shared__ double s_x[kSvStage];
+    __shared__ int s_t[2];
+    if (*err != 0) return;   // whole grid
+    const int64_t P = pref[nnz_x];
+    for (int64_t q0 = static_cast<int64_t>(blockIdx.x) * kSvChunk; q0 < P;
+         q0 += static_cast<int64_t>(gridDim.x) * kSvChunk) {
+        const int64_t q1 = P - q0 < kSvChunk ? P : q0 + kSvChunk;
+        if (threadIdx.x < kWave) {
+            const int t0 = wave_find_entry(pref, nnz_x, q0);
+            const int t1 = wave_find_entry(pref, nnz_x, q1 - 1);
+            if (threadIdx.x == 0) {
+                s_t[0] = t0;
+                s_t[1] = t1;
+            }
+        }
+        __syncthreads();
+        const int t0 = s_t[0];
+        const int nt = s_t[1] - t0 + 1;
+        const bool staged = nt <= kSvStage;
+        if (staged) {
+            for (int k = threadIdx.x; k < nt; k += blockDim.x) {
+                const int t = t0 + k;
+                const int64_t p = pref[t];
+                s_pref[k] = p;
+                s_base[k] = static_cast<int64_t>(at_rp[x_idx[t]]) - p;
+                s_x[k] = to_d(x_val[t]);
+            }
+        }
+        __syncthreads();
+        for (int64_t q = q0 + threadIdx.x; q < q1; q += blockDim.x) {
+            int64_t pos;
+            double xv;
+            if (staged) {
+                int lo = 0, hi = nt - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (s_pref[mid] <= q) lo = mid;
+                    else hi = mid - 1;
+                }
+                pos = s_base[lo] + q;
+                xv = s_x[lo];
+            } else {
+                int lo = t0, hi = t0 + nt - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (pref[mid] <= q) lo = mid;
+                    else hi = mid - 1;
+                }
+                pos = static_cast<int64_t>(at_rp[x_idx[lo]]) + (q - pref[lo]);
+                xv = to_d(x_val[lo]);
+            }
+            const int i = at_row[pos];
+            unsafeAtomicAdd(&yval[i], to_d(at_val[pos]) * xv);
+            flag[i] = 1;
+        }
+        __syncthreads();   // the chunk's staging is read no more
+    }
+}
+
+// Coalesces the map into y: a stored position i goes to y[pos[i]] (pos: the
+// exclusive prefix count of stored positions) when that is below cap; values
+// are rounded once to the value type.
+template <typename V>
+__global__ void __launch_bounds__(256) sv_emit(const uint8_t *__restrict__ flag, const double *__restrict__ yval,
+                                               const int64_t *__restrict__ pos, int64_t m, int64_t cap,
+                                               int32_t *__restrict__ y_idx, V *__restrict__ y_val) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= m || flag[i] == 0) return;
+    const int64_t p = pos[i];
+    if (p < cap) {
+        y_idx[p] = static_cast<int32_t>(i);
+        y_val[p] = static_cast<V>(yval[i]);
+    }
+}
+
+}  // namespace wsp

@@ -21,6 +21,7 @@
 #include "device_common.hpp"
 #include "tiers.hpp"
 #include "elementwise.hpp"
+#include "spmspv.hpp"
 
 using namespace wsp;
 
@@ -956,6 +957,94 @@ wingspan_status ew_values_impl(Ctx &c, int op, const wingspan_csr *A, const wing
     return WINGSPAN_OK;
 }
 
+// ---------------------------------------------------------------------------
+// SpMSpV: workspace layout and checks.
+// ---------------------------------------------------------------------------
+constexpr int64_t kSvMaxGrid = 8192;   // scatter workgroups at most (grid-stride beyond)
+
+struct SvLayout {
+    size_t off_err, off_pref, off_partials, off_flag, off_yval, off_pos, total;
+};
+
+SvLayout sv_plan(const wingspan_csr *At, int64_t nnz_x) {
+    SvLayout L{};
+    const int64_t m = std::max<int64_t>(At->ncols, 1), nx = std::max<int64_t>(nnz_x, 0);
+    size_t off = 0;
+    L.off_err = off;
+    off += align_up(sizeof(int32_t) * 4);
+    L.off_pref = off;
+    off += align_up(sizeof(int64_t) * (nx + 1));
+    L.off_partials = off;
+    const int64_t n = std::max<int64_t>(nx, m + 1);
+    off += align_up(sizeof(int64_t) * ((n + kScanTile - 1) / kScanTile + 2));
+    L.off_flag = off;
+    off += align_up(static_cast<size_t>((m + 3) / 4) * 4);   // cleared as int32 words
+    L.off_yval = off;
+    off += align_up(sizeof(double) * m);
+    L.off_pos = off;
+    off += align_up(sizeof(int64_t) * (m + 1));
+    L.total = off;
+    return L;
+}
+
+wingspan_status sv_check(const wingspan_csr *At, int64_t nnz_x) {
+    wingspan_status s = check_csr_desc(At, "At");
+    if (s != WINGSPAN_OK) return s;
+    if (nnz_x < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "nnz_x is negative");
+    if (nnz_x > At->nrows)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "x has %lld entries but length %lld", (long long)nnz_x,
+                    (long long)At->nrows);
+    return WINGSPAN_OK;
+}
+
+template <typename V>
+wingspan_status sv_impl(Ctx &c, const wingspan_csr *At, const SvLayout &L, const int32_t *x_idx, const V *x_val,
+                        int64_t nnz_x, int32_t *y_idx, V *y_val, int64_t y_cap, int64_t *y_nnz) {
+    const int64_t m = At->ncols, n = At->nrows;
+    int32_t *err = reinterpret_cast<int32_t *>(c.ws + L.off_err);
+    int64_t *pref = reinterpret_cast<int64_t *>(c.ws + L.off_pref);
+    uint8_t *flag = reinterpret_cast<uint8_t *>(c.ws + L.off_flag);
+    double *yval = reinterpret_cast<double *>(c.ws + L.off_yval);
+    int64_t *pos = reinterpret_cast<int64_t *>(c.ws + L.off_pos);
+    *y_nnz = 0;
+    if (m == 0) return WINGSPAN_OK;
+    // an empty map; x's columns' lengths scanned (checking x on the way); the scatter, sized by At's entries
+    // and reading the product count on the device
+    const int64_t nwords = (m + 3) / 4;
+    sv_clear<<<blocks_for(std::max<int64_t>(nwords, m), 256), 256, 0, c.st>>>(
+        reinterpret_cast<int32_t *>(flag), nwords, reinterpret_cast<int64_t *>(yval), m, err);
+    LAUNCH_CHECK("spmspv clear");
+    if (nnz_x > 0 && At->nnz > 0) {
+        wingspan_status s = run_scan(c, SvLenIn{At->row_ptr, x_idx, n, err}, nnz_x, pref);
+        if (s != WINGSPAN_OK) return s;
+        const int64_t chunks = (At->nnz + kSvChunk - 1) / kSvChunk;
+        sv_scatter<V><<<static_cast<unsigned>(std::min<int64_t>(chunks, kSvMaxGrid)), kSvBlock, 0, c.st>>>(
+            At->row_ptr, At->col_idx, static_cast<const V *>(At->val), x_idx, x_val, static_cast<int>(nnz_x), pref,
+            err, flag, yval);
+        LAUNCH_CHECK("spmspv scatter");
+    } else if (nnz_x > 0) {
+        // no products; x is still checked
+        wingspan_status s = run_scan(c, SvLenIn{At->row_ptr, x_idx, n, err}, nnz_x, pref);
+        if (s != WINGSPAN_OK) return s;
+    }
+    wingspan_status s = run_scan(c, SvFlagIn{flag}, m, pos);
+    if (s != WINGSPAN_OK) return s;
+    sv_emit<V><<<blocks_for(m, 256), 256, 0, c.st>>>(flag, yval, pos, m, y_cap, y_idx, y_val);
+    LAUNCH_CHECK("spmspv emit");
+    int64_t total = 0;
+    int32_t herr = 0;
+    HIP_TRY(hipMemcpyAsync(&total, pos + m, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (herr) return fail(WINGSPAN_ERR_INVALID_MATRIX, "x's indices are not strictly increasing in [0, %lld)",
+                          (long long)n);
+    *y_nnz = total;
+    if (total > y_cap)
+        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "y has %lld entries but y_cap is %lld", (long long)total,
+                    (long long)y_cap);
+    return WINGSPAN_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1203,6 +1292,48 @@ wingspan_status wingspan_elementwise_values(wingspan_ew_op op, const wingspan_cs
     if (dtype == WINGSPAN_F32)
         return ew_values_impl<float>(c, op, A, B, L, c_row_ptr_dev, c_col_idx_dev, static_cast<float *>(c_val_dev));
     return ew_values_impl<double>(c, op, A, B, L, c_row_ptr_dev, c_col_idx_dev, static_cast<double *>(c_val_dev));
+}
+
+wingspan_status wingspan_spmspv_workspace_size(const wingspan_csr *At, int64_t nnz_x, size_t *bytes) {
+    g_err.clear();
+    if (!bytes) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    wingspan_status s = sv_check(At, nnz_x);
+    if (s != WINGSPAN_OK) return s;
+    *bytes = sv_plan(At, nnz_x).total;
+    return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, const int32_t *x_idx_dev,
+                                const void *x_val_dev, int64_t nnz_x, int32_t *y_idx_dev, void *y_val_dev,
+                                int64_t y_cap, int64_t *y_nnz, void *workspace_dev, size_t workspace_bytes,
+                                void *stream) {
+    g_err.clear();
+    wingspan_status s = sv_check(At, nnz_x);
+    if (s != WINGSPAN_OK) return s;
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (!y_nnz) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "y_nnz is NULL");
+    if (nnz_x > 0 && (!x_idx_dev || !x_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "x has entries but x_idx_dev or x_val_dev is NULL");
+    if (y_cap < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "y_cap is negative");
+    if (y_cap > 0 && (!y_idx_dev || !y_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "y_cap > 0 but y_idx_dev or y_val_dev is NULL");
+    const SvLayout L = sv_plan(At, nnz_x);
+    if (workspace_bytes < L.total)
+        return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", workspace_bytes,
+                    L.total);
+    if (!workspace_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(workspace_dev) % kAlign != 0)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kAlign);
+    Ctx c{};
+    c.st = static_cast<hipStream_t>(stream);
+    c.ws = static_cast<char *>(workspace_dev);
+    c.partials = reinterpret_cast<int64_t *>(c.ws + L.off_partials);
+    if (dtype == WINGSPAN_F32)
+        return sv_impl<float>(c, At, L, x_idx_dev, static_cast<const float *>(x_val_dev), nnz_x, y_idx_dev,
+                              static_cast<float *>(y_val_dev), y_cap, y_nnz);
+    return sv_impl<double>(c, At, L, x_idx_dev, static_cast<const double *>(x_val_dev), nnz_x, y_idx_dev,
+                           static_cast<double *>(y_val_dev), y_cap, y_nnz);
 }
 
 }  // extern "C"

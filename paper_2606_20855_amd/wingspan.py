@@ -129,6 +129,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wingspan_elementwise_structure.restype = i32
     lib.wingspan_elementwise_values.argtypes = [i32, csr_p, csr_p, i32, vp, vp, vp, vp, sz, vp]
     lib.wingspan_elementwise_values.restype = i32
+    lib.wingspan_spmspv_workspace_size.argtypes = [csr_p, i64, P(sz)]
+    lib.wingspan_spmspv_workspace_size.restype = i32
+    lib.wingspan_spmspv.argtypes = [csr_p, i32, vp, vp, i64, vp, vp, i64, P(i64), vp, sz, vp]
+    lib.wingspan_spmspv.restype = i32
     _lib = lib
     return lib
 
@@ -147,6 +151,8 @@ EXPORTED = (
     "wingspan_elementwise_workspace_size",
     "wingspan_elementwise_structure",
     "wingspan_elementwise_values",
+    "wingspan_spmspv_workspace_size",
+    "wingspan_spmspv",
 )
 
 
@@ -270,6 +276,24 @@ def wingspan_elementwise_values(op: int, A: wingspan_csr, B: wingspan_csr, dtype
                                 stream: int = 0) -> None:
     _check(load().wingspan_elementwise_values(op, ctypes.byref(A), ctypes.byref(B), dtype, c_row_ptr, c_col_idx,
                                               c_val, workspace, workspace_bytes, stream or None))
+
+
+def wingspan_spmspv_workspace_size(At: wingspan_csr, nnz_x: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().wingspan_spmspv_workspace_size(ctypes.byref(At), nnz_x, ctypes.byref(n)))
+    return n.value
+
+
+def wingspan_spmspv(At: wingspan_csr, dtype: int, x_idx: int, x_val: int, nnz_x: int, y_idx: int, y_val: int,
+                    y_cap: int, workspace: int, workspace_bytes: int, stream: int = 0, check: bool = True):
+    """Returns (status, y_nnz). With check=True a non-OK status raises."""
+    y_nnz = ctypes.c_int64(0)
+    st = load().wingspan_spmspv(ctypes.byref(At), dtype, x_idx or None, x_val or None, nnz_x, y_idx or None,
+                                y_val or None, y_cap, ctypes.byref(y_nnz), workspace, workspace_bytes,
+                                stream or None)
+    if check:
+        _check(st)
+    return st, y_nnz.value
 
 
 # ---------------------------------------------------------------------------
@@ -443,3 +467,23 @@ def elementwise(op: str, A: DeviceCSR, B: DeviceCSR, stream=None) -> DeviceCSR:
     wingspan_elementwise_values(code, Ad, Bd, A.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
                                 ws.data_ptr(), nbytes, h)
     return DeviceCSR(A.nrows, A.ncols, c_rp, c_col[:nnz], c_val[:nnz])
+
+
+def spmspv(At: "DeviceCSR", x_idx, x_val, stream=None):
+    """y = A x on the GPU for A given by its columns (At, the CSR of A's
+    transpose) and x by device tensors of sorted int32 indices and values.
+    Returns (y_idx, y_val) device tensors."""
+    import torch
+    if x_val.dtype != At.val.dtype:
+        raise TypeError("x and A must share a value dtype")
+    dev = At.row_ptr.device
+    Atd = At.desc()
+    nx = int(x_idx.numel())
+    nbytes = wingspan_spmspv_workspace_size(Atd, nx)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    m = At.ncols
+    y_idx = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+    y_val = torch.empty(max(m, 1), dtype=At.val.dtype, device=dev)
+    _, n = wingspan_spmspv(Atd, At.dtype_code, x_idx.data_ptr() if nx else 0, x_val.data_ptr() if nx else 0, nx,
+                           y_idx.data_ptr(), y_val.data_ptr(), m, ws.data_ptr(), nbytes, _stream_handle(stream))
+    return y_idx[:n], y_val[:n]

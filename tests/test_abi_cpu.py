@@ -238,3 +238,30 @@ def test_elementwise_argument_errors():
                         "WINGSPAN_ERR_WORKSPACE_TOO_SMALL")]:
         got, _ = status_of(ws.wingspan_elementwise_values, *args)
         assert got == code, args
+
+
+def test_spmspv_argument_errors():
+    At = desc(12, 10, 30)   # A is 10 x 12, given by its 12 columns
+    need = ws.wingspan_spmspv_workspace_size(At, 5)
+    assert need > 0 and need % 256 == 0
+    assert ws.wingspan_spmspv_workspace_size(desc(12, 100000, 30), 5) > need
+    for args in [(At, -1), (At, 13), (desc(12, 10, -1), 5)]:
+        got, _ = status_of(ws.wingspan_spmspv_workspace_size, *args)
+        assert got == "WINGSPAN_ERR_INVALID_ARGUMENT", args
+    for args, code in [((At, 9, FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F32, 0, FAKE, 5, FAKE, FAKE, 10, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F32, FAKE, 0, 5, FAKE, FAKE, 10, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F32, FAKE, FAKE, 5, FAKE, FAKE, -1, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F32, FAKE, FAKE, 5, 0, FAKE, 10, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F64, FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, need - 1),
+                        "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"),
+                       ((At, ws.F64, FAKE, FAKE, 5, FAKE, FAKE, 10, 0, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F64, FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE + 8, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, ws.F64, FAKE, FAKE, 13, FAKE, FAKE, 10, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((desc(2**31, 10, 3), ws.F64, FAKE, FAKE, 1, FAKE, FAKE, 10, FAKE, need),
+                        "WINGSPAN_ERR_INDEX_OVERFLOW")]:
+        got, _ = status_of(ws.wingspan_spmspv, *args)
+        assert got == code, args
+    lib = ws.load()
+    st = lib.wingspan_spmspv(ctypes.byref(At), ws.F32, FAKE, FAKE, 5, FAKE, FAKE, 10, None, FAKE, need, None)
+    assert ws.STATUS[st] == "WINGSPAN_ERR_INVALID_ARGUMENT"

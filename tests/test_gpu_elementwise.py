@@ -75,7 +75,7 @@ def test_dense_rows(op):
 
 @pytest.mark.parametrize("op", ["add", "hadamard"])
 def test_chunks_over_many_empty_rows(op):
-    # 200K rows, 95% empty: a chunk of 4096 entries spans more than 1024 rows
+    # 200K rows, 95% empty: a chunk of entries spans more rows than it stages (1024)
     # and finds rows in the global row pointer
     A = matgen.random_sparse(200_000, 64, 0.05, 40, empty_rows=0.95)
     B = matgen.random_sparse(200_000, 64, 0.05, 41, empty_rows=0.9)
