@@ -15,9 +15,11 @@ input, writing into a preallocated C. Prints one JSON line:
   elementwise    SpAdd and the Hadamard product (B = A, and B a shuffled copy)
                  on the R-MAT scale-20 matrix, against HBM bandwidth
   spmspv         y = A x on the same matrix with x 10% stored
+  outer_product  outer-product SpGEMM on the 512x512-grid Laplacian, beside
+                 the two-phase Gustavson path on the same inputs
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload rmat18]
-       python bench.py --elementwise-only [--ew-workload rmat20]
+       python bench.py --elementwise-only [--ew-workload rmat20] [--outer-workload laplace512]
        python bench.py --calibrate-copy BYTES
 The second form only copies BYTES bytes device to device three times (the
 runtime's plain copy kernel): run under rocprofv3 --pmc FETCH_SIZE or
@@ -257,6 +259,61 @@ def spmspv_pass(ws, torch, A, workload, dev, steps, warmup, seed, density=0.1):
                 alg_bytes=b, GBps=round(b / (t / 1e3) / 1e9, 1), frac=round(b / (t / 1e3) / 1e9 / HBM_PEAK_GBPS, 4))
 
 
+def outer_pass(ws, torch, workload, dev, steps, warmup):
+    """Outer-product SpGEMM (per-workgroup partial Cs merged by a coalesce
+    step) on a workload, beside the two-phase Gustavson path on the same
+    inputs. Each call is timed whole with HIP events (the outer call counts its
+    products and reads back nnz(C); Gustavson runs symbolic then numeric)."""
+    import matgen
+    A, B = matgen.config(workload)
+    dAt = ws.DeviceCSR.from_host(matgen.transpose(A), dev)
+    dA = ws.DeviceCSR.from_host(A, dev)
+    dB = dA if B is A else ws.DeviceCSR.from_host(B, dev)
+    Atd, Ad, Bd = dAt.desc(), dA.desc(), dB.desc()
+    h = torch.cuda.current_stream().cuda_stream
+    n0 = ws.wingspan_outer_workspace_size(Atd, Bd, 0)
+    w0 = torch.empty(max(n0, 256), dtype=torch.uint8, device=dev)
+    P = ws.wingspan_outer_products(Atd, Bd, w0.data_ptr(), n0, h)
+    del w0
+    nbytes = ws.wingspan_outer_workspace_size(Atd, Bd, P)
+    wsb = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    m = A.nrows
+    c_rp = torch.empty(m + 1, dtype=torch.int64, device=dev)
+    c_col = torch.empty(max(P, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(P, 1), dtype=dA.val.dtype, device=dev)
+    gw, gbytes = ws.allocate_workspace(dA, dB)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def outer():
+        _, nnz = ws.wingspan_spgemm_outer(Atd, Bd, dA.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                                          P, wsb.data_ptr(), nbytes, h)
+        return nnz
+
+    def gustavson():
+        ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), gw.data_ptr(), gbytes, h, None)
+        ws.wingspan_spgemm_numeric(Ad, Bd, dA.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                                   gw.data_ptr(), gbytes, h, None)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ts = []
+        for _ in range(max(steps, 5)):
+            e[0].record()
+            fn()
+            e[1].record()
+            e[1].synchronize()
+            ts.append(e[0].elapsed_time(e[1]))
+        return float(np.mean(ts)), float(np.min(ts))
+
+    to, tomin = timed(outer)
+    nnz = outer()
+    tg, _ = timed(gustavson)
+    return dict(workload=f"{workload}: m={m}, nnz(A)={A.nnz}, {A.val.dtype}", products=P, nnz_c=nnz,
+                ms=round(to, 4), ms_min=round(tomin, 4), GFLOPs=round(2.0 * P / (to / 1e3) / 1e9, 2),
+                gustavson_ms=round(tg, 4), vs_gustavson=round(tg / to, 3))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -272,6 +329,8 @@ def main():
     ap.add_argument("--elementwise-only", action="store_true",
                     help="time only SpAdd / Hadamard and SpMSpV and print their JSON objects")
     ap.add_argument("--no-spmspv", action="store_true", help="skip the SpMSpV timing")
+    ap.add_argument("--no-outer", action="store_true", help="skip the outer-product SpGEMM timing")
+    ap.add_argument("--outer-workload", default="laplace512", help="the workload of the outer-product timing")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -302,6 +361,8 @@ def main():
                                               seed=20262)
         if not args.no_spmspv:
             out["spmspv"] = spmspv_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup, seed=20263)
+        if not args.no_outer:
+            out["outer_product"] = outer_pass(ws, torch, args.outer_workload, dev, args.steps, args.warmup)
         print(json.dumps(out), flush=True)
         return
     cfg = matgen.CONFIGS[args.workload]
@@ -422,6 +483,9 @@ def main():
         if not args.no_spmspv:
             log("timing SpMSpV (x 10% stored)")
             out["spmspv"] = spmspv_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup, seed=20263)
+    if not args.no_outer:
+        log("timing the outer-product SpGEMM")
+        out["outer_product"] = outer_pass(ws, torch, args.outer_workload, dev, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a row sample")
         out["cpu_baseline"] = cpu_baseline(A, B, args.cpu_fraction, seed=20261)

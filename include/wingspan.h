@@ -297,6 +297,45 @@ wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, co
                                 int64_t y_cap, int64_t *y_nnz, void *workspace_dev, size_t workspace_bytes,
                                 void *stream);
 
+/* ------------------------------------------------------------------------
+ * Outer-product SpGEMM, C = A B as the sum over k of the rank-1 updates
+ * A[:, k] B[k, :] (the paper's outer-product SpGEMM program, Section 5.1,
+ * which runs k in parallel and guards C with a merge level: each worker
+ * builds its own partial C and a coalesce step recombines them, Section 4.3).
+ * The result equals the Gustavson path's C (same structure; values within
+ * the rounding of a different summation order).
+ *
+ * A (m x K) is given by its columns: At is the CSR descriptor of A's
+ * transpose (At->nrows = K, At->ncols = m); B (K x n) is CSR. The
+ * intermediate storage grows with the product count
+ * P = sum over k of nnz(A[:, k]) nnz(B[k, :]), so the workspace is sized in
+ * two steps: wingspan_outer_workspace_size(At, B, 0, &bytes) gives what
+ * wingspan_outer_products needs to count P (it synchronizes `stream` once and
+ * returns P on the host); wingspan_outer_workspace_size(At, B, P, &bytes) then
+ * gives the full size (pure host code, as is the first).
+ *
+ * wingspan_spgemm_outer counts P again (returning WINGSPAN_ERR_WORKSPACE_TOO_SMALL
+ * if the workspace does not fit it) and writes c_row_ptr_dev (int64, m+1
+ * entries), c_col_idx_dev (strictly increasing columns per row) and c_val_dev
+ * (dtype, shared with At.val and B.val; products and sums in double, rounded
+ * once); *c_nnz (host) receives nnz(C). If nnz(C) > c_capacity it returns
+ * WINGSPAN_ERR_INSUFFICIENT_CAPACITY with c_row_ptr_dev and *c_nnz valid and
+ * the columns and values not written. A row of C that gathers more than 4096
+ * partial entries from the workers' partial results gives
+ * WINGSPAN_ERR_UNSUPPORTED (the Gustavson path takes any row). The call
+ * synchronizes `stream` twice.
+ * ------------------------------------------------------------------------ */
+wingspan_status wingspan_outer_workspace_size(const wingspan_csr *At, const wingspan_csr *B, int64_t products,
+                                              size_t *bytes);
+
+wingspan_status wingspan_outer_products(const wingspan_csr *At, const wingspan_csr *B, int64_t *products,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream);
+
+wingspan_status wingspan_spgemm_outer(const wingspan_csr *At, const wingspan_csr *B, wingspan_dtype dtype,
+                                      int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                      int64_t c_capacity, int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
+                                      void *stream);
+
 /* Statistics of the last call on this thread: phase 0 = symbolic, 1 = numeric,
  * 2 = single pass (wingspan_spgemm_sharded). */
 wingspan_status wingspan_last_stats(int phase, wingspan_phase_stats *out);

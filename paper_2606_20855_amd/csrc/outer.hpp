@@ -1,0 +1,296 @@
+// Outer-product SpGEMM, C = A B = sum over k of A[:, k] B[k, :] (paper,
+// Section 5.1: the outer-product program of the SpGEMM figure, which runs
+// the contraction index k in parallel and guards C with a merge level, a copy
+// of C per worker recombined by `coalesce`, Section 4.3).
+//
+// A comes by its columns (At, the CSR arrays of A's transpose) and B by its
+// rows, so the rank-1 update of index k pairs row k of At with row k of B.
+// Its |At_k| * |B_k| products, over all k, are numbered flat (q over the
+// exclusive prefix pref of the per-k counts) and cut into chunks of kOpChunk:
+//   1. each workgroup forms its chunk's products, sorts them by (row, column)
+//      in LDS and sums equal coordinates: the workgroup's own partial C;
+//   2. coalesce: every partial entry moves to its row's bucket (the partial
+//      C's rows concatenated, in arbitrary order), then each row's bucket is
+//      sorted by column and equal columns summed, in place;
+//   3. the compacted rows are scanned into C.row_ptr and gathered into CSR.
+// Products are formed and summed in double; values are rounded once.
+#pragma once
+
+#include "search.hpp"
+
+namespace wsp {
+
+constexpr int kOpChunk = 2048;     // products per workgroup (its partial C)
+constexpr int kOpBlock = 1024;     // threads of the expand kernel
+constexpr int kOpStage = 1024;     // k indices a chunk stages in LDS
+constexpr int kOpRowCap = 4096;    // longest row bucket the coalesce sorts (in LDS)
+constexpr int kOpRowBlock = 256;   // threads per long row in the coalesce
+constexpr int64_t kOpNoKey = 0x7fffffffffffffffll;
+
+// Products of rank-1 update k: |At_k| * |B_k|.
+struct OpProdIn {
+    const int32_t *at_rp, *b_rp;
+    __device__ __forceinline__ int64_t operator()(int64_t k) const {
+        return static_cast<int64_t>(at_rp[k + 1] - at_rp[k]) * static_cast<int64_t>(b_rp[k + 1] - b_rp[k]);
+    }
+};
+
+// In-place bitonic sort of n (a power of two) key/value pairs in LDS by key,
+// ascending, by the threads of the workgroup (all of them call it).
+template <typename K>
+__device__ void lds_bitonic(K *key, double *val, int n) {
+    for (int k = 2; k <= n; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int t = threadIdx.x; t < (n >> 1); t += blockDim.x) {
+                const int i = ((t & ~(j - 1)) << 1) | (t & (j - 1));   // i has bit j clear
+                const int p = i + j;
+                const bool up = (i & k) == 0;
+                const K a = key[i], b = key[p];
+                if ((a > b) == up) {
+                    key[i] = b;
+                    key[p] = a;
+                    const double v = val[i];
+                    val[i] = val[p];
+                    val[p] = v;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Exclusive workgroup scan of one int per thread; *total gets the sum. All
+// threads call it; `scratch` holds one int per wave.
+__device__ __forceinline__ int block_excl_scan(int x, int *scratch, int *total) {
+    const int nw = blockDim.x / kWave;
+    const int w = threadIdx.x / kWave;
+    const int incl = wave_incl_sum(x);
+    if (lane_id() == kWave - 1) scratch[w] = incl;
+    __syncthreads();
+    int before = 0, t = 0;
+    for (int i = 0; i < nw; ++i) {
+        const int s = scratch[i];
+        before += i < w ? s : 0;
+        t += s;
+    }
+    __syncthreads();
+    *total = t;
+    return before + incl - x;
+}
+
+// 1. A workgroup's partial C: products [q0, q0 + kOpChunk) formed, sorted by
+// key = row * n + column, equal keys summed; written compacted at part_*[q0..)
+// with their count in part_len[chunk]; row_cnt[row] counts the entries each
+// row receives from all partial Cs.
+template <typename V>
+__global__ void __launch_bounds__(kOpBlock) op_expand(const int32_t *__restrict__ at_rp,
+                                                      const int32_t *__restrict__ at_col,
+                                                      const V *__restrict__ at_val,
+                                                      const int32_t *__restrict__ b_rp,
+                                                      const int32_t *__restrict__ b_col,
+                                                      const V *__restrict__ b_val, int K, int64_t n,
+                                                      const int64_t *__restrict__ pref, int64_t P,
+                                                      int64_t *__restrict__ part_key, double *__restrict__ part_val,
+                                                      int32_t *__restrict__ part_len, int32_t *__restrict__ row_cnt) {
+    __shared__ int64_t s_key[kOpChunk];
+    __shared__ double s_val[kOpChunk];
+    __shared__ int64_t s_pref[kOpStage];
+    __shared__ int s_t[2];
+    __shared__ int s_scan[kOpBlock / kWave];
+    const int64_t q0 = static_cast<int64_t>(blockIdx.x) * kOpChunk;
+    if (q0 >= P) return;   // whole workgroup
+    const int64_t q1 = P - q0 < kOpChunk ? P : q0 + kOpChunk;
+    if (threadIdx.x < kWave) {
+        const int t0 = wave_find_entry(pref, K, q0);
+        const int t1 = wave_find_entry(pref, K, q1 - 1);
+        if (threadIdx.x == 0) {
+            s_t[0] = t0;
+            s_t[1] = t1;
+        }
+    }
+    __syncthreads();
+    const int t0 = s_t[0];
+    const int nt = s_t[1] - t0 + 1;
+    const bool staged = nt <= kOpStage;
+    if (staged)
+        for (int k = threadIdx.x; k < nt; k += blockDim.x) s_pref[k] = pref[t0 + k];
+    __syncthreads();
+    for (int s = threadIdx.x; s < kOpChunk; s += blockDim.x) {
+        const int64_t q = q0 + s;
+        int64_t key = kOpNoKey;
+        double v = 0.0;
+        if (q < q1) {
+            const int k = staged ? t0 + lds_find_entry(s_pref, nt, q) : t0 + lds_find_entry(pref + t0, nt, q);
+            const int64_t r = q - (staged ? s_pref[k - t0] : pref[k]);
+            const int64_t nb = b_rp[k + 1] - b_rp[k];   // > 0: index k has products
+            const int64_t ai = r / nb;
+            const int ia = at_rp[k] + static_cast<int>(ai);
+            const int jb = b_rp[k] + static_cast<int>(r - ai * nb);
+            key = static_cast<int64_t>(at_col[ia]) * n + b_col[jb];
+            v = to_d(at_val[ia]) * to_d(b_val[jb]);
+        }
+        s_key[s] = key;
+        s_val[s] = v;
+    }
+    __syncthreads();
+    lds_bitonic(s_key, s_val, kOpChunk);
+    // heads of runs of equal keys, two slots per thread
+    constexpr int PER = kOpChunk / kOpBlock;
+    int heads = 0;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int s = threadIdx.x * PER + u;
+        const int64_t kk = s_key[s];
+        heads += (kk != kOpNoKey && (s == 0 || s_key[s - 1] != kk)) ? 1 : 0;
+    }
+    int total = 0;
+    int pos = block_excl_scan(heads, s_scan, &total);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int s = threadIdx.x * PER + u;
+        const int64_t kk = s_key[s];
+        if (kk == kOpNoKey || (s > 0 && s_key[s - 1] == kk)) continue;
+        double sum = s_val[s];
+        for (int e = s + 1; e < kOpChunk && s_key[e] == kk; ++e) sum += s_val[e];
+        part_key[q0 + pos] = kk;
+        part_val[q0 + pos] = sum;
+        atomicAdd(&row_cnt[kk / n], 1);
+        ++pos;
+    }
+    if (threadIdx.x == 0) part_len[blockIdx.x] = total;
+}
+
+// 2a. Each partial entry moves to the next free slot of its row's bucket.
+__global__ void __launch_bounds__(256) op_bucket(const int64_t *__restrict__ part_key,
+                                                 const double *__restrict__ part_val,
+                                                 const int32_t *__restrict__ part_len, int64_t n,
+                                                 const int64_t *__restrict__ bucket_off, int32_t *__restrict__ row_fill,
+                                                 int32_t *__restrict__ bkt_col, double *__restrict__ bkt_val) {
+    const int len = part_len[blockIdx.x];
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kOpChunk;
+    for (int t = threadIdx.x; t < len; t += blockDim.x) {
+        const int64_t key = part_key[base + t];
+        const int64_t i = key / n;
+        const int64_t pos = bucket_off[i] + atomicAdd(&row_fill[i], 1);
+        bkt_col[pos] = static_cast<int32_t>(key - i * n);
+        bkt_val[pos] = part_val[base + t];
+    }
+}
+
+// 2b. Short buckets (at most 64 entries), one wave per row: sorted in
+// registers (bitonic through lane shuffles), equal columns summed, written back
+// compacted from the bucket's start (columns in bkt_col, values rounded to V in
+// out_val). Longer buckets are listed for op_merge_long; buckets beyond
+// kOpRowCap set kErrUnsupportedRow.
+constexpr int32_t kErrUnsupportedRow = 16;
+
+template <typename V>
+__global__ void __launch_bounds__(256) op_merge_short(const int64_t *__restrict__ bucket_off, int64_t m,
+                                                      int32_t *__restrict__ bkt_col,
+                                                      const double *__restrict__ bkt_val, V *__restrict__ out_val,
+                                                      int32_t *__restrict__ row_nnz, int32_t *__restrict__ long_rows,
+                                                      int32_t *counters) {
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + threadIdx.x / kWave;
+    if (row >= m) return;   // whole wave: no barriers in this kernel
+    const int ln = lane_id();
+    const int64_t lo = bucket_off[row];
+    const int64_t len = bucket_off[row + 1] - lo;
+    if (len > kWave) {
+        if (ln == 0) {
+            if (len > kOpRowCap) {
+                atomicOr(&counters[1], kErrUnsupportedRow);
+                row_nnz[row] = 0;
+            } else {
+                long_rows[atomicAdd(&counters[0], 1)] = static_cast<int32_t>(row);
+            }
+        }
+        return;
+    }
+    int key = ln < len ? bkt_col[lo + ln] : 0x7fffffff;
+    double v = ln < len ? bkt_val[lo + ln] : 0.0;
+    for (int k = 2; k <= kWave; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const int ok = __shfl_xor(key, j, kWave);
+            const double ov = __shfl_xor(v, j, kWave);
+            const bool lower = (ln & j) == 0;
+            const bool up = (ln & k) == 0;
+            // the lower lane of an ascending pair keeps the smaller key
+            const bool take = lower == up ? ok < key : ok > key;
+            if (take) {
+                key = ok;
+                v = ov;
+            }
+        }
+    }
+    const int prev = __shfl_up(key, 1, kWave);
+    const bool head = ln < len && (ln == 0 || prev != key);
+    const uint64_t hm = ballot(head);
+    // sum each run: a head adds the values of the lanes after it with its key
+    double sum = v;
+    for (int d = 1; d < kWave; ++d) {
+        const int ok = __shfl_down(key, d, kWave);
+        const double ov = __shfl_down(v, d, kWave);
+        const bool more = ln + d < len && ok == key;
+        if (ballot(head && more) == 0ull) break;
+        if (head && more) sum += ov;
+    }
+    if (head) {
+        const int pos = __popcll(hm & ((1ull << ln) - 1ull));
+        bkt_col[lo + pos] = key;
+        out_val[lo + pos] = static_cast<V>(sum);
+    }
+    if (ln == 0) row_nnz[row] = __popcll(hm);
+}
+
+// 2c. Long buckets (65 .. kOpRowCap entries), a workgroup per row, rows taken
+// grid-stride from the list op_merge_short made: the bucket is sorted in LDS
+// and compacted as in op_merge_short.
+template <typename V>
+__global__ void __launch_bounds__(kOpRowBlock) op_merge_long(const int64_t *__restrict__ bucket_off,
+                                                             int32_t *__restrict__ bkt_col,
+                                                             const double *__restrict__ bkt_val,
+                                                             V *__restrict__ out_val, int32_t *__restrict__ row_nnz,
+                                                             const int32_t *__restrict__ long_rows,
+                                                             const int32_t *counters) {
+    __shared__ int32_t s_key[kOpRowCap];
+    __shared__ double s_val[kOpRowCap];
+    __shared__ int s_scan[kOpRowBlock / kWave];
+    constexpr int PER = kOpRowCap / kOpRowBlock;
+    const int nrows = counters[0];
+    for (int idx = blockIdx.x; idx < nrows; idx += gridDim.x) {
+        const int row = long_rows[idx];
+        const int64_t lo = bucket_off[row];
+        const int len = static_cast<int>(bucket_off[row + 1] - lo);
+        int np = kWave * 2;
+        while (np < len) np <<= 1;
+        for (int s = threadIdx.x; s < np; s += blockDim.x) {
+            s_key[s] = s < len ? bkt_col[lo + s] : 0x7fffffff;
+            s_val[s] = s < len ? bkt_val[lo + s] : 0.0;
+        }
+        __syncthreads();
+        lds_bitonic(s_key, s_val, np);
+        int heads = 0;
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int s = threadIdx.x * PER + u;
+            heads += (s < len && (s == 0 || s_key[s - 1] != s_key[s])) ? 1 : 0;
+        }
+        int total = 0;
+        int pos = block_excl_scan(heads, s_scan, &total);
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int s = threadIdx.x * PER + u;
+            if (s >= len || (s > 0 && s_key[s - 1] == s_key[s])) continue;
+            const int kk = s_key[s];
+            double sum = s_val[s];
+            for (int e = s + 1; e < len && s_key[e] == kk; ++e) sum += s_val[e];
+            bkt_col[lo + pos] = kk;
+            out_val[lo + pos] = static_cast<V>(sum);
+            ++pos;
+        }
+        if (threadIdx.x == 0) row_nnz[row] = total;
+        __syncthreads();   // LDS is reused by the next row
+    }
+}
+
+}  // namespace wsp

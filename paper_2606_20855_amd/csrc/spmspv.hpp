@@ -16,7 +16,7 @@
 // lengths), so long and short columns balance by themselves.
 #pragma once
 
-#include "device_common.hpp"
+#include "search.hpp"
 
 namespace wsp {
 
@@ -56,21 +56,6 @@ struct SvFlagIn {
     const uint8_t *flag;
     __device__ __forceinline__ int64_t operator()(int64_t i) const { return flag[i] != 0 ? 1 : 0; }
 };
-
-// Last t in [0, nnz_x) with pref[t] <= q; all 64 lanes of one wave take part.
-__device__ __forceinline__ int wave_find_entry(const int64_t *__restrict__ pref, int nnz_x, int64_t q) {
-    int lo = 0, hi = nnz_x - 1;   // pref[lo] <= q holds throughout (pref[0] = 0)
-    while (hi > lo) {
-        const int step = (hi - lo + kWave) / kWave;
-        const int idx = lo + lane_id() * step;
-        const bool le = idx <= hi && pref[idx] <= q;
-        const uint64_t m = ballot(le);
-        lo = lo + (63 - __clzll(m)) * step;
-        const int h = lo + step - 1;
-        hi = h < hi ? h : hi;
-    }
-    return lo;
-}
 
 // Scatters the P = pref[nnz_x] products into the map: yval[i] += A[i, j] * x_j
 // and flag[i] = 1 for each selected entry (i, j). Workgroups take chunks of

@@ -22,6 +22,7 @@
 #include "tiers.hpp"
 #include "elementwise.hpp"
 #include "spmspv.hpp"
+#include "outer.hpp"
 
 using namespace wsp;
 
@@ -1045,6 +1046,156 @@ wingspan_status sv_impl(Ctx &c, const wingspan_csr *At, const SvLayout &L, const
     return WINGSPAN_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Outer-product SpGEMM: workspace layout and checks. The count's arrays come
+// first, at offsets that do not depend on the product count P.
+// ---------------------------------------------------------------------------
+constexpr int64_t kOpLongGrid = 2048;   // coalesce workgroups for long rows at most (grid-stride beyond)
+
+struct OpLayout {
+    size_t off_ctr, off_pref, off_partials, off_part_key, off_part_val, off_part_len, off_row_cnt, off_row_fill,
+        off_bucket, off_row_nnz, off_long, off_bkt_col, off_bkt_val, off_out_val, total;
+};
+
+OpLayout op_plan(const wingspan_csr *At, const wingspan_csr *B, int64_t P) {
+    OpLayout L{};
+    const int64_t K = std::max<int64_t>(At->nrows, 1), m = std::max<int64_t>(At->ncols, 1);
+    const int64_t p = std::max<int64_t>(P, 1), chunks = (p + kOpChunk - 1) / kOpChunk;
+    size_t off = 0;
+    L.off_ctr = off;
+    off += align_up(sizeof(int32_t) * 4);
+    L.off_pref = off;
+    off += align_up(sizeof(int64_t) * (K + 1));
+    L.off_partials = off;
+    const int64_t n = std::max<int64_t>(K, m) + 1;
+    off += align_up(sizeof(int64_t) * ((n + kScanTile - 1) / kScanTile + 2));
+    L.off_part_key = off;
+    off += align_up(sizeof(int64_t) * p);
+    L.off_part_val = off;
+    off += align_up(sizeof(double) * p);
+    L.off_part_len = off;
+    off += align_up(sizeof(int32_t) * chunks);
+    L.off_row_cnt = off;
+    off += align_up(sizeof(int32_t) * m);
+    L.off_row_fill = off;
+    off += align_up(sizeof(int32_t) * m);
+    L.off_bucket = off;
+    off += align_up(sizeof(int64_t) * (m + 1));
+    L.off_row_nnz = off;
+    off += align_up(sizeof(int32_t) * m);
+    L.off_long = off;
+    off += align_up(sizeof(int32_t) * m);
+    L.off_bkt_col = off;
+    off += align_up(sizeof(int32_t) * p);
+    L.off_bkt_val = off;
+    off += align_up(sizeof(double) * p);
+    L.off_out_val = off;
+    off += align_up(sizeof(double) * p);
+    L.total = off;
+    (void)B;
+    return L;
+}
+
+wingspan_status op_check(const wingspan_csr *At, const wingspan_csr *B) {
+    wingspan_status s = check_csr_desc(At, "At");
+    if (s != WINGSPAN_OK) return s;
+    if ((s = check_csr_desc(B, "B")) != WINGSPAN_OK) return s;
+    if (At->nrows != B->nrows)
+        return fail(WINGSPAN_ERR_DIMENSION_MISMATCH, "At has %lld rows (A's columns) but B has %lld rows",
+                    (long long)At->nrows, (long long)B->nrows);
+    return WINGSPAN_OK;
+}
+
+wingspan_status op_workspace_ok(void *ws, size_t bytes, size_t need) {
+    if (bytes < need) return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", bytes, need);
+    if (!ws) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kAlign);
+    return WINGSPAN_OK;
+}
+
+// The per-k product prefix into pref and its total, read back.
+wingspan_status op_count(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, const OpLayout &L, int64_t *P) {
+    int64_t *pref = reinterpret_cast<int64_t *>(c.ws + L.off_pref);
+    c.partials = reinterpret_cast<int64_t *>(c.ws + L.off_partials);
+    *P = 0;
+    if (At->nrows == 0) return WINGSPAN_OK;
+    wingspan_status s = run_scan(c, OpProdIn{At->row_ptr, B->row_ptr}, At->nrows, pref);
+    if (s != WINGSPAN_OK) return s;
+    HIP_TRY(hipMemcpyAsync(P, pref + At->nrows, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    return WINGSPAN_OK;
+}
+
+template <typename V>
+wingspan_status op_impl(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, const OpLayout &L, int64_t P,
+                        int64_t *c_rp, int32_t *c_col, V *c_val, int64_t c_cap, int64_t *c_nnz) {
+    const int64_t K = At->nrows, m = At->ncols, n = B->ncols;
+    auto at = [&](size_t off) { return c.ws + off; };
+    int32_t *ctr = reinterpret_cast<int32_t *>(at(L.off_ctr));
+    const int64_t *pref = reinterpret_cast<const int64_t *>(at(L.off_pref));
+    int64_t *part_key = reinterpret_cast<int64_t *>(at(L.off_part_key));
+    double *part_val = reinterpret_cast<double *>(at(L.off_part_val));
+    int32_t *part_len = reinterpret_cast<int32_t *>(at(L.off_part_len));
+    int32_t *row_cnt = reinterpret_cast<int32_t *>(at(L.off_row_cnt));
+    int32_t *row_fill = reinterpret_cast<int32_t *>(at(L.off_row_fill));
+    int64_t *bucket = reinterpret_cast<int64_t *>(at(L.off_bucket));
+    int32_t *row_nnz = reinterpret_cast<int32_t *>(at(L.off_row_nnz));
+    int32_t *long_rows = reinterpret_cast<int32_t *>(at(L.off_long));
+    int32_t *bkt_col = reinterpret_cast<int32_t *>(at(L.off_bkt_col));
+    double *bkt_val = reinterpret_cast<double *>(at(L.off_bkt_val));
+    V *out_val = reinterpret_cast<V *>(at(L.off_out_val));
+    *c_nnz = 0;
+    if (m == 0) {
+        // C has no rows: its row pointer is the single 0
+        fill_i64<<<1, 64, 0, c.st>>>(c_rp, 1, 0);
+        LAUNCH_CHECK("outer empty");
+        return WINGSPAN_OK;
+    }
+    fill_i32<<<1, 64, 0, c.st>>>(ctr, 4, 0);
+    fill_i32<<<blocks_for(m, 256), 256, 0, c.st>>>(row_cnt, m, 0);
+    fill_i32<<<blocks_for(m, 256), 256, 0, c.st>>>(row_fill, m, 0);
+    LAUNCH_CHECK("outer clear");
+    const int64_t chunks = (P + kOpChunk - 1) / kOpChunk;
+    // 1. the workgroups' partial Cs
+    if (P > 0) {
+        op_expand<V><<<static_cast<unsigned>(chunks), kOpBlock, 0, c.st>>>(
+            At->row_ptr, At->col_idx, static_cast<const V *>(At->val), B->row_ptr, B->col_idx,
+            static_cast<const V *>(B->val), static_cast<int>(K), n, pref, P, part_key, part_val, part_len, row_cnt);
+        LAUNCH_CHECK("outer expand");
+    }
+    // 2. coalesce: row buckets, then each bucket sorted and compacted
+    wingspan_status s = run_scan(c, CountIn{row_cnt}, m, bucket);
+    if (s != WINGSPAN_OK) return s;
+    if (P > 0) {
+        op_bucket<<<static_cast<unsigned>(chunks), 256, 0, c.st>>>(part_key, part_val, part_len, n, bucket, row_fill,
+                                                                   bkt_col, bkt_val);
+        LAUNCH_CHECK("outer bucket");
+    }
+    op_merge_short<V><<<blocks_for(m, 256 / kWave), 256, 0, c.st>>>(bucket, m, bkt_col, bkt_val, out_val, row_nnz,
+                                                                    long_rows, ctr);
+    op_merge_long<V><<<static_cast<unsigned>(std::min<int64_t>(m, kOpLongGrid)), kOpRowBlock, 0, c.st>>>(
+        bucket, bkt_col, bkt_val, out_val, row_nnz, long_rows, ctr);
+    LAUNCH_CHECK("outer merge");
+    // 3. C.row_ptr, then the rows gathered into CSR
+    if ((s = run_scan(c, CountIn{row_nnz}, m, c_rp)) != WINGSPAN_OK) return s;
+    int32_t herr = 0;
+    HIP_TRY(hipMemcpyAsync(c_nnz, c_rp + m, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipMemcpyAsync(&herr, ctr + 1, sizeof(int32_t), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (herr & kErrUnsupportedRow)
+        return fail(WINGSPAN_ERR_UNSUPPORTED, "a row of C gathers more than %d partial entries", kOpRowCap);
+    if (*c_nnz > c_cap)
+        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "C has %lld entries but c_capacity is %lld",
+                    (long long)*c_nnz, (long long)c_cap);
+    if (*c_nnz > 0) {
+        gather_rows<V><<<static_cast<unsigned>((*c_nnz + kGatherChunk - 1) / kGatherChunk), 256, 0, c.st>>>(
+            m, bucket, c_rp, bkt_col, out_val, c_col, c_val);
+        LAUNCH_CHECK("outer gather");
+    }
+    return WINGSPAN_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1334,6 +1485,64 @@ wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, co
                               static_cast<float *>(y_val_dev), y_cap, y_nnz);
     return sv_impl<double>(c, At, L, x_idx_dev, static_cast<const double *>(x_val_dev), nnz_x, y_idx_dev,
                            static_cast<double *>(y_val_dev), y_cap, y_nnz);
+}
+
+wingspan_status wingspan_outer_workspace_size(const wingspan_csr *At, const wingspan_csr *B, int64_t products,
+                                              size_t *bytes) {
+    g_err.clear();
+    if (!bytes) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    wingspan_status s = op_check(At, B);
+    if (s != WINGSPAN_OK) return s;
+    if (products < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "products is negative");
+    *bytes = op_plan(At, B, products).total;
+    return WINGSPAN_OK;
+}
+
+wingspan_status wingspan_outer_products(const wingspan_csr *At, const wingspan_csr *B, int64_t *products,
+                                        void *workspace_dev, size_t workspace_bytes, void *stream) {
+    g_err.clear();
+    wingspan_status s = op_check(At, B);
+    if (s != WINGSPAN_OK) return s;
+    if (!products) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "products is NULL");
+    const OpLayout L = op_plan(At, B, 0);
+    if ((s = op_workspace_ok(workspace_dev, workspace_bytes, L.off_part_key)) != WINGSPAN_OK) return s;
+    Ctx c{};
+    c.st = static_cast<hipStream_t>(stream);
+    c.ws = static_cast<char *>(workspace_dev);
+    return op_count(c, At, B, L, products);
+}
+
+wingspan_status wingspan_spgemm_outer(const wingspan_csr *At, const wingspan_csr *B, wingspan_dtype dtype,
+                                      int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                      int64_t c_capacity, int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
+                                      void *stream) {
+    g_err.clear();
+    wingspan_status s = op_check(At, B);
+    if (s != WINGSPAN_OK) return s;
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (!c_nnz) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_nnz is NULL");
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    if (c_capacity < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_capacity is negative");
+    if (c_capacity > 0 && (!c_col_idx_dev || !c_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_capacity > 0 but c_col_idx_dev or c_val_dev is NULL");
+    *c_nnz = 0;
+    const OpLayout L0 = op_plan(At, B, 0);
+    if ((s = op_workspace_ok(workspace_dev, workspace_bytes, L0.off_part_key)) != WINGSPAN_OK) return s;
+    Ctx c{};
+    c.st = static_cast<hipStream_t>(stream);
+    c.ws = static_cast<char *>(workspace_dev);
+    int64_t P = 0;
+    if ((s = op_count(c, At, B, L0, &P)) != WINGSPAN_OK) return s;
+    const OpLayout L = op_plan(At, B, P);
+    if (workspace_bytes < L.total)
+        return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed for %lld products",
+                    workspace_bytes, L.total, (long long)P);
+    if (dtype == WINGSPAN_F32)
+        return op_impl<float>(c, At, B, L, P, c_row_ptr_dev, c_col_idx_dev, static_cast<float *>(c_val_dev),
+                              c_capacity, c_nnz);
+    return op_impl<double>(c, At, B, L, P, c_row_ptr_dev, c_col_idx_dev, static_cast<double *>(c_val_dev),
+                           c_capacity, c_nnz);
 }
 
 }  // extern "C"

@@ -133,6 +133,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wingspan_spmspv_workspace_size.restype = i32
     lib.wingspan_spmspv.argtypes = [csr_p, i32, vp, vp, i64, vp, vp, i64, P(i64), vp, sz, vp]
     lib.wingspan_spmspv.restype = i32
+    lib.wingspan_outer_workspace_size.argtypes = [csr_p, csr_p, i64, P(sz)]
+    lib.wingspan_outer_workspace_size.restype = i32
+    lib.wingspan_outer_products.argtypes = [csr_p, csr_p, P(i64), vp, sz, vp]
+    lib.wingspan_outer_products.restype = i32
+    lib.wingspan_spgemm_outer.argtypes = [csr_p, csr_p, i32, vp, vp, vp, i64, P(i64), vp, sz, vp]
+    lib.wingspan_spgemm_outer.restype = i32
     _lib = lib
     return lib
 
@@ -153,6 +159,9 @@ EXPORTED = (
     "wingspan_elementwise_values",
     "wingspan_spmspv_workspace_size",
     "wingspan_spmspv",
+    "wingspan_outer_workspace_size",
+    "wingspan_outer_products",
+    "wingspan_spgemm_outer",
 )
 
 
@@ -294,6 +303,33 @@ def wingspan_spmspv(At: wingspan_csr, dtype: int, x_idx: int, x_val: int, nnz_x:
     if check:
         _check(st)
     return st, y_nnz.value
+
+
+def wingspan_outer_workspace_size(At: wingspan_csr, B: wingspan_csr, products: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().wingspan_outer_workspace_size(ctypes.byref(At), ctypes.byref(B), products, ctypes.byref(n)))
+    return n.value
+
+
+def wingspan_outer_products(At: wingspan_csr, B: wingspan_csr, workspace: int, workspace_bytes: int,
+                            stream: int = 0) -> int:
+    p = ctypes.c_int64(0)
+    _check(load().wingspan_outer_products(ctypes.byref(At), ctypes.byref(B), ctypes.byref(p), workspace,
+                                          workspace_bytes, stream or None))
+    return p.value
+
+
+def wingspan_spgemm_outer(At: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int, c_col_idx: int, c_val: int,
+                          c_capacity: int, workspace: int, workspace_bytes: int, stream: int = 0,
+                          check: bool = True):
+    """Returns (status, c_nnz). With check=True a non-OK status raises."""
+    nnz = ctypes.c_int64(0)
+    st = load().wingspan_spgemm_outer(ctypes.byref(At), ctypes.byref(B), dtype, c_row_ptr, c_col_idx or None,
+                                      c_val or None, c_capacity, ctypes.byref(nnz), workspace, workspace_bytes,
+                                      stream or None)
+    if check:
+        _check(st)
+    return st, nnz.value
 
 
 # ---------------------------------------------------------------------------
@@ -487,3 +523,29 @@ def spmspv(At: "DeviceCSR", x_idx, x_val, stream=None):
     _, n = wingspan_spmspv(Atd, At.dtype_code, x_idx.data_ptr() if nx else 0, x_val.data_ptr() if nx else 0, nx,
                            y_idx.data_ptr(), y_val.data_ptr(), m, ws.data_ptr(), nbytes, _stream_handle(stream))
     return y_idx[:n], y_val[:n]
+
+
+def spgemm_outer(At: "DeviceCSR", B: "DeviceCSR", stream=None) -> "DeviceCSR":
+    """C = A B by outer products on the GPU, A given by its columns (At, the
+    CSR of A's transpose). Counts the products, sizes the workspace, then
+    computes C with the exact capacity."""
+    import torch
+    if At.val.dtype != B.val.dtype:
+        raise TypeError("A and B must share a value dtype")
+    dev = At.row_ptr.device
+    Atd, Bd = At.desc(), B.desc()
+    h = _stream_handle(stream)
+    n0 = wingspan_outer_workspace_size(Atd, Bd, 0)
+    ws0 = torch.empty(max(n0, 256), dtype=torch.uint8, device=dev)
+    P = wingspan_outer_products(Atd, Bd, ws0.data_ptr(), n0, h)
+    nbytes = wingspan_outer_workspace_size(Atd, Bd, P)
+    del ws0
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    m = At.ncols
+    c_rp = torch.empty(m + 1, dtype=torch.int64, device=dev)
+    cap = P   # nnz(C) <= P
+    c_col = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(cap, 1), dtype=At.val.dtype, device=dev)
+    _, nnz = wingspan_spgemm_outer(Atd, Bd, At.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(), cap,
+                                   ws.data_ptr(), nbytes, h)
+    return DeviceCSR(m, B.ncols, c_rp, c_col[:nnz], c_val[:nnz])

@@ -265,3 +265,27 @@ def test_spmspv_argument_errors():
     lib = ws.load()
     st = lib.wingspan_spmspv(ctypes.byref(At), ws.F32, FAKE, FAKE, 5, FAKE, FAKE, 10, None, FAKE, need, None)
     assert ws.STATUS[st] == "WINGSPAN_ERR_INVALID_ARGUMENT"
+
+
+def test_outer_argument_errors():
+    At, B = desc(9, 12, 30), desc(9, 15, 40)   # A is 12 x 9 (by its 9 columns), B is 9 x 15
+    base = ws.wingspan_outer_workspace_size(At, B, 0)
+    full = ws.wingspan_outer_workspace_size(At, B, 100000)
+    assert base % 256 == 0 and full > base
+    got, _ = status_of(ws.wingspan_outer_workspace_size, At, desc(10, 15, 40), 0)
+    assert got == "WINGSPAN_ERR_DIMENSION_MISMATCH"
+    got, _ = status_of(ws.wingspan_outer_workspace_size, At, B, -1)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    got, _ = status_of(ws.wingspan_outer_products, At, B, FAKE, 0)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"
+    got, _ = status_of(ws.wingspan_outer_products, At, B, FAKE + 8, base)
+    assert got == "WINGSPAN_ERR_INVALID_ARGUMENT"
+    for args, code in [((At, B, 9, FAKE, FAKE, FAKE, 10, FAKE, full), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, B, ws.F32, 0, FAKE, FAKE, 10, FAKE, full), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, B, ws.F32, FAKE, 0, FAKE, 10, FAKE, full), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, B, ws.F32, FAKE, FAKE, FAKE, -1, FAKE, full), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, B, ws.F64, FAKE, FAKE, FAKE, 10, 0, full), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((At, B, ws.F64, FAKE, FAKE, FAKE, 10, FAKE, 16), "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"),
+                       ((At, desc(9, 15, -2), ws.F64, FAKE, FAKE, FAKE, 10, FAKE, full), "WINGSPAN_ERR_INVALID_ARGUMENT")]:
+        got, _ = status_of(ws.wingspan_spgemm_outer, *args)
+        assert got == code, args
