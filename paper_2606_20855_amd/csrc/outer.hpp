@@ -79,21 +79,24 @@ __device__ __forceinline__ int block_excl_scan(int x, int *scratch, int *total) 
 }
 
 // 1. A workgroup's partial C: products [q0, q0 + kOpChunk) formed, sorted by
-// key = row * n + column, equal keys summed; written compacted at part_*[q0..)
+// key = row << 32 | column (row-major order), equal keys summed; written compacted at part_*[q0..)
 // with their count in part_len[chunk]; row_cnt[row] counts the entries each
-// row receives from all partial Cs.
+// row receives from all partial Cs (one atomic per run of a row in the
+// partial C, which its sort made contiguous).
 template <typename V>
 __global__ void __launch_bounds__(kOpBlock) op_expand(const int32_t *__restrict__ at_rp,
                                                       const int32_t *__restrict__ at_col,
                                                       const V *__restrict__ at_val,
                                                       const int32_t *__restrict__ b_rp,
                                                       const int32_t *__restrict__ b_col,
-                                                      const V *__restrict__ b_val, int K, int64_t n,
+                                                      const V *__restrict__ b_val, int K,
                                                       const int64_t *__restrict__ pref, int64_t P,
                                                       int64_t *__restrict__ part_key, double *__restrict__ part_val,
                                                       int32_t *__restrict__ part_len, int32_t *__restrict__ row_cnt) {
     __shared__ int64_t s_key[kOpChunk];
     __shared__ double s_val[kOpChunk];
+    __shared__ int64_t c_key[kOpChunk];   // the partial C, compacted
+    __shared__ double c_val[kOpChunk];
     __shared__ int64_t s_pref[kOpStage];
     __shared__ int s_t[2];
     __shared__ int s_scan[kOpBlock / kWave];
@@ -126,7 +129,7 @@ __global__ void __launch_bounds__(kOpBlock) op_expand(const int32_t *__restrict_
             const int64_t ai = r / nb;
             const int ia = at_rp[k] + static_cast<int>(ai);
             const int jb = b_rp[k] + static_cast<int>(r - ai * nb);
-            key = static_cast<int64_t>(at_col[ia]) * n + b_col[jb];
+            key = static_cast<int64_t>(at_col[ia]) << 32 | static_cast<uint32_t>(b_col[jb]);
             v = to_d(at_val[ia]) * to_d(b_val[jb]);
         }
         s_key[s] = key;
@@ -152,66 +155,87 @@ __global__ void __launch_bounds__(kOpBlock) op_expand(const int32_t *__restrict_
         if (kk == kOpNoKey || (s > 0 && s_key[s - 1] == kk)) continue;
         double sum = s_val[s];
         for (int e = s + 1; e < kOpChunk && s_key[e] == kk; ++e) sum += s_val[e];
-        part_key[q0 + pos] = kk;
-        part_val[q0 + pos] = sum;
-        atomicAdd(&row_cnt[kk / n], 1);
+        c_key[pos] = kk;
+        c_val[pos] = sum;
         ++pos;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < total; t += blockDim.x) {
+        const int64_t kk = c_key[t];
+        part_key[q0 + t] = kk;
+        part_val[q0 + t] = c_val[t];
+        const int64_t row = kk >> 32;
+        if (t == 0 || (c_key[t - 1] >> 32) != row) {
+            int e = t + 1;
+            while (e < total && (c_key[e] >> 32) == row) ++e;
+            atomicAdd(&row_cnt[row], e - t);
+        }
     }
     if (threadIdx.x == 0) part_len[blockIdx.x] = total;
 }
 
-// 2a. Each partial entry moves to the next free slot of its row's bucket.
+// 2a. Each run of a row in a partial C claims that many slots of the row's
+// bucket (one atomic) and copies its entries there.
 __global__ void __launch_bounds__(256) op_bucket(const int64_t *__restrict__ part_key,
                                                  const double *__restrict__ part_val,
-                                                 const int32_t *__restrict__ part_len, int64_t n,
+                                                 const int32_t *__restrict__ part_len,
                                                  const int64_t *__restrict__ bucket_off, int32_t *__restrict__ row_fill,
                                                  int32_t *__restrict__ bkt_col, double *__restrict__ bkt_val) {
+    __shared__ int32_t s_row[kOpChunk];
     const int len = part_len[blockIdx.x];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kOpChunk;
+    for (int t = threadIdx.x; t < len; t += blockDim.x) s_row[t] = static_cast<int32_t>(part_key[base + t] >> 32);
+    __syncthreads();
     for (int t = threadIdx.x; t < len; t += blockDim.x) {
-        const int64_t key = part_key[base + t];
-        const int64_t i = key / n;
-        const int64_t pos = bucket_off[i] + atomicAdd(&row_fill[i], 1);
-        bkt_col[pos] = static_cast<int32_t>(key - i * n);
-        bkt_val[pos] = part_val[base + t];
+        const int row = s_row[t];
+        if (t > 0 && s_row[t - 1] == row) continue;
+        int e = t + 1;
+        while (e < len && s_row[e] == row) ++e;
+        const int64_t pos = bucket_off[row] + atomicAdd(&row_fill[row], e - t);
+        for (int u = t; u < e; ++u) {
+            bkt_col[pos + (u - t)] = static_cast<int32_t>(part_key[base + u] & 0xffffffffll);
+            bkt_val[pos + (u - t)] = part_val[base + u];
+        }
     }
 }
 
-// 2b. Short buckets (at most 64 entries), one wave per row: sorted in
-// registers (bitonic through lane shuffles), equal columns summed, written back
-// compacted from the bucket's start (columns in bkt_col, values rounded to V in
-// out_val). Longer buckets are listed for op_merge_long; buckets beyond
-// kOpRowCap set kErrUnsupportedRow.
+// 2b. Short buckets, S lanes per row (S = 32: buckets of at most 32 entries;
+// S = 64: 33 to 64, and the longer ones are listed for op_merge_long, those
+// beyond kOpRowCap setting kErrUnsupportedRow): sorted in registers (bitonic
+// through lane shuffles within the S-lane group), equal columns summed, written
+// back compacted from the bucket's start (columns in bkt_col, values rounded to
+// V in out_val).
 constexpr int32_t kErrUnsupportedRow = 16;
 
-template <typename V>
+template <int S, typename V>
 __global__ void __launch_bounds__(256) op_merge_short(const int64_t *__restrict__ bucket_off, int64_t m,
                                                       int32_t *__restrict__ bkt_col,
                                                       const double *__restrict__ bkt_val, V *__restrict__ out_val,
                                                       int32_t *__restrict__ row_nnz, int32_t *__restrict__ long_rows,
                                                       int32_t *counters) {
-    const int64_t row = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + threadIdx.x / kWave;
-    if (row >= m) return;   // whole wave: no barriers in this kernel
-    const int ln = lane_id();
-    const int64_t lo = bucket_off[row];
-    const int64_t len = bucket_off[row + 1] - lo;
-    if (len > kWave) {
-        if (ln == 0) {
-            if (len > kOpRowCap) {
-                atomicOr(&counters[1], kErrUnsupportedRow);
-                row_nnz[row] = 0;
-            } else {
-                long_rows[atomicAdd(&counters[0], 1)] = static_cast<int32_t>(row);
-            }
+    static_assert(S == 32 || S == 64, "groups of 32 or 64 lanes");
+    const int64_t row = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) / S;
+    const int ln = lane_id() % S;
+    const int64_t lo = row < m ? bucket_off[row] : 0;
+    const int64_t len = row < m ? bucket_off[row + 1] - lo : 0;
+    // this kernel's rows: lengths (S/2, S] (and 0 .. S/2 too when S = 32)
+    const bool mine = row < m && len <= S && (S == 32 || len > S / 2);
+    if (S == 64 && row < m && len > S && ln == 0) {
+        if (len > kOpRowCap) {
+            atomicOr(&counters[1], kErrUnsupportedRow);
+            row_nnz[row] = 0;
+        } else {
+            long_rows[atomicAdd(&counters[0], 1)] = static_cast<int32_t>(row);
         }
-        return;
     }
-    int key = ln < len ? bkt_col[lo + ln] : 0x7fffffff;
-    double v = ln < len ? bkt_val[lo + ln] : 0.0;
-    for (int k = 2; k <= kWave; k <<= 1) {
+    // a wave without a row of this kernel is done; in the others every group takes part in the shuffles
+    if (ballot(mine) == 0ull) return;
+    int key = mine && ln < len ? bkt_col[lo + ln] : 0x7fffffff;
+    double v = mine && ln < len ? bkt_val[lo + ln] : 0.0;
+    for (int k = 2; k <= S; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            const int ok = __shfl_xor(key, j, kWave);
-            const double ov = __shfl_xor(v, j, kWave);
+            const int ok = __shfl_xor(key, j, S);
+            const double ov = __shfl_xor(v, j, S);
             const bool lower = (ln & j) == 0;
             const bool up = (ln & k) == 0;
             // the lower lane of an ascending pair keeps the smaller key
@@ -222,14 +246,16 @@ __global__ void __launch_bounds__(256) op_merge_short(const int64_t *__restrict_
             }
         }
     }
-    const int prev = __shfl_up(key, 1, kWave);
-    const bool head = ln < len && (ln == 0 || prev != key);
-    const uint64_t hm = ballot(head);
+    const int prev = __shfl_up(key, 1, S);
+    const bool head = mine && ln < len && (ln == 0 || prev != key);
+    const uint64_t hw = ballot(head);
+    const int gbase = lane_id() - ln;   // the group's first lane in the wave
+    const uint64_t hm = S == 64 ? hw : (hw >> gbase) & 0xffffffffull;
     // sum each run: a head adds the values of the lanes after it with its key
     double sum = v;
-    for (int d = 1; d < kWave; ++d) {
-        const int ok = __shfl_down(key, d, kWave);
-        const double ov = __shfl_down(v, d, kWave);
+    for (int d = 1; d < S; ++d) {
+        const int ok = __shfl_down(key, d, S);
+        const double ov = __shfl_down(v, d, S);
         const bool more = ln + d < len && ok == key;
         if (ballot(head && more) == 0ull) break;
         if (head && more) sum += ov;
@@ -239,7 +265,7 @@ __global__ void __launch_bounds__(256) op_merge_short(const int64_t *__restrict_
         bkt_col[lo + pos] = key;
         out_val[lo + pos] = static_cast<V>(sum);
     }
-    if (ln == 0) row_nnz[row] = __popcll(hm);
+    if (mine && ln == 0) row_nnz[row] = __popcll(hm);
 }
 
 // 2c. Long buckets (65 .. kOpRowCap entries), a workgroup per row, rows taken

@@ -1130,7 +1130,7 @@ wingspan_status op_count(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, 
 template <typename V>
 wingspan_status op_impl(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, const OpLayout &L, int64_t P,
                         int64_t *c_rp, int32_t *c_col, V *c_val, int64_t c_cap, int64_t *c_nnz) {
-    const int64_t K = At->nrows, m = At->ncols, n = B->ncols;
+    const int64_t K = At->nrows, m = At->ncols;
     auto at = [&](size_t off) { return c.ws + off; };
     int32_t *ctr = reinterpret_cast<int32_t *>(at(L.off_ctr));
     const int64_t *pref = reinterpret_cast<const int64_t *>(at(L.off_pref));
@@ -1161,19 +1161,21 @@ wingspan_status op_impl(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, c
     if (P > 0) {
         op_expand<V><<<static_cast<unsigned>(chunks), kOpBlock, 0, c.st>>>(
             At->row_ptr, At->col_idx, static_cast<const V *>(At->val), B->row_ptr, B->col_idx,
-            static_cast<const V *>(B->val), static_cast<int>(K), n, pref, P, part_key, part_val, part_len, row_cnt);
+            static_cast<const V *>(B->val), static_cast<int>(K), pref, P, part_key, part_val, part_len, row_cnt);
         LAUNCH_CHECK("outer expand");
     }
     // 2. coalesce: row buckets, then each bucket sorted and compacted
     wingspan_status s = run_scan(c, CountIn{row_cnt}, m, bucket);
     if (s != WINGSPAN_OK) return s;
     if (P > 0) {
-        op_bucket<<<static_cast<unsigned>(chunks), 256, 0, c.st>>>(part_key, part_val, part_len, n, bucket, row_fill,
+        op_bucket<<<static_cast<unsigned>(chunks), 256, 0, c.st>>>(part_key, part_val, part_len, bucket, row_fill,
                                                                    bkt_col, bkt_val);
         LAUNCH_CHECK("outer bucket");
     }
-    op_merge_short<V><<<blocks_for(m, 256 / kWave), 256, 0, c.st>>>(bucket, m, bkt_col, bkt_val, out_val, row_nnz,
-                                                                    long_rows, ctr);
+    op_merge_short<32, V><<<blocks_for(m, 256 / 32), 256, 0, c.st>>>(bucket, m, bkt_col, bkt_val, out_val, row_nnz,
+                                                                      long_rows, ctr);
+    op_merge_short<64, V><<<blocks_for(m, 256 / 64), 256, 0, c.st>>>(bucket, m, bkt_col, bkt_val, out_val, row_nnz,
+                                                                      long_rows, ctr);
     op_merge_long<V><<<static_cast<unsigned>(std::min<int64_t>(m, kOpLongGrid)), kOpRowBlock, 0, c.st>>>(
         bucket, bkt_col, bkt_val, out_val, row_nnz, long_rows, ctr);
     LAUNCH_CHECK("outer merge");
