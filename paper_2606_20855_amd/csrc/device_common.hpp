@@ -243,7 +243,7 @@ __device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOM
 // Per-wave LDS scratch of kMarkInts ints used by for_each_product_wg to
 // locate the A entries of blocks that span several of them. It must hold -1
 // everywhere before the first call; for_each_product_wg leaves it that way.
-constexpr int kScalarOwners = 8;      // entries per block resolved with scalar reads
+constexpr int kScalarOwners = 4;      // entries per block resolved with scalar reads (4 measured best of 4, 8, 16)
 constexpr int kMarkInts = 2 * kWave;   // short-row iteration: marks of two blocks at once
 constexpr int kMarkIntsLong = kWave;   // long-row iteration: one block at a time
 
