@@ -1130,8 +1130,10 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                         __builtin_nontemporal_store(v, &c_val[cb + pbase + i]);
                     }
                 }
+                // no barrier here: the next accumulator writes (the next slice's or row's value pass) come after
+                // the value pass's own barriers, and nothing else read or written before them is touched by the
+                // copy (the entry cache, the prefix scratch and the bitmap words are not)
                 if (threadIdx.x == 0) sclaim = 0;   // every wave has left the staging loop
-                __syncthreads();
                 r0 = r1;
                 if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
             }
