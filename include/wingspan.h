@@ -321,9 +321,9 @@ wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, co
  * once); *c_nnz (host) receives nnz(C). If nnz(C) > c_capacity it returns
  * WINGSPAN_ERR_INSUFFICIENT_CAPACITY with c_row_ptr_dev and *c_nnz valid and
  * the columns and values not written. A row of C that gathers more than 4096
- * partial entries from the workers' partial results gives
- * WINGSPAN_ERR_UNSUPPORTED (the Gustavson path takes any row). The call
- * synchronizes `stream` twice.
+ * partial entries from the workers' partial results, or more than 2^31 - 1
+ * products in all, gives WINGSPAN_ERR_UNSUPPORTED (the Gustavson path takes
+ * any row). The call synchronizes `stream` twice.
  * ------------------------------------------------------------------------ */
 wingspan_status wingspan_outer_workspace_size(const wingspan_csr *At, const wingspan_csr *B, int64_t products,
                                               size_t *bytes);

@@ -1536,6 +1536,9 @@ wingspan_status wingspan_spgemm_outer(const wingspan_csr *At, const wingspan_csr
     c.ws = static_cast<char *>(workspace_dev);
     int64_t P = 0;
     if ((s = op_count(c, At, B, L0, &P)) != WINGSPAN_OK) return s;
+    if (P > INT32_MAX)   // a row's count of partial entries is an int32
+        return fail(WINGSPAN_ERR_UNSUPPORTED, "%lld products: the outer product takes at most %d",
+                    (long long)P, INT32_MAX);
     const OpLayout L = op_plan(At, B, P);
     if (workspace_bytes < L.total)
         return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed for %lld products",
