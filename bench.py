@@ -355,13 +355,17 @@ def main():
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     if args.elementwise_only:
-        A2 = matgen.config(args.ew_workload)[0]
+        log(f"generating {args.ew_workload}")
+        A2 = matgen.matrix(args.ew_workload)
         out = dict(steps=args.steps, warmup=args.warmup)
+        log("timing SpAdd and the Hadamard product (identity and shuffled B)")
         out["elementwise"] = elementwise_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup,
                                               seed=20262)
         if not args.no_spmspv:
+            log("timing SpMSpV (x 10% stored)")
             out["spmspv"] = spmspv_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup, seed=20263)
         if not args.no_outer:
+            log("timing the outer-product SpGEMM")
             out["outer_product"] = outer_pass(ws, torch, args.outer_workload, dev, args.steps, args.warmup)
         print(json.dumps(out), flush=True)
         return
@@ -475,7 +479,7 @@ def main():
         sh["vs_two_phase_step"] = round(ms_per_step / sh["ms"], 3)
         out["sharded_single_pass"] = sh
     if not (args.no_elementwise and args.no_spmspv):
-        A2 = matgen.config(args.ew_workload)[0]
+        A2 = matgen.matrix(args.ew_workload)
         if not args.no_elementwise:
             log("timing SpAdd and the Hadamard product (identity and shuffled B)")
             out["elementwise"] = elementwise_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup,

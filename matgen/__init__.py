@@ -7,7 +7,9 @@ without sharing any code with each other.
 from .csr import CSR
 from .generators import (
     CONFIGS,
+    MATRICES,
     config,
+    matrix,
     er,
     er_rect,
     laplacian2d,
@@ -25,7 +27,9 @@ from .generators import (
 __all__ = [
     "CSR",
     "CONFIGS",
+    "MATRICES",
     "config",
+    "matrix",
     "er",
     "er_rect",
     "laplacian2d",

@@ -243,6 +243,11 @@ def _cfg_rmat20(seed=20):
     return A, A
 
 
+def _cfg_rmat22(seed=22):
+    A = rmat(22, 16, (0.57, 0.19, 0.19, 0.05), seed, np.float64, "pm1")
+    return A, A
+
+
 CONFIGS = {
     "er1000": dict(make=_cfg_er1000, seed=1, dtype="f64",
                    desc="C=A*A, Erdos-Renyi 1000x1000, 10 distinct nnz/row, fp64 U[-1,1]"),
@@ -255,6 +260,21 @@ CONFIGS = {
     "rmat20": dict(make=_cfg_rmat20, seed=20, dtype="f64",
                    desc="C=A*A, R-MAT scale 20, edge factor 16, (.57,.19,.19,.05), fp64 U[-1,1]"),
 }
+
+# Single matrices that no product is formed from: the larger input of the
+# elementwise and SpMSpV measurements.
+MATRICES = {
+    "rmat22": dict(make=_cfg_rmat22, seed=22, dtype="f64",
+                   desc="R-MAT scale 22, edge factor 16, (.57,.19,.19,.05), fp64 U[-1,1]"),
+}
+
+
+def matrix(name: str):
+    """A named workload's A: one of CONFIGS (its A) or of MATRICES."""
+    if name in CONFIGS:
+        return config(name)[0]
+    cfg = MATRICES[name]
+    return cfg["make"](cfg["seed"])[0]
 
 
 def config(name: str):
