@@ -666,20 +666,33 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
         }
         if (threadIdx.x == 0) *claim = 0;
         __syncthreads();
-        // 2. exclusive scan of the block counts; ctot[nch] = total blocks
-        if (wv == 0) {
-            int carry = 0;
-            for (int c0 = 0; c0 < nch; c0 += kWave) {
-                const int c = c0 + ln;
-                const int v = c < nch ? ctot[c] : 0;
-                const int inc = wave_incl_sum(v);
-                if (c < nch) ctot[c] = carry + inc - v;
-                carry += __builtin_amdgcn_readlane(inc, kWave - 1);
+        // 2. exclusive scan of the block counts. With fewer than 64 chunks (nearly every row) each wave scans
+        //    them itself, in registers (lane i: the first block of chunk i; lane nch: the total), and no barrier
+        //    is needed; otherwise wave 0 scans them into ctot (ctot[nch] = total blocks)
+        const bool few = nch < kWave;
+        int cpre = 0;
+        if (few) {
+            const int v = ln < nch ? ctot[ln] : 0;
+            cpre = wave_incl_sum(v) - v;
+        } else {
+            if (wv == 0) {
+                int carry = 0;
+                for (int c0 = 0; c0 < nch; c0 += kWave) {
+                    const int c = c0 + ln;
+                    const int v = c < nch ? ctot[c] : 0;
+                    const int inc = wave_incl_sum(v);
+                    if (c < nch) ctot[c] = carry + inc - v;
+                    carry += __builtin_amdgcn_readlane(inc, kWave - 1);
+                }
+                if (ln == 0) ctot[nch] = carry;
             }
-            if (ln == 0) ctot[nch] = carry;
+            __syncthreads();
         }
-        __syncthreads();
-        const int nb = uniform(ctot[nch]);
+        // first block of chunk i (i <= nch); i is uniform
+        auto first_block = [&](int i) -> int {
+            return few ? __builtin_amdgcn_readlane(cpre, i) : uniform(ctot[i]);
+        };
+        const int nb = first_block(nch);
         // a wave's chunk, held in registers, and its block range
         int c = -1, cb0 = 0, cb1 = 0;
         int boff = 0, len = 0, incl = 0, tot = 0;   // flattened blocks
@@ -690,10 +703,10 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
             while (b < e) {
                 if (b >= cb1) {
                     int cc = c < 0 ? 0 : c;
-                    while (uniform(ctot[cc + 1]) <= b) ++cc;
+                    while (first_block(cc + 1) <= b) ++cc;
                     c = cc;
-                    cb0 = uniform(ctot[c]);
-                    cb1 = uniform(ctot[c + 1]);
+                    cb0 = first_block(c);
+                    cb1 = first_block(c + 1);
                     const int a = g0 + c * kWave + ln;
                     bs = 0;
                     len = 0;
@@ -752,7 +765,7 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                 int lo = 0, hi = nch - 1;
                 while (lo < hi) {
                     const int mid = (lo + hi + 1) >> 1;
-                    if (uniform(ctot[mid]) <= b0) lo = mid;
+                    if (first_block(mid) <= b0) lo = mid;
                     else hi = mid - 1;
                 }
                 c = lo;   // run() searches forward from here
