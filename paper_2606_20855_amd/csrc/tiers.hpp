@@ -846,15 +846,15 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     const int ci = static_cast<int>(threadIdx.x);
     uint32_t bits[WROWS];
     int pk = 0, plo = 0, phi = 0;
-    double pav = 0.0;
+    V pav = V(0);   // converted where it is used, so the load need not land before the words' loads go out
     auto fetch_words = [&](int a_lo, int a_hi, int slot) {
         const uint32_t *src = cache + static_cast<int64_t>(slot) * row_words;
         const int nw0 = static_cast<int>((ncols < SH::REGION_COLS ? ncols : SH::REGION_COLS) + 31) >> 5;
         pk = 0;
-        pav = 0.0;
+        pav = V(0);
         if (ci < kCacheEntries && a_lo + ci < a_hi) {
             pk = M.a_col[a_lo + ci];
-            pav = to_d(M.a_val[a_lo + ci]);
+            pav = M.a_val[a_lo + ci];
         }
 #pragma unroll
         for (int q = 0; q < WROWS; ++q) {
@@ -917,7 +917,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 if (rg0 == 0) {
                     // prefetched
                     k = pk;
-                    av = pav;
+                    av = to_d(pav);
                     lo = plo;
                     hi = phi;
                 } else {
@@ -969,16 +969,22 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 for (int q = 0; q < WROWS; ++q) bits[q] = bw[wbase + q * kWave + ln].x;
             }
             // 2. exclusive popcount prefix (lane-contiguous rows, so free of bank conflicts); each word is
-            //    stored with its prefix
+            //    stored with its prefix. A 64-word row holds at most 2048 columns, so two rows' counts share
+            //    one scan as the 16-bit halves of a word; the wave's total comes from the same scans.
             {
+                static_assert(WROWS % 2 == 0 && kWave * 32 < 65536, "rows scanned in pairs of 16-bit counts");
                 uint32_t cnt[WROWS];
+                uint32_t inc2[WROWS / 2];
                 int wtot = 0;
 #pragma unroll
-                for (int q = 0; q < WROWS; ++q) {
-                    cnt[q] = __popc(bits[q]);
-                    wtot += static_cast<int>(cnt[q]);
+                for (int q = 0; q < WROWS; ++q) cnt[q] = __popc(bits[q]);
+#pragma unroll
+                for (int h = 0; h < WROWS / 2; ++h) {
+                    inc2[h] = static_cast<uint32_t>(
+                        wave_incl_sum(static_cast<int>(cnt[2 * h] | (cnt[2 * h + 1] << 16))));
+                    const uint32_t t = __builtin_amdgcn_readlane(inc2[h], kWave - 1);
+                    wtot += static_cast<int>((t & 0xffffu) + (t >> 16));
                 }
-                wtot = __builtin_amdgcn_readlane(wave_incl_sum(wtot), kWave - 1);
                 if (ln == 0) scratch[wv] = wtot;
                 if (threadIdx.x == 0 && rg0 == 0) s_next = claimed;
                 __syncthreads();
@@ -986,11 +992,15 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
 #pragma unroll
                 for (int i = 0; i < NW; ++i) run += i < wv ? scratch[i] : 0;
 #pragma unroll
-                for (int q = 0; q < WROWS; ++q) {
-                    const int inc = wave_incl_sum(static_cast<int>(cnt[q]));
-                    bw[wbase + q * kWave + ln] =
-                        make_uint2(bits[q], static_cast<uint32_t>(run + inc - static_cast<int>(cnt[q])));
-                    run += __builtin_amdgcn_readlane(inc, kWave - 1);
+                for (int h = 0; h < WROWS / 2; ++h) {
+                    const uint32_t t = __builtin_amdgcn_readlane(inc2[h], kWave - 1);
+                    const int lo = static_cast<int>(inc2[h] & 0xffffu), hi = static_cast<int>(inc2[h] >> 16);
+                    bw[wbase + 2 * h * kWave + ln] =
+                        make_uint2(bits[2 * h], static_cast<uint32_t>(run + lo - static_cast<int>(cnt[2 * h])));
+                    run += static_cast<int>(t & 0xffffu);
+                    bw[wbase + (2 * h + 1) * kWave + ln] = make_uint2(
+                        bits[2 * h + 1], static_cast<uint32_t>(run + hi - static_cast<int>(cnt[2 * h + 1])));
+                    run += static_cast<int>(t >> 16);
                 }
             }
             if (rg0 == 0) {
