@@ -1099,7 +1099,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                             int cv[kStageStep];
 #pragma unroll
                             for (int q = 0; q < kStageStep; ++q) {
-                                cv[q] = cbase + __builtin_ctz(wbits | 0x80000000u);
+                                // unspecified once wbits is empty (q >= n - i), and then never written
+                                cv[q] = cbase + __builtin_ctz(wbits);
                                 wbits &= wbits - 1u;
                             }
                             if constexpr (SH::PACKED) {
