@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define WINGSPAN_ABI_VERSION 3
+#define WINGSPAN_ABI_VERSION 4
 
 typedef enum { WINGSPAN_F32 = 0, WINGSPAN_F64 = 1 } wingspan_dtype;
 
@@ -93,6 +93,9 @@ typedef struct {
                                the LDS hash tables */
     int32_t timing;         /* 1: time each tier's kernels with HIP events on `stream`
                                (the call then synchronizes the stream before returning) */
+    int32_t wide_offsets;   /* 1: the dense tier forms B's entry offsets in 64 bits even
+                               where 32 bits hold them (the path B takes when nnz(B) times
+                               the value size exceeds 2^32); a test switch, results equal */
 } wingspan_options;
 
 /* Tiers a row can be assigned to. */

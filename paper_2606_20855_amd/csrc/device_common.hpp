@@ -279,7 +279,19 @@ struct TwoPhaseVisit {};
 // so the step's loads are issued back to back and waited for once.
 constexpr int kSpanBlocks = 4;
 
-template <typename V, bool VALUES, bool LONG, typename Visit>
+// base[ix] for ix >= 0. With OFF32 the element's byte offset is formed in 32
+// bits (one shift, and the load takes the base from scalar registers), which
+// the caller may ask for only when every offset it uses is below 2^32.
+template <bool OFF32, typename T>
+__device__ __forceinline__ T load_at(const T *__restrict__ base, int ix) {
+    if constexpr (OFF32)
+        return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(base) +
+                                            static_cast<uint32_t>(ix) * static_cast<uint32_t>(sizeof(T)));
+    else
+        return base[ix];
+}
+
+template <typename V, bool VALUES, bool LONG, bool OFF32, typename Visit>
 __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int incl, int tot, int lb0, int lb1,
                                              const int32_t *__restrict__ b_col, const V *__restrict__ b_val,
                                              int32_t *mark, Visit &visit) {
@@ -431,8 +443,8 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
         V vraw[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            craw[u] = b_col[ix[u]];
-            if (VALUES) vraw[u] = b_val[ix[u]];
+            craw[u] = load_at<OFF32>(b_col, ix[u]);
+            if (VALUES) vraw[u] = load_at<OFF32>(b_val, ix[u]);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -603,14 +615,15 @@ struct has_cached_bounds<R, std::void_t<decltype(std::declval<const R &>().cache
 // LONG also selects the general-step shape (see chunk_blocks). ALIGNED (for
 // visits over whole B rows, where slices are long) replaces the flattening by
 // entry-aligned blocks (see chunk_blocks_aligned): more blocks, but never a
-// block shared by two entries.
+// block shared by two entries. OFF32 (see load_at) forms the general steps' B
+// offsets in 32 bits: only for B with nnz * sizeof(V) <= 2^32.
 // All threads of the workgroup must call it. ctot holds kCtotInts ints of LDS.
 constexpr int kMaxChunks = 256;
 constexpr int kCtotInts = kMaxChunks + 2;   // block offsets, total, claim counter
 constexpr int kUnitBlocks = 4;
 
-template <int BLOCK, typename V, bool VALUES, bool LONG = false, bool ALIGNED = false, typename RangeF,
-          typename Visit>
+template <int BLOCK, typename V, bool VALUES, bool LONG = false, bool ALIGNED = false, bool OFF32 = false,
+          typename RangeF, typename Visit>
 __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ a_col,
                                                     const V *__restrict__ a_val, int a_lo, int a_hi,
                                                     RangeF range, const int32_t *__restrict__ b_col,
@@ -735,7 +748,7 @@ __device__ __forceinline__ void for_each_product_wg(const int32_t *__restrict__ 
                 if constexpr (ALIGNED)
                     chunk_blocks_aligned<V, VALUES>(bs, av, len, bstart, nblk, b - cb0, ee - cb0, b_col, b_val, visit);
                 else
-                    chunk_blocks<V, VALUES, LONG>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark,
+                    chunk_blocks<V, VALUES, LONG, OFF32>(boff, av, len, incl, tot, b - cb0, ee - cb0, b_col, b_val, mark,
                                                   visit);
                 b = ee;
             }

@@ -709,14 +709,15 @@ struct RankAccumulate : TwoPhaseVisit {
     const uint2 *bw;
     double *acc;
     int col0, r0, r1;
+    // the column's rank relative to r0 (outside [0, r1 - r0) when the slice does not hold it)
     __device__ __forceinline__ int pre(int col) const {
         const int rel = col - col0;
         const uint2 e = bw[rel >> 5];
-        const int r = static_cast<int>(e.y) + __popc(e.x & ((1u << (rel & 31)) - 1u));
-        return (r >= r0 && r < r1) ? r - r0 : -1;
+        return static_cast<int>(e.y) + __popc(e.x & ((1u << (rel & 31)) - 1u)) - r0;
     }
+    // one unsigned compare keeps the slice's ranks and drops the rest, -1 included
     __device__ __forceinline__ void post(int k, double prod) const {
-        if (k >= 0) atomicAdd(&acc[k], prod);
+        if (static_cast<uint32_t>(k) < static_cast<uint32_t>(r1 - r0)) atomicAdd(&acc[k], prod);
     }
     __device__ __forceinline__ int safe_col() const { return col0; }
     __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
@@ -794,7 +795,9 @@ __device__ __forceinline__ int opaque_zero() {
 // A and B) instead of running the structure pass.
 // POOL selects the output: CSR at C.row_ptr, or pool segments claimed through
 // the sink (compiled apart, so the CSR kernel carries none of the pool state).
-template <typename V, bool POOL>
+// OFF32: B's offsets in the value passes' general steps are formed in 32 bits,
+// for B with nnz * sizeof(V) <= 2^32 (the launch checks).
+template <typename V, bool POOL, bool OFF32>
 __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     Mats<V> M, const RankRow *__restrict__ rr, int nrows, const int32_t *__restrict__ wtab, int nwin, int64_t ncols,
     RowSink out, int32_t *__restrict__ c_col, V *__restrict__ c_val, Control *ctrl,
@@ -1043,7 +1046,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 // values
                 const int lo_from = j == pj ? 0 : j == pj2 ? 1 : 2;
                 const int hi_from = j2 == pj2 ? 0 : j2 == nwr ? 1 : 2;
-                for_each_product_wg<BLOCK, V, true, true>(
+                for_each_product_wg<BLOCK, V, true, true, false, OFF32>(
                     M.a_col, M.a_val, a_lo, a_hi,
                     SliceRange{wtab, stride, rg0 + j, rg0 + j2, lo_from, hi_from, e_bs, e_len, e_hi}, M.b_col,
                     M.b_val, mark, ctot, RankAccumulate{{}, bw, acc, static_cast<int>(col0), r0, r1}, ecache);

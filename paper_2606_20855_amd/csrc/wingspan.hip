@@ -86,6 +86,7 @@ struct Opts {
     bool validate = false;
     bool force_spill = false;
     bool timing = false;
+    bool wide_offsets = false;
     bool dense_disabled = false;
     int hash_log2_max_sym = kHashLog2MaxSym;
     int hash_log2_max_num = kHashLog2MaxNum;
@@ -105,6 +106,7 @@ wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
         r.validate = o->validate != 0;
         r.force_spill = o->force_spill != 0;
         r.timing = o->timing != 0;
+        r.wide_offsets = o->wide_offsets != 0;
         if (o->max_lds_slots != 0) {
             const int32_t s = o->max_lds_slots;
             if (s < 64 || s > (1 << 14) || (s & (s - 1)) != 0)
@@ -461,6 +463,13 @@ void fill_stats(const Ctx &c, int phase) {
     st.total_products = c.host.total_products;
 }
 
+// Whether every byte offset of B's columns and values fits in 32 bits, so the
+// rank kernel may form its B offsets in 32 bits.
+template <typename V>
+bool offsets_fit_32(const wingspan_csr *B) {
+    return B->nnz <= (int64_t(1) << 32) / static_cast<int64_t>(sizeof(V));
+}
+
 // Workgroups of the persistent rank kernel: one per compute unit of the
 // current device (its LDS use allows no second), or fewer when there are fewer
 // rows.
@@ -710,9 +719,13 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, c_rp,
                                                             cached ? c.slot_of_row : nullptr, c.rrows);
         LAUNCH_CHECK("rank rows");
-        dense_rank_kernel<V, false><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
-            M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl, cached ? c.cache : nullptr,
-            c.L.row_words);
+        const uint32_t *cache = cached ? c.cache : nullptr;
+        if (!c.o.wide_offsets && offsets_fit_32<V>(B))
+            dense_rank_kernel<V, false, true><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+                M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl, cache, c.L.row_words);
+        else
+            dense_rank_kernel<V, false, false><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+                M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, c_col, c_val, c.ctrl, cache, c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense rank numeric");
     } else if (cnt) {
@@ -810,8 +823,14 @@ wingspan_status sharded_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, nullptr, nullptr,
                                                             c.rrows);
         LAUNCH_CHECK("rank rows");
-        dense_rank_kernel<V, true><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
-            M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr, c.L.row_words);
+        if (!c.o.wide_offsets && offsets_fit_32<V>(B))
+            dense_rank_kernel<V, true, true><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+                M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr,
+                c.L.row_words);
+        else
+            dense_rank_kernel<V, true, false><<<rank_grid(cnt), RankShape<V>::BLOCK, 0, c.st>>>(
+                M, c.rrows, cnt, c.wtab, c.L.nwin, B->ncols, sink, pool_col, pool_val, c.ctrl, nullptr,
+                c.L.row_words);
         stats.launches[WINGSPAN_TIER_DENSE]++;
         LAUNCH_CHECK("dense rank single pass");
     }

@@ -44,13 +44,13 @@ def test_library_exports_every_header_function():
 
 
 def test_abi_version():
-    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 3
+    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 4
 
 
 def test_struct_layouts_match_header():
     # sizes the C side sees (x86-64 SysV)
     assert ctypes.sizeof(ws.wingspan_csr) == 48
-    assert ctypes.sizeof(ws.wingspan_options) == 32
+    assert ctypes.sizeof(ws.wingspan_options) == 36
     assert ctypes.sizeof(ws.wingspan_phase_stats) == 4 * 8 * 4 + 4 * 4 + 4 * 4 + 4 + 4 + 8 + 8 + 8
 
 

@@ -154,3 +154,18 @@ def test_long_rows_cached_and_fresh(dtype):
     got2, num2 = _numeric(dA, dB, c_rp, nnz, fresh, nbytes, {})
     assert num2["structure_cache_rows"] == 0
     assert_matches(got2, ref, A.val.dtype, what="long rows, fresh")
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+def test_wide_offsets_path(dtype):
+    # the rank kernel forms B's offsets in 32 bits unless nnz(B) * sizeof(value) exceeds 2^32; the switch
+    # takes the 64-bit path on a small B, which must give the same C
+    A = matgen.rmat(11, 16, seed=59, dtype=dtype, dist="open01" if dtype == np.float32 else "pm1")
+    dA = _dev(A)
+    ref = oracle.spgemm(A, A)
+    for opts in (DENSE, dict(DENSE, wide_offsets=1)):
+        wsb, nbytes = _workspace(dA, dA, opts)
+        c_rp, nnz = _symbolic(dA, dA, wsb, nbytes, opts)
+        got, num = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, opts)
+        assert num["rows"]["dense"] > 0
+        assert_matches(got, ref, A.val.dtype, what=f"offsets {opts}")
