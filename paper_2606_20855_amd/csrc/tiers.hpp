@@ -713,7 +713,9 @@ struct RankAccumulate : TwoPhaseVisit {
     __device__ __forceinline__ int pre(int col) const {
         const int rel = col - col0;
         const uint2 e = bw[rel >> 5];
-        return static_cast<int>(e.y) + __popc(e.x & ((1u << (rel & 31)) - 1u)) - r0;
+        // the bits below the column's own: a bit-field extract of width rel mod 32 (the instruction takes the
+        // width's low five bits itself)
+        return static_cast<int>(e.y) + __popc(__builtin_amdgcn_ubfe(e.x, 0u, static_cast<uint32_t>(rel))) - r0;
     }
     // one unsigned compare keeps the slice's ranks and drops the rest, -1 included
     __device__ __forceinline__ void post(int k, double prod) const {
