@@ -84,11 +84,12 @@ def test_random(shape, density, dtype):
 
 @pytest.mark.parametrize("dtype", [np.float32, np.float64])
 @pytest.mark.parametrize("opts", [None, dict(tiny_max=-1), dict(max_lds_slots=64), dict(force_spill=1),
-                                  dict(max_lds_slots=64, dense_min_nnz=-1)])
+                                  dict(max_lds_slots=64, dense_min_nnz=-1), dict(max_lds_slots=64, wide_offsets=1)])
 def test_tiers_rmat(opts, dtype):
     # R-MAT scale 11: rows from a handful of products to thousands, so every
     # tier writes to the pool; max_lds_slots=64 sends most rows to the rank
-    # kernel, dense_min_nnz=-1 (no dense tier) to the spill tier
+    # kernel (with wide_offsets, its instantiation for B too large for 32-bit
+    # offsets), dense_min_nnz=-1 (no dense tier) to the spill tier
     A = matgen.rmat(11, 16, seed=61, dtype=dtype, dist="open01" if dtype == np.float32 else "pm1")
     S, st, ref = check(A, A, opts, what=f"rmat11 {opts}")
     if opts and opts.get("max_lds_slots") == 64 and "dense_min_nnz" not in opts:
