@@ -2,11 +2,12 @@
  * wingspan.h -- C ABI of the MI355X (gfx950) sparse-times-sparse matrix
  * multiply C = A * B with CSR inputs and a CSR output (SpGEMM).
  *
- * The operation is the one the WingSpan paper benchmarks in Section 5.1
- * ("the matrix product C = A*B where A, B and C are all sparse"), computed
- * row by row with Gustavson's algorithm (Section 5.1, the four SpGEMM
- * programs figure: for each output fiber, accumulate a * b into a workspace,
- * then copy the workspace into the output fiber in coordinate order).
+ * The operation is the one the WingSpan paper benchmarks in Section 5.1: the
+ * product of two sparse matrices whose result is stored sparse as well,
+ * computed row by row with Gustavson's algorithm (Section 5.1, the four
+ * SpGEMM programs figure: for each output fiber, accumulate a * b into a
+ * workspace, then copy the workspace into the output fiber in coordinate
+ * order).
  *
  * C[i,j] = sum over stored entries A[i,k], B[k,j] of A[i,k] * B[k,j].
  * The pattern of C is structural: (i, j) is stored whenever at least one
@@ -171,6 +172,18 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
                                 int64_t c_capacity, int64_t *c_nnz,
                                 void *workspace_dev, size_t workspace_bytes,
                                 void *stream, const wingspan_options *options);
+
+/* Per-row product counts: row_products_dev[i] (int64, A.nrows entries, written
+ * by the library) receives the number of scalar products A[i,k] * B[k,j] that
+ * Gustavson's loop forms for row i (Section 5.1, the SpGEMM programs figure:
+ * one multiply per stored A[i,k] and stored B[k,j]), i.e. the sum over the
+ * entries (i, k) of A of the length of row k of B. These are the counts both
+ * phases bin the rows by, from the same kernels. Takes the workspace
+ * wingspan_spgemm_workspace_size() gives for (A, B) with default options;
+ * asynchronous on `stream`. A.val and B.val are not read. */
+wingspan_status wingspan_spgemm_row_products(const wingspan_csr *A, const wingspan_csr *B,
+                                             int64_t *row_products_dev, void *workspace_dev,
+                                             size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Single pass with sharded output.

@@ -116,10 +116,14 @@ def row_products(A, B, rows=None, lib=None) -> np.ndarray:
     return out
 
 
-def spgemm(A, B, rows=None, with_mag: bool = True, lib=None) -> OracleResult:
+def spgemm(A, B, rows=None, with_mag: bool = True, lib=None, capacity: Optional[int] = None) -> OracleResult:
     """C = A * B restricted to `rows` of A (default: all rows, in order).
 
-    `lib` selects another build of the oracle (used by the mutation test)."""
+    `lib` selects another build of the oracle (used by the mutation test).
+    Without `capacity` the oracle runs twice (a counting pass sizes the
+    output); with it, the output arrays are allocated at that many entries and
+    the oracle runs once (an upper bound of nnz is the sum over the rows of
+    min(products of the row, B.ncols)); a capacity that is too small raises."""
     if A.ncols != B.nrows:
         raise ValueError("A.ncols != B.nrows")
     if A.val.dtype != B.val.dtype:
@@ -132,14 +136,22 @@ def spgemm(A, B, rows=None, with_mag: bool = True, lib=None) -> OracleResult:
     rp = np.zeros(len(rows) + 1, dtype=np.int64)
     args = (B.ncols, _ptr(arp), _ptr(aci), _ptr(av), _ptr(brp), _ptr(bci), _ptr(bv), dt,
             _ptr(rows), len(rows))
-    nnz = lib.oracle_spgemm_rows(*args, _ptr(rp), None, None, None, 0)
-    if nnz < 0:
-        raise RuntimeError(f"oracle: {_ERRORS.get(nnz, nnz)}")
-    col = np.zeros(nnz, dtype=np.int32)
-    val = np.zeros(nnz, dtype=A.val.dtype)
-    mag = np.zeros(nnz, dtype=np.float64) if with_mag else None
-    got = lib.oracle_spgemm_rows(*args, _ptr(rp), _ptr(col), _ptr(val), _ptr(mag), nnz)
-    if got != nnz:
+    if capacity is None:
+        nnz = lib.oracle_spgemm_rows(*args, _ptr(rp), None, None, None, 0)
+        if nnz < 0:
+            raise RuntimeError(f"oracle: {_ERRORS.get(nnz, nnz)}")
+        cap = nnz
+    else:
+        cap = int(capacity)
+    col = np.zeros(max(cap, 1), dtype=np.int32)
+    val = np.zeros(max(cap, 1), dtype=A.val.dtype)
+    mag = np.zeros(max(cap, 1), dtype=np.float64) if with_mag else None
+    got = lib.oracle_spgemm_rows(*args, _ptr(rp), _ptr(col), _ptr(val), _ptr(mag), cap)
+    if got < 0 or (capacity is None and got != cap):
         raise RuntimeError(f"oracle: {_ERRORS.get(got, got)}")
+    nnz = got
+    col, val = col[:nnz], val[:nnz]
+    if with_mag:
+        mag = mag[:nnz]
     prods = row_products(A, B, rows, lib=lib)
     return OracleResult(rp, col, val, mag if with_mag else np.zeros(0), prods)

@@ -1,7 +1,6 @@
 /*
  * Test infrastructure only -- the CPU oracle for C = A * B with A, B and C all
- * sparse (Section 5.1 of the WingSpan paper: "the matrix product C = A*B where
- * A, B and C are all sparse").
+ * sparse, the sparse matrix product of Section 5.1 of the WingSpan paper.
  *
  * Nothing in the GPU library includes, links or calls this file. Only the
  * tests, the smoke check and the benchmark's CPU-baseline leg load it. It is

@@ -112,6 +112,22 @@ __global__ void __launch_bounds__(kScanBlock) scan_tiles(In in, int64_t n, const
     if (blockIdx.x == 0 && threadIdx.x == 0) out[n] = partials[nb];
 }
 
+// Products of row i of A: with pref the exclusive prefix of B-row lengths
+// over A's entries, the row's entries [a_rp[i], a_rp[i+1]) select B rows whose
+// lengths sum to pref[a_rp[i+1]] - pref[a_rp[i]].
+__device__ __forceinline__ int64_t row_products_of(const int32_t *__restrict__ a_rp,
+                                                   const int64_t *__restrict__ pref, int64_t i) {
+    return pref[a_rp[i + 1]] - pref[a_rp[i]];
+}
+
+// out[i] = products of row i, for every row (the counts the binning uses).
+__global__ void __launch_bounds__(256) row_products_kernel(const int32_t *__restrict__ a_rp,
+                                                           const int64_t *__restrict__ pref, int64_t m,
+                                                           int64_t *__restrict__ out) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < m) out[i] = row_products_of(a_rp, pref, i);
+}
+
 // ---------------------------------------------------------------------------
 // Binning.
 // ---------------------------------------------------------------------------
@@ -179,7 +195,7 @@ __global__ void __launch_bounds__(256) bin_count(const int32_t *__restrict__ a_r
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i < m) {
         const int32_t a0 = a_rp[i], a1 = a_rp[i + 1];
-        const int64_t f = pref[a1] - pref[a0];
+        const int64_t f = row_products_of(a_rp, pref, i);
         const int64_t c = cfg.numeric ? (c_rp[i + 1] - c_rp[i]) : 0;
         int64_t bound;
         const int b = choose_bin(f, c, cfg, &bound);
@@ -226,7 +242,7 @@ __global__ void __launch_bounds__(256) bin_scatter(const int32_t *__restrict__ a
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     int b = -1, r = 0;
     if (i < m) {
-        const int64_t f = pref[a_rp[i + 1]] - pref[a_rp[i]];
+        const int64_t f = row_products_of(a_rp, pref, i);
         const int64_t c = cfg.numeric ? (c_rp[i + 1] - c_rp[i]) : 0;
         int64_t bound;
         b = choose_bin(f, c, cfg, &bound);

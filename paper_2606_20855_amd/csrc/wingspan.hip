@@ -178,7 +178,11 @@ struct Layout {
     int nslab;
 };
 
-Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
+// budget > 0: the layout must fit `budget` bytes (the static scratch of the
+// entry point that allocates nothing): no structure cache, and the spill pool
+// takes what the other arrays leave, at least one slab. total > budget means
+// the problem does not fit.
+Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o, size_t budget = 0) {
     Layout L{};
     const int64_t m = A->nrows, n = B->ncols, nnz_a = A->nnz;
     size_t off = 0;
@@ -212,12 +216,16 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o) {
     L.slab_cap = std::min(kMaxSlabCap, std::max<int64_t>(64, next_pow2(2 * std::max<int64_t>(n, 1))));
     const int64_t slab_bytes = L.slab_cap * 12;
     L.nslab = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxSlabs, kPoolBytes / slab_bytes)));
+    if (budget > 0) {
+        const int64_t left = budget > off ? static_cast<int64_t>(budget - off) : 0;
+        L.nslab = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(L.nslab, left / slab_bytes)));
+    }
     off += align_up(static_cast<size_t>(slab_bytes) * L.nslab);
     // structure cache: the symbolic phase's column bitmaps of dense rows, reused by the rank-indexed numeric
     // kernel; rows beyond kStructCacheBytes run their own structure pass
     L.cache_rows = 0;
     L.row_words = 0;
-    if (L.rank_mode && L.nwin > 0 && !o.dense_disabled && n > 0 && n <= kBitmapMaxCols && m > 0) {
+    if (budget == 0 && L.rank_mode && L.nwin > 0 && !o.dense_disabled && n > 0 && n <= kBitmapMaxCols && m > 0) {
         L.row_words = (n + 31) / 32;
         L.row_words = (L.row_words + 63) / 64 * 64;
         L.cache_rows = std::min<int64_t>(m, kStructCacheBytes / (L.row_words * 4));
@@ -876,10 +884,10 @@ wingspan_status finish_timing(int phase) {
 }
 
 wingspan_status setup(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, const wingspan_options *opt,
-                      void *ws, size_t ws_bytes, void *stream) {
+                      void *ws, size_t ws_bytes, void *stream, size_t budget = 0) {
     wingspan_status s = parse_opts(opt, &c.o);
     if (s != WINGSPAN_OK) return s;
-    c.L = plan(A, B, c.o);
+    c.L = plan(A, B, c.o, budget);
     if (ws_bytes < c.L.total)
         return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", ws_bytes, c.L.total);
     if (!ws) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "workspace is NULL");
@@ -1250,12 +1258,12 @@ wingspan_status wingspan_spgemm_workspace_size(const wingspan_csr *A, const wing
 
 static wingspan_status symbolic_entry(const wingspan_csr *A, const wingspan_csr *B, int64_t *c_row_ptr_dev,
                                       int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes, void *stream,
-                                      const wingspan_options *options, Ctx &c) {
+                                      const wingspan_options *options, Ctx &c, size_t budget = 0) {
     wingspan_status s = check_pair(A, B);
     if (s != WINGSPAN_OK) return s;
     if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
     if (!c_nnz) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_nnz is NULL");
-    if ((s = setup(c, A, B, options, workspace_dev, workspace_bytes, stream)) != WINGSPAN_OK) return s;
+    if ((s = setup(c, A, B, options, workspace_dev, workspace_bytes, stream, budget)) != WINGSPAN_OK) return s;
     if ((s = timer_begin(c.o.timing)) != WINGSPAN_OK) return s;
     if ((s = symbolic_impl(c, A, B, c_row_ptr_dev, c_nnz)) != WINGSPAN_OK) return s;
     return finish_timing(0);
@@ -1320,6 +1328,23 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
         return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_col_idx_dev or c_val_dev is NULL");
     return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, workspace_dev, workspace_bytes,
                          stream, options, true, c);
+}
+
+wingspan_status wingspan_spgemm_row_products(const wingspan_csr *A, const wingspan_csr *B,
+                                             int64_t *row_products_dev, void *workspace_dev, size_t workspace_bytes,
+                                             void *stream) {
+    g_err.clear();
+    wingspan_status s = check_pair(A, B);
+    if (s != WINGSPAN_OK) return s;
+    if (A->nrows > 0 && !row_products_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "row_products_dev is NULL");
+    Ctx c{};
+    if ((s = setup(c, A, B, nullptr, workspace_dev, workspace_bytes, stream)) != WINGSPAN_OK) return s;
+    if (A->nrows == 0) return WINGSPAN_OK;
+    // the analysis pass of both phases: B-row lengths scanned over A's entries, then per-row differences
+    if ((s = run_scan(c, BRowLenIn{A->col_idx, B->row_ptr}, A->nnz, c.pref)) != WINGSPAN_OK) return s;
+    row_products_kernel<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, A->nrows, row_products_dev);
+    LAUNCH_CHECK("row products");
+    return WINGSPAN_OK;
 }
 
 wingspan_status wingspan_spgemm_sharded(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,

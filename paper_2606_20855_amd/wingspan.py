@@ -118,6 +118,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wingspan_spgemm_numeric.restype = i32
     lib.wingspan_spgemm.argtypes = [csr_p, csr_p, i32, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
     lib.wingspan_spgemm.restype = i32
+    lib.wingspan_spgemm_row_products.argtypes = [csr_p, csr_p, vp, vp, sz, vp]
+    lib.wingspan_spgemm_row_products.restype = i32
     lib.wingspan_spgemm_sharded.argtypes = [csr_p, csr_p, i32, vp, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
     lib.wingspan_spgemm_sharded.restype = i32
     lib.wingspan_sharded_to_csr_workspace_size.argtypes = [i64, P(sz)]
@@ -152,6 +154,7 @@ EXPORTED = (
     "wingspan_spgemm_symbolic",
     "wingspan_spgemm_numeric",
     "wingspan_spgemm",
+    "wingspan_spgemm_row_products",
     "wingspan_spgemm_sharded",
     "wingspan_sharded_to_csr_workspace_size",
     "wingspan_sharded_to_csr",
@@ -239,6 +242,12 @@ def wingspan_spgemm(A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int
                                   c_capacity, ctypes.byref(nnz), workspace, workspace_bytes, stream or None,
                                   _opt_ptr(options)))
     return nnz.value
+
+
+def wingspan_spgemm_row_products(A: wingspan_csr, B: wingspan_csr, row_products: int, workspace: int,
+                                 workspace_bytes: int, stream: int = 0) -> None:
+    _check(load().wingspan_spgemm_row_products(ctypes.byref(A), ctypes.byref(B), row_products or None, workspace,
+                                               workspace_bytes, stream or None))
 
 
 def wingspan_spgemm_sharded(A: wingspan_csr, B: wingspan_csr, dtype: int, row_off: int, row_nnz: int,
@@ -422,6 +431,16 @@ def spgemm(A: DeviceCSR, B: DeviceCSR, options=None, stream=None, workspace=None
     wingspan_spgemm_numeric(Ad, Bd, A.dtype_code, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
                             ws.data_ptr(), nbytes, h, options)
     return DeviceCSR(A.nrows, B.ncols, c_rp, c_col[:nnz], c_val[:nnz])
+
+
+def row_products(A: DeviceCSR, B: DeviceCSR, stream=None):
+    """Per-row product counts of C = A * B on the GPU (int64 device tensor)."""
+    import torch
+    dev = A.row_ptr.device
+    ws, nbytes = allocate_workspace(A, B)
+    out = torch.empty(max(A.nrows, 1), dtype=torch.int64, device=dev)
+    wingspan_spgemm_row_products(A.desc(), B.desc(), out.data_ptr(), ws.data_ptr(), nbytes, _stream_handle(stream))
+    return out[:A.nrows]
 
 
 @dataclass

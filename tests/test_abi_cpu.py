@@ -289,3 +289,20 @@ def test_outer_argument_errors():
                        ((At, desc(9, 15, -2), ws.F64, FAKE, FAKE, FAKE, 10, FAKE, full), "WINGSPAN_ERR_INVALID_ARGUMENT")]:
         got, _ = status_of(ws.wingspan_spgemm_outer, *args)
         assert got == code, args
+
+
+def test_row_products_argument_errors():
+    A, B = desc(10, 12, 5), desc(12, 7, 9)
+    need = ws.wingspan_spgemm_workspace_size(A, B, ws.F64)
+    got, _ = status_of(ws.wingspan_spgemm_row_products, A, desc(11, 7, 9), FAKE, FAKE, need)
+    assert got == "WINGSPAN_ERR_DIMENSION_MISMATCH"
+    for args, code in [((A, B, 0, FAKE, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((A, B, FAKE, FAKE, need - 1), "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"),
+                       ((A, B, FAKE, 0, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((A, B, FAKE, FAKE + 8, need), "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                       ((desc(10, 12, 2**31), B, FAKE, FAKE, need), "WINGSPAN_ERR_INDEX_OVERFLOW")]:
+        got, _ = status_of(ws.wingspan_spgemm_row_products, *args)
+        assert got == code, args
+    # an A without rows may pass a NULL output (it then stops at the workspace check)
+    got, _ = status_of(ws.wingspan_spgemm_row_products, desc(0, 12, 0, col=0, val=0), B, 0, FAKE, 0)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"

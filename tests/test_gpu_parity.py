@@ -9,7 +9,7 @@ import pytest
 
 import matgen
 import oracle
-from gpu_util import assert_matches, golden, row_ptr_sha256, run_gpu
+from gpu_util import assert_matches, golden, gpu_row_products, row_ptr_sha256, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -20,6 +20,8 @@ def check(A, B, options=None, what=""):
     assert_matches(got, ref, A.val.dtype, what=what or str(options))
     assert sym["total_products"] == int(ref.products.sum())
     assert num["c_nnz_total"] == ref.nnz
+    # the analysis pass's per-row product counts, row by row (the counts the rows are binned by)
+    assert np.array_equal(gpu_row_products(A, B), ref.products), f"{what}: per-row product counts differ"
     return got, sym, num, ref
 
 

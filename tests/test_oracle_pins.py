@@ -293,6 +293,23 @@ def test_row_subset_matches_full():
         assert full.products[i] == sub.products[s]
 
 
+def test_single_pass_capacity_mode_matches_counting_mode():
+    # the binding's one-call mode (output sized by a bound) returns the same rows as the counting mode; a bound
+    # that is too small is refused rather than truncated
+    A = matgen.rmat(9, 16, seed=11, dtype=np.float32)
+    full = oracle.spgemm(A, A)
+    rows = np.arange(100, 400, dtype=np.int64)
+    bound = int(np.minimum(oracle.row_products(A, A, rows), A.ncols).sum())
+    one = oracle.spgemm(A, A, rows=rows, capacity=bound)
+    two = oracle.spgemm(A, A, rows=rows)
+    for f in ("row_ptr", "col_idx", "val", "mag", "products"):
+        assert np.array_equal(getattr(one, f), getattr(two, f)), f
+    a, b = full.row_ptr[100], full.row_ptr[400]
+    assert np.array_equal(one.col_idx, full.col_idx[a:b])
+    with pytest.raises(RuntimeError):
+        oracle.spgemm(A, A, rows=rows, capacity=two.nnz - 1)
+
+
 def test_invariants_rmat_small():
     A = matgen.rmat(10, 16, seed=3, dtype=np.float32)
     assert A.is_canonical()
