@@ -173,6 +173,35 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
                                 void *workspace_dev, size_t workspace_bytes,
                                 void *stream, const wingspan_options *options);
 
+/* ------------------------------------------------------------------------
+ * wingspan_spgemm without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).
+ *
+ * Same arguments, results and errors as wingspan_spgemm, minus the workspace:
+ * the scratch comes from a static device array of
+ * WINGSPAN_NOALLOC_SCRATCH_BYTES in the library itself, one per device, held
+ * from the library's first use on that device until the process ends. The
+ * call allocates nothing (no hipMalloc, no library allocation). The scratch
+ * holds no structure cache (the numeric phase computes its dense rows'
+ * column sets itself) and a spill pool sized to what the other arrays leave.
+ * A product whose scratch would exceed WINGSPAN_NOALLOC_SCRATCH_BYTES returns
+ * WINGSPAN_ERR_WORKSPACE_TOO_SMALL before any HIP call; wingspan_spgemm with
+ * a caller-owned workspace takes it. options->timing is refused
+ * (WINGSPAN_ERR_INVALID_ARGUMENT): its events would be allocated.
+ *
+ * All calls on one device share that device's scratch, and each call leaves
+ * its contents behind: calls that overlap in time on one device (two host
+ * threads, or two streams) race and their results are undefined. Serialize
+ * them. The call synchronizes `stream` as wingspan_spgemm does.
+ * ------------------------------------------------------------------------ */
+#define WINGSPAN_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+
+wingspan_status wingspan_spgemm_noalloc(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                        int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                        int64_t c_capacity, int64_t *c_nnz, void *stream,
+                                        const wingspan_options *options);
+
 /* Per-row product counts: row_products_dev[i] (int64, A.nrows entries, written
  * by the library) receives the number of scalar products A[i,k] * B[k,j] that
  * Gustavson's loop forms for row i (Section 5.1, the SpGEMM programs figure:

@@ -14,6 +14,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "../../include/wingspan.h"
@@ -1228,6 +1229,43 @@ wingspan_status op_impl(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, c
 }  // namespace
 
 // ---------------------------------------------------------------------------
+// Static scratch of wingspan_spgemm_noalloc: a device array in the library's
+// code object, so that entry point needs no allocation. Every device the
+// library runs on holds its own copy, at its own address, until the process
+// ends. Host code never uses the array's name as an address (on the host it
+// names a stand-in, not device memory): it takes the device address from
+// hipGetSymbolAddress, once per device, with that device current.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char wsp_static_scratch[WINGSPAN_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of the static scratch.
+wingspan_status static_scratch(void **out) {
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(WINGSPAN_ERR_UNSUPPORTED, "device %d: the static scratch is kept for devices 0..%d", dev,
+                    kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(wsp_static_scratch)));
+        if (p == nullptr || reinterpret_cast<uintptr_t>(p) % kAlign != 0)
+            return fail(WINGSPAN_ERR_HIP, "hipGetSymbolAddress gave an unusable scratch address %p", p);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return WINGSPAN_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
 // C ABI
 // ---------------------------------------------------------------------------
 extern "C" {
@@ -1328,6 +1366,41 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
         return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_col_idx_dev or c_val_dev is NULL");
     return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, workspace_dev, workspace_bytes,
                          stream, options, true, c);
+}
+
+wingspan_status wingspan_spgemm_noalloc(const wingspan_csr *A, const wingspan_csr *B, wingspan_dtype dtype,
+                                        int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
+                                        int64_t c_capacity, int64_t *c_nnz, void *stream,
+                                        const wingspan_options *options) {
+    g_err.clear();
+    if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
+    if (c_capacity < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_capacity is negative");
+    if (!c_nnz) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_nnz is NULL");
+    if (!c_row_ptr_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_row_ptr_dev is NULL");
+    wingspan_status s = check_pair(A, B);
+    if (s != WINGSPAN_OK) return s;
+    Opts o;
+    if ((s = parse_opts(options, &o)) != WINGSPAN_OK) return s;
+    if (o.timing)   // the timing events would be created (allocated) on first use
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "options->timing is not available without allocation");
+    const size_t cap = WINGSPAN_NOALLOC_SCRATCH_BYTES;
+    const size_t need = plan(A, B, o, cap).total;
+    if (need > cap)
+        return fail(WINGSPAN_ERR_WORKSPACE_TOO_SMALL,
+                    "this product needs %zu bytes of scratch; the static scratch holds %zu", need, cap);
+    void *scratch = nullptr;
+    if ((s = static_scratch(&scratch)) != WINGSPAN_OK) return s;
+    Ctx c{};
+    s = symbolic_entry(A, B, c_row_ptr_dev, c_nnz, scratch, cap, stream, options, c, cap);
+    if (s != WINGSPAN_OK) return s;
+    if (*c_nnz > c_capacity)
+        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "nnz(C) = %lld exceeds c_capacity = %lld",
+                    (long long)*c_nnz, (long long)c_capacity);
+    if (*c_nnz > 0 && (!c_col_idx_dev || !c_val_dev))
+        return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_col_idx_dev or c_val_dev is NULL");
+    return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, scratch, cap, stream, options, true,
+                         c);
 }
 
 wingspan_status wingspan_spgemm_row_products(const wingspan_csr *A, const wingspan_csr *B,

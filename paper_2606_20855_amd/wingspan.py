@@ -118,6 +118,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wingspan_spgemm_numeric.restype = i32
     lib.wingspan_spgemm.argtypes = [csr_p, csr_p, i32, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
     lib.wingspan_spgemm.restype = i32
+    lib.wingspan_spgemm_noalloc.argtypes = [csr_p, csr_p, i32, vp, vp, vp, i64, P(i64), vp, opt_p]
+    lib.wingspan_spgemm_noalloc.restype = i32
     lib.wingspan_spgemm_row_products.argtypes = [csr_p, csr_p, vp, vp, sz, vp]
     lib.wingspan_spgemm_row_products.restype = i32
     lib.wingspan_spgemm_sharded.argtypes = [csr_p, csr_p, i32, vp, vp, vp, vp, i64, P(i64), vp, sz, vp, opt_p]
@@ -154,6 +156,7 @@ EXPORTED = (
     "wingspan_spgemm_symbolic",
     "wingspan_spgemm_numeric",
     "wingspan_spgemm",
+    "wingspan_spgemm_noalloc",
     "wingspan_spgemm_row_products",
     "wingspan_spgemm_sharded",
     "wingspan_sharded_to_csr_workspace_size",
@@ -241,6 +244,18 @@ def wingspan_spgemm(A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int
     _check(load().wingspan_spgemm(ctypes.byref(A), ctypes.byref(B), dtype, c_row_ptr, c_col_idx, c_val,
                                   c_capacity, ctypes.byref(nnz), workspace, workspace_bytes, stream or None,
                                   _opt_ptr(options)))
+    return nnz.value
+
+
+NOALLOC_SCRATCH_BYTES = 256 << 20   # WINGSPAN_NOALLOC_SCRATCH_BYTES
+
+
+def wingspan_spgemm_noalloc(A: wingspan_csr, B: wingspan_csr, dtype: int, c_row_ptr: int, c_col_idx: int,
+                            c_val: int, c_capacity: int, stream: int = 0, options=None) -> int:
+    nnz = ctypes.c_int64(0)
+    _check(load().wingspan_spgemm_noalloc(ctypes.byref(A), ctypes.byref(B), dtype, c_row_ptr, c_col_idx or None,
+                                          c_val or None, c_capacity, ctypes.byref(nnz), stream or None,
+                                          _opt_ptr(options)))
     return nnz.value
 
 

@@ -306,3 +306,26 @@ def test_row_products_argument_errors():
     # an A without rows may pass a NULL output (it then stops at the workspace check)
     got, _ = status_of(ws.wingspan_spgemm_row_products, desc(0, 12, 0, col=0, val=0), B, 0, FAKE, 0)
     assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL"
+
+
+def test_noalloc_argument_errors():
+    A, B = desc(10, 12, 5), desc(12, 7, 9)
+    call = ws.wingspan_spgemm_noalloc
+    for args, kw, code in [((A, desc(11, 7, 9), ws.F64, FAKE, FAKE, FAKE, 10), {}, "WINGSPAN_ERR_DIMENSION_MISMATCH"),
+                           ((A, B, 7, FAKE, FAKE, FAKE, 10), {}, "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                           ((A, B, ws.F64, 0, FAKE, FAKE, 10), {}, "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                           ((A, B, ws.F64, FAKE, FAKE, FAKE, -1), {}, "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                           ((A, B, ws.F64, FAKE, FAKE, FAKE, 10), dict(options=ws.make_options(timing=1)),
+                            "WINGSPAN_ERR_INVALID_ARGUMENT"),
+                           ((A, B, ws.F64, FAKE, FAKE, FAKE, 10), dict(options=ws.make_options(max_lds_slots=100)),
+                            "WINGSPAN_ERR_INVALID_ARGUMENT")]:
+        got, _ = status_of(call, *args, **kw)
+        assert got == code, (args, kw)
+    # a product whose scratch would pass the static array's size is refused before any HIP call
+    big = desc(2**30, 2**30, 2**31 - 1)
+    got, msg = status_of(call, big, big, ws.F32, FAKE, FAKE, FAKE, 10)
+    assert got == "WINGSPAN_ERR_WORKSPACE_TOO_SMALL" and str(ws.NOALLOC_SCRATCH_BYTES) in msg
+    lib = ws.load()
+    st = lib.wingspan_spgemm_noalloc(ctypes.byref(A), ctypes.byref(B), ws.F64, FAKE, FAKE, FAKE, 10, None, None,
+                                     None)
+    assert ws.STATUS[st] == "WINGSPAN_ERR_INVALID_ARGUMENT"
