@@ -172,17 +172,11 @@ __device__ __forceinline__ int lds_insert(int32_t *keys, double *vals, int log2t
     const uint32_t mask = (1u << log2t) - 1u;
     uint32_t h = hash_slot(col, log2t);
     for (uint32_t probe = 0; probe <= mask; ++probe) {
-        const int cur = __hip_atomic_load(&keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (cur == col) {
+        // one compare-and-swap per probe: it claims an empty slot or reports the key that holds it
+        const int old = atomicCAS(&keys[h], kEmptyKey, col);
+        if (old == kEmptyKey || old == col) {
             if (NUM) atomicAdd(&vals[h], prod);
-            return 0;
-        }
-        if (cur == kEmptyKey) {
-            const int old = atomicCAS(&keys[h], kEmptyKey, col);
-            if (old == kEmptyKey || old == col) {
-                if (NUM) atomicAdd(&vals[h], prod);
-                return old == kEmptyKey ? 1 : 0;
-            }
+            return old == kEmptyKey ? 1 : 0;
         }
         h = (h + 1) & mask;
     }
@@ -683,7 +677,43 @@ __global__ void __launch_bounds__(DenseShape<WV>::BLOCK) dense_num_kernel(Mats<V
 // of windows.
 // ---------------------------------------------------------------------------
 constexpr int kRankWinCols = 8192;
-constexpr int kStageStep = 2;   // entries a lane stages per step (measured best of 1..4 and 8 on R-MAT 18)
+
+// Position of the q-th set bit (counting from 0) of x, for q < popcount(x):
+// the largest p whose bits below it number at most q, by binary search (the
+// bits below p are a bit-field extract of width p, then a popcount).
+__device__ __forceinline__ int select_set_bit(uint32_t x, int q) {
+    const uint32_t uq = static_cast<uint32_t>(q);
+    int pos = __popc(x & 0xffffu) <= uq ? 16 : 0;
+#pragma unroll
+    for (int w = 8; w >= 1; w >>= 1) {
+        const int t = pos + w;
+        pos = static_cast<uint32_t>(__popc(__builtin_amdgcn_ubfe(x, 0u, static_cast<uint32_t>(t)))) <= uq ? t : pos;
+    }
+    return pos;
+}
+
+// Two consecutive values at p (8-byte aligned for float, 16 for double) in
+// one streaming store.
+typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef double f64x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void store_pair_nt(int32_t *p, int32_t a, int32_t b) {
+    __builtin_nontemporal_store(i32x2{a, b}, reinterpret_cast<i32x2 *>(p));
+}
+__device__ __forceinline__ void store_pair_nt(float *p, float a, float b) {
+    __builtin_nontemporal_store(f32x2{a, b}, reinterpret_cast<f32x2 *>(p));
+}
+__device__ __forceinline__ void store_pair_nt(double *p, double a, double b) {
+    __builtin_nontemporal_store(f64x2{a, b}, reinterpret_cast<f64x2 *>(p));
+}
+
+// Marks slot k of the rank kernel's slice with bitmap word wd: the low half of
+// the slot's 8-byte accumulator (float output) or the stage array (double).
+template <bool PACKED>
+__device__ __forceinline__ void rank_mark(double *acc, int32_t *stage, int k, int wd) {
+    if constexpr (PACKED) reinterpret_cast<uint2 *>(acc)[k].x = static_cast<uint32_t>(wd);
+    else stage[k] = wd;
+}
 
 // Shape: 1024 threads, regions of 8192 bitmap words (262144 columns), and a
 // rank accumulator of CAP doubles. With float output a staged entry (column,
@@ -699,6 +729,7 @@ struct RankShape {
     static constexpr int CAP = PACKED ? 10864 : 7232;
     static constexpr int STAGE = PACKED ? 1 : CAP;   // separate column stage (ints)
     static_assert(REGION_COLS % kRankWinCols == 0, "regions hold whole windows");
+    static_assert(CAP % 2 == 0, "the copy reads slots in pairs");
     static_assert(REGION_WORDS % (BLOCK / kWave * kWave) == 0, "prefix scan takes whole word rows per wave");
 };
 
@@ -812,12 +843,11 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     constexpr int WIN_WORDS = kRankWinCols / 32;
     constexpr int CAP = SH::CAP;
     __shared__ uint2 bw[RW];                 // x: column bits, y: exclusive prefix within the region
-    __shared__ double acc[CAP];
-    __shared__ int32_t stage[SH::STAGE];
+    __shared__ __align__(16) double acc[CAP];
+    __shared__ __align__(16) int32_t stage[SH::STAGE];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
-    __shared__ int32_t sclaim;   // staging's group counter
     __shared__ int32_t s_next;   // the claimed next row
     __shared__ int64_t s_claim[2];   // pool output: the row's first entry and writable length
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries], e_hi[kCacheEntries];
@@ -835,10 +865,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     int32_t *mark = marks + wv * kMarkIntsLong;
     init_marks(mark, kMarkIntsLong);
     for (int i = threadIdx.x; i < CAP; i += BLOCK) acc[i] = 0.0;
-    if (threadIdx.x == 0) {
-        sclaim = 0;
-        s_next = atomicAdd(&ctrl->rank_next, 1);
-    }
+    if constexpr (!SH::PACKED)
+        for (int i = threadIdx.x; i < CAP; i += BLOCK) stage[i] = -1;
+    if (threadIdx.x == 0) s_next = atomicAdd(&ctrl->rank_next, 1);
     __syncthreads();
     const int idx = uniform(s_next);
     if (idx >= nrows) return;   // the whole workgroup
@@ -953,6 +982,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 ecache.col_ready = true;
                 ecache.vals_ready = true;
             } else {
+                // the previous slice's copy reads the bitmap words until every wave has left it
+                __syncthreads();
                 for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
                 __syncthreads();
                 auto mark_col = [&](int col, double) {
@@ -1060,96 +1091,116 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                     fetched = true;
                     if (slot >= 0) fetch_words(a_lo, a_hi, slot);
                 }
+                const int n = r1 - r0;
+                // Emission of ranks [r0, r1). A slot's mark (the low half of its 8-byte accumulator slot for float
+                // output, the stage array for double) is -1, or the index of the bitmap word holding that rank.
                 if constexpr (SH::PACKED) {
-                    // float output: round each accumulator once and keep the float in the high half of its own
-                    // 8-byte slot, so the staging below only writes (it never waits on an accumulator read)
-                    for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
+                    // float output: round each accumulator once into the high half of its own slot; the low half
+                    // becomes "no mark"
+                    for (int i = threadIdx.x; i < n; i += BLOCK) {
                         const float v = static_cast<float>(acc[i]);
-                        reinterpret_cast<uint2 *>(acc)[i].y = __float_as_uint(v);
+                        reinterpret_cast<uint2 *>(acc)[i] = make_uint2(0xffffffffu, __float_as_uint(v));
                     }
                     __syncthreads();
                 }
-                // stage ranks [r0, r1) in rank order, one bitmap word per lane: the waves claim the windows'
-                // words in 64-word groups from an LDS counter, so the waves holding dense groups (many entries
-                // per word) take fewer of them and all finish together. A word's entries hold consecutive ranks;
-                // a lane stages them kStageStep per step (the wave loops while any lane has entries left), so
-                // the cost follows the entries, not the columns. Every rank is staged by exactly one lane.
-                const int wa = j * WIN_WORDS;
-                const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
-                int gnext = 0;
-                if (ln == 0) gnext = atomicAdd(&sclaim, 1);
-                gnext = uniform(gnext);
-                while (true) {
-                    const int g = gnext;
-                    if (wa + g * kWave >= wb) break;
-                    const int wd = wa + g * kWave + ln;
-                    const uint2 e = wd < wb ? bw[wd] : make_uint2(0u, 0u);
-                    // the next claim is in flight while this group is staged
-                    if (ln == 0) gnext = atomicAdd(&sclaim, 1);
-                    gnext = uniform(gnext);
-                    uint32_t wbits = e.x;
-                    int r = static_cast<int>(e.y);
-                    // drop the entries below r0
-                    while (wbits != 0u && r < r0) {
-                        wbits &= wbits - 1u;
-                        ++r;
-                    }
-                    int n = __popc(wbits);
-                    if (r + n > r1) n = r1 - r;
-                    if (n < 0) n = 0;
-                    const int k0 = r - r0;   // this lane's first slot
-                    const int cbase = static_cast<int>(col0) + wd * 32;
-                    for (int i = 0; ballot(i < n) != 0ull; i += kStageStep) {
-                        if (i < n) {
-                            int cv[kStageStep];
-#pragma unroll
-                            for (int q = 0; q < kStageStep; ++q) {
-                                // unspecified once wbits is empty (q >= n - i), and then never written
-                                cv[q] = cbase + __builtin_ctz(wbits);
-                                wbits &= wbits - 1u;
-                            }
-                            if constexpr (SH::PACKED) {
-                                // the column goes into the low half of the slot, beside the float value
-#pragma unroll
-                                for (int q = 0; q < kStageStep; ++q) {
-                                    if (i + q < n)
-                                        reinterpret_cast<uint2 *>(acc)[k0 + i + q].x = static_cast<uint32_t>(cv[q]);
-                                }
-                            } else {
-#pragma unroll
-                                for (int q = 0; q < kStageStep; ++q) {
-                                    if (i + q < n) stage[k0 + i + q] = cv[q];
-                                }
-                            }
+                // Marks: every word holding ranks of the slice marks the first of them, and the one at a multiple
+                // of 128 slots past r0 if it holds such a rank further on (a word holds at most 32 ranks, so at most
+                // one). Each 128-slot block of the slice then starts on a mark.
+                {
+                    const int wa = j * WIN_WORDS;
+                    const int wb = j2 * WIN_WORDS < nwords ? j2 * WIN_WORDS : nwords;
+                    for (int wd = wa + static_cast<int>(threadIdx.x); wd < wb; wd += BLOCK) {
+                        const uint2 e = bw[wd];
+                        const int f = static_cast<int>(e.y) > r0 ? static_cast<int>(e.y) - r0 : 0;
+                        const int l = static_cast<int>(e.y) + __popc(e.x) - r0;
+                        const int le = l < n ? l : n;
+                        if (f < le) {
+                            rank_mark<SH::PACKED>(acc, stage, f, wd);
+                            const int m128 = (f + 2 * kWave - 1) & ~(2 * kWave - 1);
+                            if (m128 > f && m128 < le) rank_mark<SH::PACKED>(acc, stage, m128, wd);
                         }
                     }
                 }
                 __syncthreads();
                 if (prefetch && slot >= 0) fetch_bounds(a_lo, a_hi);
-                // copy the slice to C with coalesced stores, clearing the accumulator
-                const int64_t pbase = done + r0;
-                for (int i = threadIdx.x; i < r1 - r0; i += BLOCK) {
-                    int32_t colv;
-                    V v;
-                    if constexpr (SH::PACKED) {
-                        const uint2 e = reinterpret_cast<const uint2 *>(acc)[i];
-                        colv = static_cast<int32_t>(e.x);
-                        v = static_cast<V>(__uint_as_float(e.y));
-                    } else {
-                        colv = stage[i];
-                        v = static_cast<V>(acc[i]);
-                    }
-                    acc[i] = 0.0;
-                    if (pbase + i < seg) {
-                        // streaming stores: C is written once, and must not push B out of the L2
-                        __builtin_nontemporal_store(colv, &c_col[cb + pbase + i]);
-                        __builtin_nontemporal_store(v, &c_val[cb + pbase + i]);
+                // copy the slice to C with coalesced stores, two slots per lane: wave w takes the 128-slot blocks
+                // w, w + NW, ..., lane l slots 2l and 2l + 1 of the block. A slot's word is the last mark at or
+                // before it in its block (a max-scan, since words increase with rank), its column the
+                // (rank - word's first rank)-th set bit of that word. Marks and accumulators are cleared for the
+                // next slice as they are read.
+                {
+                    int32_t *const colp = c_col + (cb + done + r0);   // uniform bases: 32-bit lane offsets
+                    V *const valp = c_val + (cb + done + r0);
+                    const int64_t lim = seg - (done + r0);   // slots at or past it are not written
+                    // pairs of slots (even slot first) go out as one column store and one value store when both
+                    // pairs are aligned to their size
+                    const bool pair_aligned = (reinterpret_cast<uintptr_t>(colp) % (2 * sizeof(int32_t))) == 0 &&
+                                              (reinterpret_cast<uintptr_t>(valp) % (2 * sizeof(V))) == 0;
+                    for (int b0 = wv * 2 * kWave; b0 < n; b0 += 2 * BLOCK) {
+                        const int i0 = b0 + 2 * ln;
+                        int mk0 = -1, mk1 = -1;
+                        V v0 = V(0), v1 = V(0);
+                        if (i0 < n) {
+                            // i0 is even: the two slots are one 16-byte read (and clear)
+                            if constexpr (SH::PACKED) {
+                                const uint4 u = reinterpret_cast<const uint4 *>(acc)[i0 >> 1];
+                                mk0 = static_cast<int>(u.x);
+                                v0 = static_cast<V>(__uint_as_float(u.y));
+                                mk1 = static_cast<int>(u.z);
+                                v1 = static_cast<V>(__uint_as_float(u.w));
+                            } else {
+                                const int2 m2 = reinterpret_cast<const int2 *>(stage)[i0 >> 1];
+                                const double2 a2 = reinterpret_cast<const double2 *>(acc)[i0 >> 1];
+                                reinterpret_cast<int2 *>(stage)[i0 >> 1] = make_int2(-1, -1);
+                                mk0 = m2.x;
+                                mk1 = m2.y;
+                                v0 = static_cast<V>(a2.x);
+                                v1 = static_cast<V>(a2.y);
+                            }
+                            reinterpret_cast<double2 *>(acc)[i0 >> 1] = make_double2(0.0, 0.0);
+                        }
+                        // slot i0 + 1's word: the last mark up to it; slot i0's: the last mark up to i0 - 1, or its own
+                        const int w1 = wave_incl_max(mk1 > mk0 ? mk1 : mk0);
+                        int w0 = __shfl_up(w1, 1, kWave);
+                        w0 = ln == 0 ? -1 : w0;
+                        w0 = mk0 > w0 ? mk0 : w0;
+                        if (i0 < n) {
+                            const uint2 e0 = bw[w0];
+                            const int p0 = select_set_bit(e0.x, r0 + i0 - static_cast<int>(e0.y));
+                            const int c0 = static_cast<int>(col0) + w0 * 32 + p0;
+                            // slot i0 + 1 holds the next set bit of the same word, or else the first rank of a
+                            // later word, its lowest set bit (a mark at an odd slot is a word's first rank: marks
+                            // inside a word sit at multiples of 128)
+                            const uint32_t above = p0 < 31 ? e0.x >> (p0 + 1) : 0u;
+                            int c1 = 0;
+                            if (w1 == w0) {
+                                c1 = c0 + 1 + static_cast<int>(__builtin_ctz(above | 0x80000000u));
+                            } else {
+                                const uint32_t x1 = bw[w1].x;
+                                c1 = static_cast<int>(col0) + w1 * 32 + static_cast<int>(__builtin_ctz(x1 | 0x80000000u));
+                            }
+                            const bool two = i0 + 1 < n && i0 + 1 < lim;
+                            if (pair_aligned && two) {
+                                // streaming stores: C is written once, and must not push B out of the L2
+                                store_pair_nt(colp + i0, c0, c1);
+                                store_pair_nt(valp + i0, v0, v1);
+                            } else {
+                                if (i0 < lim) {
+                                    __builtin_nontemporal_store(c0, &colp[i0]);
+                                    __builtin_nontemporal_store(v0, &valp[i0]);
+                                }
+                                if (two) {
+                                    __builtin_nontemporal_store(c1, &colp[i0 + 1]);
+                                    __builtin_nontemporal_store(v1, &valp[i0 + 1]);
+                                }
+                            }
+                        }
                     }
                 }
-                // no barrier here: the next accumulator writes (the next slice's or row's value pass) come after
-                // the value pass's own barriers, and nothing else read or written before them is touched by the
-                // copy (the entry cache, the prefix scratch and the bitmap words are not)
-                if (threadIdx.x == 0) sclaim = 0;   // every wave has left the staging loop
+                // no barrier here: the next accumulator and mark writes (the next slice's or row's value pass, then
+                // its marks) come after the value pass's own barriers; the bitmap words the copy reads are rewritten
+                // only after a barrier (the next region's or row's prefix, or the structure pass's clear); the entry
+                // cache and the prefix scratch are not touched by the copy
                 r0 = r1;
                 if (r1 == rend_w) j = j2;   // the windows are done; otherwise the next slice of window j
             }
