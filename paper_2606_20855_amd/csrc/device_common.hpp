@@ -49,6 +49,12 @@ struct Stamp {
     int64_t off_slot, off_cache, row_words, cache_rows;
     int64_t cached_rows;   // rows that received a cache slot
     uint64_t rp_sum;
+    // The numeric phase's binning of the rows by C's exact row counts, done once C.row_ptr was known, with
+    // these settings (num_bins 1), and B's window table (wtab 1): the numeric phase takes them when its own
+    // settings are the same.
+    int64_t num_bins, wtab;
+    int64_t nb_dense_min_nnz;
+    int32_t nb_tiny_max, nb_hash_log2_max, nb_force_spill, nb_dense_ok;
 };
 constexpr uint64_t kStampMagic = 0x57535f5354525543ull;
 

@@ -171,6 +171,7 @@ wingspan_status check_pair(const wingspan_csr *A, const wingspan_csr *B) {
 struct Layout {
     size_t off_stamp, off_ctrl, off_pref, off_row_nnz, off_perm, off_rrows, off_partials, off_wtab, off_pool, total;
     size_t off_slot, off_cache;   // structure cache (cache_rows == 0: none)
+    size_t off_ctrl_num, off_perm_num;   // the numeric binning kept from the symbolic phase (with the cache)
     int64_t row_words, cache_rows;
     int nwin;          // numeric dense windows per row (0: dense numeric tier unavailable)
     int wcols;         // columns per window of the window table
@@ -231,6 +232,10 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o, size_t 
         L.row_words = (L.row_words + 63) / 64 * 64;
         L.cache_rows = std::min<int64_t>(m, kStructCacheBytes / (L.row_words * 4));
     }
+    L.off_ctrl_num = off;
+    if (L.cache_rows > 0) off += align_up(sizeof(Control));
+    L.off_perm_num = off;
+    if (L.cache_rows > 0) off += align_up(sizeof(int32_t) * m);
     L.off_slot = off;
     if (L.cache_rows > 0) off += align_up(sizeof(int32_t) * m);
     L.off_cache = off;
@@ -259,6 +264,10 @@ struct Ctx {
     Stamp *stamp;
     int32_t *slot_of_row;
     uint32_t *cache;
+    Control *ctrl_num;        // the numeric binning the symbolic phase kept (with the cache)
+    int32_t *perm_num;
+    const int32_t *bins;      // numeric phase: the row ids grouped by bin it uses (perm or perm_num)
+    bool wtab_ready = false;  // numeric phase: the window table is the one the symbolic phase built
     Control host;
     Stamp host_stamp;
 };
@@ -276,6 +285,9 @@ void carve(Ctx &c, void *ws) {
     c.stamp = reinterpret_cast<Stamp *>(c.ws + c.L.off_stamp);
     c.slot_of_row = reinterpret_cast<int32_t *>(c.ws + c.L.off_slot);
     c.cache = reinterpret_cast<uint32_t *>(c.ws + c.L.off_cache);
+    c.ctrl_num = reinterpret_cast<Control *>(c.ws + c.L.off_ctrl_num);
+    c.perm_num = reinterpret_cast<int32_t *>(c.ws + c.L.off_perm_num);
+    c.bins = c.perm;
 }
 
 // The stamp a symbolic phase on (A, B) with this layout leaves (magic and
@@ -298,6 +310,29 @@ Stamp make_stamp(const Ctx &c, const wingspan_csr *A, const wingspan_csr *B, int
     t.row_words = c.L.row_words;
     t.cache_rows = c.L.cache_rows;
     return t;
+}
+
+// How the numeric phase bins rows (by C's exact row counts).
+BinCfg numeric_bin_cfg(const Ctx &c, const wingspan_csr *B) {
+    BinCfg cfg{};
+    cfg.ncols = B->ncols;
+    cfg.numeric = 1;
+    cfg.tiny_max = c.o.tiny_max;
+    cfg.force_spill = c.o.force_spill;
+    cfg.hash_log2_max = c.o.hash_log2_max_num;
+    cfg.dense_min_nnz = c.o.dense_min_nnz;
+    cfg.dense_ok = c.L.nwin > 0;
+    return cfg;
+}
+
+void stamp_bins(Stamp &t, const BinCfg &cfg, bool wtab) {
+    t.num_bins = 1;
+    t.wtab = wtab ? 1 : 0;
+    t.nb_dense_min_nnz = cfg.dense_min_nnz;
+    t.nb_tiny_max = cfg.tiny_max;
+    t.nb_hash_log2_max = cfg.hash_log2_max;
+    t.nb_force_spill = cfg.force_spill;
+    t.nb_dense_ok = cfg.dense_ok;
 }
 
 // Whether the numeric phase may use the structure cache: the stamp is valid,
@@ -372,6 +407,40 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
     const int64_t words = sizeof(Control) / sizeof(int32_t);
     zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl), words);
     LAUNCH_CHECK("zero_words");
+    c.bins = c.perm;
+    c.wtab_ready = false;
+    if (numeric && c.L.cache_rows > 0 && !c.o.validate) {
+        // The symbolic phase on the same workspace may have binned the rows by this C.row_ptr already: check
+        // its stamp (with C.row_ptr's checksum) and take its bins if they were made with these settings
+        rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, m, &c.ctrl->rp_sum);
+        LAUNCH_CHECK("stamp");
+        Control kept;
+        HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipMemcpyAsync(&c.host_stamp, c.stamp, sizeof(Stamp), hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipMemcpyAsync(&kept, c.ctrl_num, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
+        const BinCfg cfg = numeric_bin_cfg(c, B);
+        const Stamp &h = c.host_stamp;
+        if (stamp_matches(c, A, B) && h.num_bins == 1 && h.nb_dense_min_nnz == cfg.dense_min_nnz &&
+            h.nb_tiny_max == cfg.tiny_max && h.nb_hash_log2_max == cfg.hash_log2_max &&
+            h.nb_force_spill == cfg.force_spill && h.nb_dense_ok == cfg.dense_ok) {
+            const uint64_t rp_sum = c.host.rp_sum;
+            c.host = kept;
+            c.host.rp_sum = rp_sum;
+            c.bins = c.perm_num;
+            c.wtab_ready = h.wtab == 1;
+            if ((s = timer_stop(c, kSlotAnalysis)) != WINGSPAN_OK) return s;
+            const int64_t slab_limit = c.L.slab_cap / 2;
+            if (c.host.spill_max_bound > slab_limit)
+                return fail(WINGSPAN_ERR_UNSUPPORTED,
+                            "a row needs %lld hash slots but the spill pool's slabs hold %lld entries",
+                            (long long)c.host.spill_max_bound, (long long)slab_limit);
+            return WINGSPAN_OK;
+        }
+        // not kept for this call: bin here (the checksum is added again below)
+        zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl), words);
+        LAUNCH_CHECK("zero_words");
+    }
     if (mode == kModeSymbolic) {
         // the structure cache is being rewritten: invalid until this phase completes
         write_stamp<<<1, 1, 0, c.st>>>(c.stamp, Stamp{});
@@ -398,7 +467,8 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
         s = run_scan(c, BRowLenIn{A->col_idx, B->row_ptr}, A->nnz, c.pref);
         if (s != WINGSPAN_OK) return s;
     }
-    if (numeric && c.dtype_f64 >= 0) {
+    if (numeric && c.dtype_f64 >= 0 && !c.L.rank_mode) {
+        // only the column-window dense kernel's sentinel slots depend on it
         const unsigned zb = 1024;
         if (c.dtype_f64) {
             find_zero_values<double><<<zb, 256, 0, c.st>>>(static_cast<const double *>(A->val), A->nnz, c.ctrl);
@@ -419,7 +489,7 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
     cfg.hash_log2_max = mode == kModeSymbolic ? c.o.hash_log2_max_sym : c.o.hash_log2_max_num;
     cfg.dense_min_nnz = c.o.dense_min_nnz;
     if (mode == kModeNumeric) {
-        cfg.dense_ok = c.L.nwin > 0;
+        cfg = numeric_bin_cfg(c, B);
     } else if (mode == kModeSymbolic) {
         cfg.dense_ok = !c.o.dense_disabled && B->ncols <= kBitmapMaxCols;
     } else {
@@ -654,8 +724,30 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
     s = run_scan(c, CountIn{c.row_nnz}, A->nrows, c_rp);
     if (s != WINGSPAN_OK) return s;
     if (caching) {
-        // the cache is complete: stamp it with the inputs, the layout and C.row_ptr's checksum
-        write_stamp<<<1, 1, 0, c.st>>>(c.stamp, make_stamp(c, A, B, std::min<int64_t>(cnt_dense, c.L.cache_rows)));
+        // C.row_ptr is known: bin the rows as the numeric phase does, and build B's window table for the dense
+        // rows (the numeric phase's dense rows are symbolic dense rows too: a row's entries never exceed its
+        // products), so a numeric phase on this workspace starts from them
+        const BinCfg ncfg = numeric_bin_cfg(c, B);
+        const int64_t words = sizeof(Control) / sizeof(int32_t);
+        zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl_num), words);
+        bin_count<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, A->nrows, ncfg, c.ctrl_num,
+                                                                 c.row_nnz);
+        bin_offsets<<<1, 1, 0, c.st>>>(c.ctrl_num, c.pref, A->nnz);
+        bin_scatter<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, A->nrows, ncfg,
+                                                                   c.ctrl_num, c.perm_num);
+        LAUNCH_CHECK("numeric binning");
+        const bool wtab = cnt_dense > 0 && c.L.nwin > 0;
+        if (wtab) {
+            const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
+            build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows,
+                                                                           c.L.nwin, c.L.wcols, c.wtab);
+            LAUNCH_CHECK("build_window_table");
+        }
+        // the cache is complete: stamp it with the inputs, the layout, the bins' settings and C.row_ptr's
+        // checksum
+        Stamp t = make_stamp(c, A, B, std::min<int64_t>(cnt_dense, c.L.cache_rows));
+        stamp_bins(t, ncfg, wtab);
+        write_stamp<<<1, 1, 0, c.st>>>(c.stamp, t);
         rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, A->nrows, &c.stamp->rp_sum);
         seal_stamp<<<1, 1, 0, c.st>>>(c.stamp);
         LAUNCH_CHECK("stamp");
@@ -683,7 +775,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
                     (long long)c_entries);
     const Mats<V> M{A->row_ptr, A->col_idx, static_cast<const V *>(A->val),
                     B->row_ptr, B->col_idx, static_cast<const V *>(B->val)};
-    const int32_t *perm = c.perm;
+    const int32_t *perm = c.bins;
     RowSink sink;
     sink.c_rp = c_rp;
 
@@ -714,7 +806,7 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
 
     int32_t start, cnt;
     bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
-    if (cnt) {
+    if (cnt && !c.wtab_ready) {
         const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
         build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows, c.L.nwin,
                                                                        c.L.wcols, c.wtab);

@@ -169,3 +169,23 @@ def test_wide_offsets_path(dtype):
         got, num = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, opts)
         assert num["rows"]["dense"] > 0
         assert_matches(got, ref, A.val.dtype, what=f"offsets {opts}")
+
+
+@pytest.mark.parametrize("change", [dict(tiny_max=16), dict(max_lds_slots=512), dict(dense_min_nnz=200),
+                                    dict(force_spill=1)])
+def test_numeric_settings_differ_from_symbolic(change):
+    # the symbolic phase bins the rows for a numeric phase with its own settings; a numeric call with other
+    # settings (same layout) must bin them itself, and match the oracle
+    A = matgen.rmat(11, 16, seed=61, dtype=np.float32)
+    dA = _dev(A)
+    ref = oracle.spgemm(A, A)
+    wsb, nbytes = _workspace(dA, dA, DENSE)
+    c_rp, nnz = _symbolic(dA, dA, wsb, nbytes, DENSE)
+    got, num = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, dict(DENSE, **change))
+    assert_matches(got, ref, A.val.dtype, what=f"numeric {change}")
+    if change.get("force_spill"):
+        assert num["rows"]["spill"] > 0 and num["rows"]["dense"] == 0
+    # and the same workspace again with the symbolic phase's own settings
+    got2, num2 = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, DENSE)
+    assert_matches(got2, ref, A.val.dtype, what="numeric with the symbolic settings")
+    assert num2["structure_cache_rows"] > 0 and num2["rows"]["dense"] > 0
