@@ -11,6 +11,9 @@ input, writing into a preallocated C. Prints one JSON line:
              algorithmic bytes and its HIP-event time on the library's stream
   numeric_phase  algorithmic bytes of the numeric phase / its time
   cpu_baseline   the CPU oracle (single thread) on a seeded random sample of rows
+  configs        every other SpGEMM workload: GFLOP/s, phase times, numeric
+                 algorithmic GB/s against peak, the dominant kernel, and the CPU
+                 oracle on the same workload (all rows, or a row sample)
   sharded_single_pass  the single pass with sharded output on the same workload
   elementwise    SpAdd and the Hadamard product (B = A, and B a shuffled copy)
                  on the R-MAT scale-20 matrix, against HBM bandwidth
@@ -88,21 +91,31 @@ def alg_bytes(rows, a_nnz, products, c_nnz, s):
     return 12 * rows + (12 + s) * a_nnz + (4 + s) * products + (4 + s) * c_nnz
 
 
-def cpu_baseline(A, B, fraction: float, seed: int):
+def oracle_pass(A, B, rows=None):
+    """One pass of the CPU oracle's Gustavson over `rows` (all by default),
+    with the output sized beforehand by the bound sum(min(row products,
+    B.ncols)) so the oracle runs once (no counting pass). Returns (seconds,
+    products, output entries)."""
     import oracle
+    prods = oracle.row_products(A, B, rows)
+    cap = int(np.minimum(prods, B.ncols).sum())
+    t0 = time.perf_counter()
+    res = oracle.spgemm(A, B, rows=rows, with_mag=False, capacity=cap)
+    return time.perf_counter() - t0, int(prods.sum()), res.nnz
+
+
+def cpu_baseline(A, B, fraction: float, seed: int):
     rng = np.random.default_rng(seed)
     rows = np.sort(rng.choice(A.nrows, size=max(1, int(A.nrows * fraction)), replace=False)).astype(np.int64)
-    prods = int(oracle.row_products(A, B, rows).sum())
-    t0 = time.perf_counter()
-    res = oracle.spgemm(A, B, rows=rows, with_mag=False)
-    dt = time.perf_counter() - t0
+    dt, prods, nnz = oracle_pass(A, B, rows)
     return dict(
         value=round(2.0 * prods / dt / 1e9, 5),
         unit="GFLOP/s",
         cores=1,
         kind="oracle",
         sample=(f"{len(rows)} rows ({fraction:.0%}) drawn uniformly at random (seed {seed}) from the same "
-                f"matrix; {prods} products, {res.nnz} output entries, {dt:.1f} s single-threaded"),
+                f"matrix; {prods} products, {nnz} output entries, {dt:.1f} s single-threaded, one pass of the "
+                f"oracle"),
     )
 
 
@@ -314,6 +327,145 @@ def outer_pass(ws, torch, workload, dev, steps, warmup):
                 gustavson_ms=round(tg, 4), vs_gustavson=round(tg / to, 3))
 
 
+def host_description() -> dict:
+    """The host the CPU baseline ran on: logical CPUs, model name, sockets."""
+    desc = dict(nproc=os.cpu_count())
+    model, sockets = None, set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name") and model is None:
+                    model = line.split(":", 1)[1].strip()
+                elif line.startswith("physical id"):
+                    sockets.add(line.split(":", 1)[1].strip())
+    except OSError:
+        pass
+    desc["cpu_model"] = model
+    desc["sockets"] = len(sockets) or None
+    return desc
+
+
+def measure_spgemm(ws, torch, A, B, dev, steps, warmup, tier_steps=3):
+    """One SpGEMM workload: `steps` timed steps (symbolic phase, then numeric
+    phase into a preallocated C), HIP events around each phase on the
+    library's stream, options at their defaults (no per-tier timing inside the
+    calls); then `tier_steps` more steps with the library's per-tier HIP events
+    (options.timing) for the kernel breakdown and the dominant kernel's
+    roofline. Returns the measurements (and the device arrays' sizes)."""
+    dA = ws.DeviceCSR.from_host(A, dev)
+    dB = dA if B is A else ws.DeviceCSR.from_host(B, dev)
+    Ad, Bd = dA.desc(), dB.desc()
+    dt = dA.dtype_code
+    s = 4 if dt == ws.F32 else 8
+    timing = ws.make_options(timing=1)
+    wsb, nbytes = ws.allocate_workspace(dA, dB)
+    stream = torch.cuda.current_stream()
+    h = stream.cuda_stream
+    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device=dev)
+    nnz = ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, None)
+    c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(nnz, 1), dtype=dA.val.dtype, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+
+    def step(opts):
+        ev[0].record(stream)
+        ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
+        ev[1].record(stream)
+        ws.wingspan_spgemm_numeric(Ad, Bd, dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
+                                   wsb.data_ptr(), nbytes, h, opts)
+        ev[2].record(stream)
+
+    for _ in range(warmup):
+        step(None)
+    torch.cuda.synchronize()
+    sym_ms, num_ms = [], []
+    t_start = time.perf_counter()
+    for _ in range(steps):
+        step(None)
+        ev[2].synchronize()
+        sym_ms.append(ev[0].elapsed_time(ev[1]))
+        num_ms.append(ev[1].elapsed_time(ev[2]))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed / steps * 1e3
+    # per-tier kernel times (the library's events on its stream)
+    tier_ms, ana_ms = {t: [] for t in ws.TIERS}, []
+    for _ in range(tier_steps):
+        step(timing)
+        num = ws.wingspan_last_stats(1)
+        sym = ws.wingspan_last_stats(0)
+        ev[2].synchronize()
+        ana_ms.append(num["analysis_ms"])
+        for t in ws.TIERS:
+            tier_ms[t].append(num["kernel_ms"][t])
+    P = int(sym["total_products"])
+    nnz_c = int(num["c_nnz_total"])
+    b_num = alg_bytes(A.nrows, A.nnz, P, nnz_c, s)
+    t_num = float(np.mean(num_ms))
+    numeric_phase = dict(ms=round(t_num, 4), ms_min=round(float(np.min(num_ms)), 4), alg_bytes=b_num,
+                         GBps=round(b_num / (t_num / 1e3) / 1e9, 1),
+                         frac=round(b_num / (t_num / 1e3) / 1e9 / HBM_PEAK_GBPS, 4))
+    dom = max(ws.TIERS, key=lambda t: np.mean(tier_ms[t]))
+    k_ms = float(np.mean(tier_ms[dom]))
+    launches = int(num["launches"][dom])
+    b_dom = alg_bytes(num["rows"][dom], num["a_nnz"][dom], num["products"][dom], num["c_nnz"][dom], s)
+    per_launch = b_dom / max(launches, 1)
+    achieved = per_launch / (k_ms / max(launches, 1) / 1e3) / 1e9 if k_ms > 0 else 0.0
+    roofline = dict(bound="hbm", kernel=KERNEL_NAMES[dom], achieved=round(achieved, 1), peak=HBM_PEAK_GBPS,
+                    unit="GB/s", frac=round(achieved / HBM_PEAK_GBPS, 4),
+                    alg_bytes_per_launch=int(per_launch), launches_per_step=launches,
+                    avg_launch_ms=round(k_ms / max(launches, 1), 4))
+    out = dict(
+        m=A.nrows, n=B.ncols, nnz_a=A.nnz, nnz_b=B.nnz, products=P, nnz_c=nnz_c,
+        value_dtype=str(A.val.dtype), accumulate="f64",
+        ms_per_step=round(ms_per_step, 4), GFLOPs=round(2.0 * P / (ms_per_step / 1e3) / 1e9, 2),
+        symbolic_ms=round(float(np.mean(sym_ms)), 4), numeric_ms=round(t_num, 4),
+        numeric_phase=numeric_phase, roofline=roofline, dominant=dom,
+        numeric_tier_ms={t: round(float(np.mean(tier_ms[t])), 4) for t in ws.TIERS},
+        numeric_analysis_ms=round(float(np.mean(ana_ms)), 4),
+        numeric_tier_rows={t: int(num["rows"][t]) for t in ws.TIERS},
+        numeric_tier_products={t: int(num["products"][t]) for t in ws.TIERS},
+        workspace_MiB=round(nbytes / 2**20, 1),
+    )
+    return out, (dA, dB)
+
+
+def cpu_oracle_config(A, B, trials: int, fraction: float, seed: int):
+    """The CPU oracle (single thread) on a workload: min of `trials` runs over
+    all rows when fraction >= 1, else one run over a seeded random `fraction`
+    of the rows, in row blocks whose outputs are dropped as they are made."""
+    if fraction >= 1.0:
+        runs = [oracle_pass(A, B) for _ in range(trials)]
+        dt, prods = min(r[0] for r in runs), runs[0][1]
+        sample = f"all {A.nrows} rows, min of {trials} one-pass runs"
+    else:
+        rng = np.random.default_rng(seed)
+        rows = np.sort(rng.choice(A.nrows, size=max(1, int(A.nrows * fraction)), replace=False)).astype(np.int64)
+        blocks = np.array_split(rows, max(1, len(rows) // 4096))
+        runs = []
+        for _ in range(trials):
+            dt, prods = 0.0, 0
+            for r in blocks:
+                t, p, _ = oracle_pass(A, B, r)
+                dt += t
+                prods += p
+            runs.append(dt)
+        dt = min(runs)
+        sample = (f"{len(rows)} rows ({fraction:.0%}, seed {seed}) in blocks of about 4096 rows, one pass each, "
+                  f"min of {trials}")
+    return dict(GFLOPs=round(2.0 * prods / dt / 1e9, 5), seconds=round(dt, 3), products=prods, cores=1,
+                sample=sample)
+
+
+CONFIG_CPU = {   # CPU oracle per workload: (trials, fraction of rows), each run about 0.1-10 s
+    "er1000": (3, 1.0),
+    "laplace512": (3, 1.0),
+    "er_rect": (3, 0.2),
+    "rmat18": (1, 0.1),
+    "rmat20": (1, 0.01),
+}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -331,6 +483,10 @@ def main():
     ap.add_argument("--no-spmspv", action="store_true", help="skip the SpMSpV timing")
     ap.add_argument("--no-outer", action="store_true", help="skip the outer-product SpGEMM timing")
     ap.add_argument("--outer-workload", default="laplace512", help="the workload of the outer-product timing")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other SpGEMM workloads (timed beside the headline one in `configs`)")
+    ap.add_argument("--config-steps", type=int, default=5, help="timed steps per other workload")
+    ap.add_argument("--configs-only", default="", help="comma-separated workloads to time in `configs`")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -373,111 +529,51 @@ def main():
     t0 = time.time()
     A, B = matgen.config(args.workload)
     log(f"generated {args.workload}: m={A.nrows} nnz(A)={A.nnz} in {time.time() - t0:.1f}s")
-    dA = ws.DeviceCSR.from_host(A, dev)
-    dB = dA if B is A else ws.DeviceCSR.from_host(B, dev)
-    Ad, Bd = dA.desc(), dB.desc()
-    dt = dA.dtype_code
-    s = 4 if dt == ws.F32 else 8
-    opts = ws.make_options(timing=1)
-    wsb, nbytes = ws.allocate_workspace(dA, dB, opts)
-    stream = torch.cuda.current_stream()
-    h = stream.cuda_stream
-    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device=dev)
-    nnz = ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
-    c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
-    c_val = torch.empty(max(nnz, 1), dtype=dA.val.dtype, device=dev)
-    log(f"nnz(C)={nnz}, workspace {nbytes / 2**20:.1f} MiB")
-
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-
-    def step():
-        ev[0].record(stream)
-        ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
-        sym = ws.wingspan_last_stats(0)
-        ev[1].record(stream)
-        ws.wingspan_spgemm_numeric(Ad, Bd, dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
-                                   wsb.data_ptr(), nbytes, h, opts)
-        num = ws.wingspan_last_stats(1)
-        ev[2].record(stream)
-        return sym, num
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    sym_ms, num_ms, tier_ms, ana_ms = [], [], {t: [] for t in ws.TIERS}, []
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        sym, num = step()
-        ev[2].synchronize()
-        sym_ms.append(ev[0].elapsed_time(ev[1]))
-        num_ms.append(ev[1].elapsed_time(ev[2]))
-        ana_ms.append(num["analysis_ms"])
-        for t in ws.TIERS:
-            tier_ms[t].append(num["kernel_ms"][t])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    ms_per_step = elapsed / args.steps * 1e3
-
-    P = int(sym["total_products"])
-    nnz_c = int(num["c_nnz_total"])
-    gflops = 2.0 * P / (ms_per_step / 1e3) / 1e9
-
-    # numeric phase against HBM bandwidth on algorithmic bytes
-    b_num = alg_bytes(A.nrows, A.nnz, P, nnz_c, s)
-    t_num = float(np.mean(num_ms))
-    numeric_phase = dict(ms=round(t_num, 4), ms_min=round(float(np.min(num_ms)), 4),
-                         alg_bytes=b_num, GBps=round(b_num / (t_num / 1e3) / 1e9, 1),
-                         frac=round(b_num / (t_num / 1e3) / 1e9 / HBM_PEAK_GBPS, 4))
-
-    # dominant numeric kernel
-    dom = max(ws.TIERS, key=lambda t: np.mean(tier_ms[t]))
-    k_ms = float(np.mean(tier_ms[dom]))
-    launches = int(num["launches"][dom])
-    b_dom = alg_bytes(num["rows"][dom], num["a_nnz"][dom], num["products"][dom], num["c_nnz"][dom], s)
-    per_launch = b_dom / max(launches, 1)
-    achieved = per_launch / (k_ms / max(launches, 1) / 1e3) / 1e9 if k_ms > 0 else 0.0
-    traffic = measured_traffic() if dom == "dense" else None
-    roofline = dict(bound="hbm", kernel=KERNEL_NAMES[dom], achieved=round(achieved, 1), peak=HBM_PEAK_GBPS,
-                    unit="GB/s", frac=round(achieved / HBM_PEAK_GBPS, 4), traffic=traffic,
-                    alg_bytes_per_launch=int(per_launch), launches_per_step=launches,
-                    avg_launch_ms=round(k_ms / max(launches, 1), 4))
-
+    res, (dA, dB) = measure_spgemm(ws, torch, A, B, dev, args.steps, args.warmup)
+    log(f"{args.workload}: nnz(C)={res['nnz_c']}, {res['ms_per_step']} ms per step, numeric phase "
+        f"{res['numeric_ms']} ms, workspace {res['workspace_MiB']} MiB")
+    P, nnz_c = res["products"], res["nnz_c"]
+    roofline = dict(res["roofline"])
+    roofline["traffic"] = measured_traffic() if res["dominant"] == "dense" else None
     out = dict(
         metric=METRIC,
-        value=round(gflops, 2),
+        value=res["GFLOPs"],
         unit="GFLOP/s",
         n_gpus=1,
         steps=args.steps,
         warmup=args.warmup,
-        ms_per_step=round(ms_per_step, 4),
+        ms_per_step=res["ms_per_step"],
         higher_is_better=True,
         scaling="weak",
         vs_baseline=None,
         dtype="f64",
+        value_dtype="f32" if A.val.dtype == np.float32 else "f64",
+        accumulate_dtype="f64",
         data="synthetic",
         config=dict(
             workload=f"{args.workload}: {cfg['desc']}",
             m=A.nrows, n=B.ncols, nnz_a=A.nnz, nnz_b=B.nnz, products=P, nnz_c=nnz_c,
             value_dtype=str(A.val.dtype), accumulate="f64",
-            seed=cfg["seed"], options="defaults (timing on)",
+            seed=cfg["seed"], options="defaults",
         ),
         roofline=roofline,
-        numeric_phase=numeric_phase,
-        symbolic_ms=round(float(np.mean(sym_ms)), 4),
-        numeric_ms=round(t_num, 4),
-        numeric_tier_ms={t: round(float(np.mean(tier_ms[t])), 4) for t in ws.TIERS},
-        numeric_analysis_ms=round(float(np.mean(ana_ms)), 4),
-        numeric_tier_rows={t: int(num["rows"][t]) for t in ws.TIERS},
-        numeric_tier_products={t: int(num["products"][t]) for t in ws.TIERS},
+        numeric_phase=res["numeric_phase"],
+        symbolic_ms=res["symbolic_ms"],
+        numeric_ms=res["numeric_ms"],
+        numeric_tier_ms=res["numeric_tier_ms"],
+        numeric_analysis_ms=res["numeric_analysis_ms"],
+        numeric_tier_rows=res["numeric_tier_rows"],
+        numeric_tier_products=res["numeric_tier_products"],
     )
     if not args.no_sharded:
         log("timing the single pass with sharded output")
-        del c_col, c_val
         torch.cuda.empty_cache()
         sh = sharded_pass(ws, torch, dA, dB, nnz_c, P, args.steps, args.warmup)
-        sh["vs_two_phase_step"] = round(ms_per_step / sh["ms"], 3)
+        sh["vs_two_phase_step"] = round(res["ms_per_step"] / sh["ms"], 3)
+        sh["vs_two_phase_step_with_gather"] = round(res["ms_per_step"] / (sh["ms"] + sh["to_csr_ms"]), 3)
         out["sharded_single_pass"] = sh
+    del dA, dB
+    torch.cuda.empty_cache()
     if not (args.no_elementwise and args.no_spmspv):
         A2 = matgen.matrix(args.ew_workload)
         if not args.no_elementwise:
@@ -487,12 +583,38 @@ def main():
         if not args.no_spmspv:
             log("timing SpMSpV (x 10% stored)")
             out["spmspv"] = spmspv_pass(ws, torch, A2, args.ew_workload, dev, args.steps, args.warmup, seed=20263)
+        del A2
+        torch.cuda.empty_cache()
     if not args.no_outer:
         log("timing the outer-product SpGEMM")
         out["outer_product"] = outer_pass(ws, torch, args.outer_workload, dev, args.steps, args.warmup)
+    host = host_description()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a row sample")
-        out["cpu_baseline"] = cpu_baseline(A, B, args.cpu_fraction, seed=20261)
+        cb = cpu_baseline(A, B, args.cpu_fraction, seed=20261)
+        cb.update(host=host)
+        out["cpu_baseline"] = cb
+    if not args.no_configs:
+        names = [n for n in (args.configs_only.split(",") if args.configs_only else matgen.CONFIGS)
+                 if n and n != args.workload]
+        out["configs"] = {}
+        for name in names:
+            ccfg = matgen.CONFIGS[name]
+            t0 = time.time()
+            Ac, Bc = matgen.config(name)
+            log(f"timing {name}: m={Ac.nrows} nnz(A)={Ac.nnz} (generated in {time.time() - t0:.1f}s)")
+            r, _ = measure_spgemm(ws, torch, Ac, Bc, dev, args.config_steps, 1)
+            r["workload"] = f"{name}: {ccfg['desc']}"
+            torch.cuda.empty_cache()
+            if not args.no_cpu_baseline:
+                trials, frac = CONFIG_CPU[name]
+                log(f"timing the CPU oracle on {name}")
+                r["cpu_oracle"] = cpu_oracle_config(Ac, Bc, trials, frac, seed=20264)
+                r["cpu_oracle"]["gpu_vs_cpu"] = round(r["GFLOPs"] / max(r["cpu_oracle"]["GFLOPs"], 1e-12), 1)
+            out["configs"][name] = r
+            del Ac, Bc
+        if not args.no_cpu_baseline:
+            out["configs_cpu_host"] = host
     print(json.dumps(out), flush=True)
 
 

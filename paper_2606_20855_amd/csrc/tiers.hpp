@@ -808,6 +808,31 @@ __global__ void __launch_bounds__(256) rank_rows(const int32_t *__restrict__ row
     out[i] = r;
 }
 
+// rank_rows for the dense bins of a binning held on the device (their range of
+// perm read from ctrl): the grid covers every row, threads past the dense rows
+// do nothing.
+__global__ void __launch_bounds__(256) rank_rows_of_bins(const int32_t *__restrict__ perm,
+                                                         const Control *__restrict__ ctrl,
+                                                         const int32_t *__restrict__ a_rp,
+                                                         const int64_t *__restrict__ c_rp,
+                                                         const int32_t *__restrict__ slot_of_row,
+                                                         RankRow *__restrict__ out) {
+    const int start = ctrl->bin_offset[kBinDense0];
+    int n = 0;
+    for (int b = kBinDense0; b < kBinDense0 + kNumClasses; ++b) n += ctrl->bin_count[b];
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int row = perm[start + i];
+    RankRow r;
+    r.row = row;
+    r.a_lo = a_rp[row];
+    r.a_hi = a_rp[row + 1];
+    r.slot = slot_of_row[row];
+    r.cb = c_rp[row];
+    r.seg = c_rp[row + 1] - r.cb;
+    out[i] = r;
+}
+
 // A zero the compiler cannot see through: an address offset by it is not
 // uniform, so the load is a vector load. Prefetches must be vector loads:
 // a scalar load counts with the LDS operations, and every barrier and LDS wait

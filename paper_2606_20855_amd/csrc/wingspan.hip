@@ -16,6 +16,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/wingspan.h"
 #include "analysis.hpp"
@@ -192,6 +193,8 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o, size_t 
     off += align_up(sizeof(Stamp));
     L.off_ctrl = off;
     off += align_up(sizeof(Control));
+    L.off_ctrl_num = off;   // next to the stamp and the control block: the three are read back in one copy
+    off += align_up(sizeof(Control));
     L.off_pref = off;
     off += align_up(sizeof(int64_t) * (nnz_a + 1));
     L.off_row_nnz = off;
@@ -232,8 +235,6 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o, size_t 
         L.row_words = (L.row_words + 63) / 64 * 64;
         L.cache_rows = std::min<int64_t>(m, kStructCacheBytes / (L.row_words * 4));
     }
-    L.off_ctrl_num = off;
-    if (L.cache_rows > 0) off += align_up(sizeof(Control));
     L.off_perm_num = off;
     if (L.cache_rows > 0) off += align_up(sizeof(int32_t) * m);
     L.off_slot = off;
@@ -268,6 +269,7 @@ struct Ctx {
     int32_t *perm_num;
     const int32_t *bins;      // numeric phase: the row ids grouped by bin it uses (perm or perm_num)
     bool wtab_ready = false;  // numeric phase: the window table is the one the symbolic phase built
+    bool rrows_ready = false; // numeric phase: the dense rows' descriptions are the symbolic phase's
     Control host;
     Stamp host_stamp;
 };
@@ -409,16 +411,23 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
     LAUNCH_CHECK("zero_words");
     c.bins = c.perm;
     c.wtab_ready = false;
+    c.rrows_ready = false;
     if (numeric && c.L.cache_rows > 0 && !c.o.validate) {
         // The symbolic phase on the same workspace may have binned the rows by this C.row_ptr already: check
         // its stamp (with C.row_ptr's checksum) and take its bins if they were made with these settings
         rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, m, &c.ctrl->rp_sum);
         LAUNCH_CHECK("stamp");
-        Control kept;
-        HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
-        HIP_TRY(hipMemcpyAsync(&c.host_stamp, c.stamp, sizeof(Stamp), hipMemcpyDeviceToHost, c.st));
-        HIP_TRY(hipMemcpyAsync(&kept, c.ctrl_num, sizeof(Control), hipMemcpyDeviceToHost, c.st));
+        // the stamp, the control block and the kept binning, adjacent in the workspace, in one copy
+        static_assert(sizeof(Stamp) <= kAlign * 2, "stamp region");
+        const size_t span = c.L.off_ctrl_num + sizeof(Control) - c.L.off_stamp;
+        thread_local std::vector<char> back;
+        back.resize(span);
+        HIP_TRY(hipMemcpyAsync(back.data(), c.ws + c.L.off_stamp, span, hipMemcpyDeviceToHost, c.st));
         HIP_TRY(hipStreamSynchronize(c.st));
+        Control kept;
+        std::memcpy(&c.host_stamp, back.data(), sizeof(Stamp));
+        std::memcpy(&c.host, back.data() + (c.L.off_ctrl - c.L.off_stamp), sizeof(Control));
+        std::memcpy(&kept, back.data() + (c.L.off_ctrl_num - c.L.off_stamp), sizeof(Control));
         const BinCfg cfg = numeric_bin_cfg(c, B);
         const Stamp &h = c.host_stamp;
         if (stamp_matches(c, A, B) && h.num_bins == 1 && h.nb_dense_min_nnz == cfg.dense_min_nnz &&
@@ -429,6 +438,7 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
             c.host.rp_sum = rp_sum;
             c.bins = c.perm_num;
             c.wtab_ready = h.wtab == 1;
+            c.rrows_ready = h.wtab == 1;   // built with the window table
             if ((s = timer_stop(c, kSlotAnalysis)) != WINGSPAN_OK) return s;
             const int64_t slab_limit = c.L.slab_cap / 2;
             if (c.host.spill_max_bound > slab_limit)
@@ -441,8 +451,9 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
         zero_words<<<blocks_for(words, 256), 256, 0, c.st>>>(reinterpret_cast<int32_t *>(c.ctrl), words);
         LAUNCH_CHECK("zero_words");
     }
-    if (mode == kModeSymbolic) {
-        // the structure cache is being rewritten: invalid until this phase completes
+    if (mode == kModeSymbolic || mode == kModeSharded) {
+        // the structure cache (and what the symbolic phase keeps for the numeric one) is being rewritten:
+        // invalid until a symbolic phase completes
         write_stamp<<<1, 1, 0, c.st>>>(c.stamp, Stamp{});
     } else if (numeric && c.L.cache_rows > 0) {
         rowptr_checksum<<<64, 256, 0, c.st>>>(c_rp, m, &c.ctrl->rp_sum);
@@ -741,6 +752,9 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
             const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
             build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows,
                                                                            c.L.nwin, c.L.wcols, c.wtab);
+            // and the descriptions of the numeric phase's dense rows (their cache slots are this phase's)
+            rank_rows_of_bins<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(c.perm_num, c.ctrl_num, A->row_ptr, c_rp,
+                                                                           c.slot_of_row, c.rrows);
             LAUNCH_CHECK("build_window_table");
         }
         // the cache is complete: stamp it with the inputs, the layout, the bins' settings and C.row_ptr's
@@ -817,8 +831,9 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if (cnt && c.L.rank_mode) {
         const bool cached = stamp_matches(c, A, B);
         stats.structure_cache_rows = cached ? c.host_stamp.cached_rows : 0;
-        rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, c_rp,
-                                                            cached ? c.slot_of_row : nullptr, c.rrows);
+        if (!c.rrows_ready || !cached)
+            rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, c_rp,
+                                                                cached ? c.slot_of_row : nullptr, c.rrows);
         LAUNCH_CHECK("rank rows");
         const uint32_t *cache = cached ? c.cache : nullptr;
         if (!c.o.wide_offsets && offsets_fit_32<V>(B))

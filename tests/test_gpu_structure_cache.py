@@ -189,3 +189,19 @@ def test_numeric_settings_differ_from_symbolic(change):
     got2, num2 = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, DENSE)
     assert_matches(got2, ref, A.val.dtype, what="numeric with the symbolic settings")
     assert num2["structure_cache_rows"] > 0 and num2["rows"]["dense"] > 0
+
+
+def test_single_pass_between_phases_invalidates_the_kept_state():
+    # the single pass (sharded output) reuses the workspace's row tables; a numeric phase after it on the same
+    # workspace must not take the symbolic phase's kept state, and still matches the oracle
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(11, 16, seed=63, dtype=np.float32)
+    dA = _dev(A)
+    ref = oracle.spgemm(A, A)
+    wsb, nbytes = _workspace(dA, dA, DENSE)
+    c_rp, nnz = _symbolic(dA, dA, wsb, nbytes, DENSE)
+    S = ws.spgemm_sharded(dA, dA, options=ws.make_options(**DENSE), workspace=wsb)
+    assert S.nnz == nnz
+    got, num = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, DENSE)
+    assert num["structure_cache_rows"] == 0
+    assert_matches(got, ref, A.val.dtype, what="numeric after a single pass")
