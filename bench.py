@@ -15,6 +15,8 @@ input, writing into a preallocated C. Prints one JSON line:
                  algorithmic GB/s against peak, the dominant kernel, and the CPU
                  oracle on the same workload (all rows, or a row sample)
   sharded_single_pass  the single pass with sharded output on the same workload
+  forced_spill   the global-memory spill tier with every row above the
+                 register tier forced to it
   elementwise    SpAdd and the Hadamard product (B = A, and B a shuffled copy)
                  on the R-MAT scale-20 matrix, against HBM bandwidth
   spmspv         y = A x on the same matrix with x 10% stored
@@ -119,7 +121,7 @@ def cpu_baseline(A, B, fraction: float, seed: int):
     )
 
 
-def sharded_pass(ws, torch, dA, dB, nnz_c, P, steps, warmup):
+def sharded_pass(ws, torch, dA, dB, nnz_c, P, steps, warmup, gather=True):
     """The single pass with sharded output on the same workload: each row of C
     claims its pool segment when it is done (no symbolic phase). Timed with
     HIP events on its stream, pool sized to nnz(C); the gather into plain CSR
@@ -153,21 +155,64 @@ def sharded_pass(ws, torch, dA, dB, nnz_c, P, steps, warmup):
         ms.append(e0.elapsed_time(e1))
         for t in ws.TIERS:
             tiers[t].append(st["kernel_ms"][t])
-    # gather into CSR
-    S = ws.ShardedCSR(m, dB.ncols, row_off[:m], row_nnz[:m], pool_col, pool_val, nnz_c)
-    ws.sharded_to_csr(S)
-    torch.cuda.synchronize()
-    e0.record()
-    C = ws.sharded_to_csr(S)
-    e1.record()
-    e1.synchronize()
-    to_csr_ms = e0.elapsed_time(e1)
-    del C
+    # gather into CSR (needs a second copy of C beside the pool)
+    to_csr_ms = None
+    if gather:
+        S = ws.ShardedCSR(m, dB.ncols, row_off[:m], row_nnz[:m], pool_col, pool_val, nnz_c)
+        ws.sharded_to_csr(S)
+        torch.cuda.synchronize()
+        e0.record()
+        C = ws.sharded_to_csr(S)
+        e1.record()
+        e1.synchronize()
+        to_csr_ms = round(e0.elapsed_time(e1), 4)
+        del C
     t = float(np.mean(ms))
     return dict(ms=round(t, 4), ms_min=round(float(np.min(ms)), 4), GFLOPs=round(2.0 * P / (t / 1e3) / 1e9, 2),
                 tier_ms={k: round(float(np.mean(v)), 4) for k, v in tiers.items()},
                 tier_rows={k: int(st["rows"][k]) for k in ws.TIERS},
-                to_csr_ms=round(to_csr_ms, 4), pool_entries=nnz_c)
+                to_csr_ms=to_csr_ms, pool_entries=nnz_c)
+
+
+def forced_spill_pass(ws, torch, dA, dB, steps, warmup):
+    """The global-memory spill tier on a workload: every row above the
+    register tier forced to it (options.force_spill), symbolic and numeric
+    phases timed with HIP events, per-tier times from the library's events."""
+    dev = dA.row_ptr.device
+    Ad, Bd, dt = dA.desc(), dB.desc(), dA.dtype_code
+    opts = ws.make_options(force_spill=1)
+    topts = ws.make_options(force_spill=1, timing=1)
+    wsb, nbytes = ws.allocate_workspace(dA, dB, opts)
+    h = torch.cuda.current_stream().cuda_stream
+    c_rp = torch.empty(dA.nrows + 1, dtype=torch.int64, device=dev)
+    nnz = ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
+    c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    c_val = torch.empty(max(nnz, 1), dtype=dA.val.dtype, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+
+    def step(o):
+        ev[0].record()
+        ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, o)
+        ev[1].record()
+        ws.wingspan_spgemm_numeric(Ad, Bd, dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(), wsb.data_ptr(),
+                                   nbytes, h, o)
+        ev[2].record()
+        ev[2].synchronize()
+        return ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+
+    for _ in range(warmup):
+        step(opts)
+    t = [step(opts) for _ in range(steps)]
+    step(topts)
+    num = ws.wingspan_last_stats(1)
+    sym = ws.wingspan_last_stats(0)
+    P = int(sym["total_products"])
+    ts, tn = float(np.mean([x[0] for x in t])), float(np.mean([x[1] for x in t]))
+    return dict(symbolic_ms=round(ts, 3), numeric_ms=round(tn, 3), GFLOPs=round(2.0 * P / ((ts + tn) / 1e3) / 1e9, 2),
+                spill_rows=int(num["rows"]["spill"]), spill_products=int(num["products"]["spill"]),
+                spill_launches=int(num["launches"]["spill"]),
+                numeric_spill_kernel_ms=round(float(num["kernel_ms"]["spill"]), 3),
+                symbolic_spill_kernel_ms=round(float(sym["kernel_ms"]["spill"]), 3))
 
 
 def ew_alg_bytes(m, na, nb, nc, s, op):
@@ -457,6 +502,10 @@ def cpu_oracle_config(A, B, trials: int, fraction: float, seed: int):
                 sample=sample)
 
 
+# workloads whose single pass is timed beside their two-phase step (R-MAT 20: its dense rows span several
+# 262144-column regions, so the single pass sends them to the spill tier)
+SHARDED_CONFIGS = ("rmat20",)
+
 CONFIG_CPU = {   # CPU oracle per workload: (trials, fraction of rows), each run about 0.1-10 s
     "er1000": (3, 1.0),
     "laplace512": (3, 1.0),
@@ -483,6 +532,7 @@ def main():
     ap.add_argument("--no-spmspv", action="store_true", help="skip the SpMSpV timing")
     ap.add_argument("--no-outer", action="store_true", help="skip the outer-product SpGEMM timing")
     ap.add_argument("--outer-workload", default="laplace512", help="the workload of the outer-product timing")
+    ap.add_argument("--no-spill", action="store_true", help="skip the forced spill-tier timing")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other SpGEMM workloads (timed beside the headline one in `configs`)")
     ap.add_argument("--config-steps", type=int, default=5, help="timed steps per other workload")
@@ -572,6 +622,10 @@ def main():
         sh["vs_two_phase_step"] = round(res["ms_per_step"] / sh["ms"], 3)
         sh["vs_two_phase_step_with_gather"] = round(res["ms_per_step"] / (sh["ms"] + sh["to_csr_ms"]), 3)
         out["sharded_single_pass"] = sh
+    if not args.no_spill:
+        log("timing the spill tier (every row above the register tier forced to it)")
+        torch.cuda.empty_cache()
+        out["forced_spill"] = forced_spill_pass(ws, torch, dA, dB, max(2, args.steps // 3), 1)
     del dA, dB
     torch.cuda.empty_cache()
     if not (args.no_elementwise and args.no_spmspv):
@@ -603,8 +657,18 @@ def main():
             t0 = time.time()
             Ac, Bc = matgen.config(name)
             log(f"timing {name}: m={Ac.nrows} nnz(A)={Ac.nnz} (generated in {time.time() - t0:.1f}s)")
-            r, _ = measure_spgemm(ws, torch, Ac, Bc, dev, args.config_steps, 1)
+            r, (dAc, dBc) = measure_spgemm(ws, torch, Ac, Bc, dev, args.config_steps, 1)
             r["workload"] = f"{name}: {ccfg['desc']}"
+            torch.cuda.empty_cache()
+            if name in SHARDED_CONFIGS and not args.no_sharded:
+                log(f"timing the single pass with sharded output on {name}")
+                c_bytes = r["nnz_c"] * (4 + (4 if Ac.val.dtype == np.float32 else 8))
+                sh = sharded_pass(ws, torch, dAc, dBc, r["nnz_c"], r["products"], 2, 1, gather=2 * c_bytes < 150e9)
+                sh["vs_two_phase_step"] = round(r["ms_per_step"] / sh["ms"], 3)
+                if sh["to_csr_ms"] is not None:
+                    sh["vs_two_phase_step_with_gather"] = round(r["ms_per_step"] / (sh["ms"] + sh["to_csr_ms"]), 3)
+                r["sharded_single_pass"] = sh
+            del dAc, dBc
             torch.cuda.empty_cache()
             if not args.no_cpu_baseline:
                 trials, frac = CONFIG_CPU[name]

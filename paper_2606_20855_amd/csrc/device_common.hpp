@@ -34,7 +34,6 @@ enum : int32_t {
     kErrProbeExhausted = 1,   // a hash table filled up (structure larger than C.row_ptr says)
     kErrRowMismatch = 2,      // a row produced a different entry count than C.row_ptr
     kErrInvalidMatrix = 4,    // validation found a non-canonical input
-    kErrPoolLayout = 8,       // a kernel was given rows it cannot write to a pool (host routing error)
 };
 
 // Record of what the last symbolic phase left in the workspace for the
@@ -65,7 +64,7 @@ struct Control {
     int64_t spill_max_bound;
     int64_t c_nnz;
     unsigned long long pool_claimed;   // single pass: pool entries the rows have claimed
-    int32_t spill_next;
+    int32_t spill_next[kNumClasses];   // the spill tier's row claims, one counter per size class
     int32_t error_flags;
     int32_t has_zero_values;   // some A or B value could give a zero product
     int32_t rank_next;         // the rank kernel's row claims

@@ -878,11 +878,6 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries], e_hi[kCacheEntries];
     __shared__ double e_av[kCacheEntries];
 
-    // pool output needs a row's entry count before its first write: one region only
-    if (POOL && nwin > SH::REGION_WINS) {
-        if (threadIdx.x == 0) atomicOr(&ctrl->error_flags, kErrPoolLayout);
-        return;
-    }
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     const int ln = lane_id();
     const int64_t stride = static_cast<int64_t>(nwin) + 1;
@@ -959,6 +954,39 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             row_seg = POOL ? 0 : uniform(static_cast<int64_t>(n_hi.y));
         };
 
+        // Pool output needs the row's entry count before its first write. A row of one region claims once that
+        // region's count is known (below); a row spanning several regions counts its entries first, region by
+        // region (a structure pass and a popcount each), and claims the total here.
+        const bool multi_region = nwin > SH::REGION_WINS;
+        if constexpr (POOL) {
+            if (multi_region) {
+                int total = 0;
+                for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
+                    const int rg1 = nwin - rg0 < SH::REGION_WINS ? nwin : rg0 + SH::REGION_WINS;
+                    const int64_t col0 = static_cast<int64_t>(rg0) * kRankWinCols;
+                    const int ncw =
+                        static_cast<int>(ncols - col0 < SH::REGION_COLS ? ncols - col0 : SH::REGION_COLS);
+                    const int nwords = (ncw + 31) >> 5;
+                    // the previous row's copy reads the bitmap words until every wave has left it
+                    __syncthreads();
+                    for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
+                    __syncthreads();
+                    for_each_product_wg<BLOCK, V, false, true, true>(
+                        M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val, mark,
+                        ctot, [&](int col, double) {
+                            const int rel = static_cast<int>(col - col0);
+                            atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
+                        });
+                    int cnt = 0;
+                    for (int i = threadIdx.x; i < nwords; i += BLOCK) cnt += __popc(bw[i].x);
+                    total += block_sum<BLOCK>(cnt, scratch);
+                }
+                if (threadIdx.x == 0) s_claim[0] = out.claim(row, total, &s_claim[1]);
+                __syncthreads();
+                cb = uniform(s_claim[0]);
+                seg = uniform(s_claim[1]);
+            }
+        }
         int64_t done = 0;   // entries of the row emitted in earlier regions
         for (int rg0 = 0; rg0 < nwin; rg0 += SH::REGION_WINS) {
             const int rg1 = nwin - rg0 < SH::REGION_WINS ? nwin : rg0 + SH::REGION_WINS;
@@ -1078,9 +1106,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
 #pragma unroll
             for (int i = 0; i < NW; ++i) region_total += scratch[i];
             region_total = uniform(region_total);
-            if (POOL && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
+            if (POOL && !multi_region && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
             __syncthreads();
-            if (POOL) {
+            if (POOL && !multi_region) {
                 cb = uniform(s_claim[0]);
                 seg = uniform(s_claim[1]);
             }
@@ -1246,11 +1274,13 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
 
 // ---------------------------------------------------------------------------
 // Spill tier: persistent workgroups, each owning one slab of a bounded global
-// pool (keys then doubles, slab_cap slots each). A workgroup claims rows from
-// a shared counter (the dynamic schedule: whoever finishes takes the next
-// row), builds the row's hash table in its slab with global atomics, and in
-// the numeric phase compacts the table into the row of C and merge-sorts it
-// there, using the slab as the merge buffer.
+// pool (keys then doubles, slab_cap slots each). A launch takes the rows of one
+// size class, with slabs sized for that class's largest table, so small rows
+// run many workgroups at once and only the heaviest share few large slabs. A
+// workgroup claims rows from the class's counter (the dynamic schedule:
+// whoever finishes takes the next row), builds the row's hash table in its
+// slab with global atomics, and in the numeric phase compacts the table into
+// the row of C and merge-sorts it there, using the slab as the merge buffer.
 // ---------------------------------------------------------------------------
 constexpr int kSpillBlock = 512;
 constexpr int kRunLen = 2048;      // LDS-sorted run length
@@ -1447,7 +1477,7 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
     Mats<V> M, const int32_t *__restrict__ rows, int32_t nrows, const int64_t *__restrict__ pref,
     int64_t ncols, char *__restrict__ pool, int64_t slab_cap, int32_t *__restrict__ row_nnz,
     RowSink out, int32_t *__restrict__ c_col, V *__restrict__ c_val,
-    Control *ctrl) {
+    Control *ctrl, int32_t *next) {
     constexpr int NW = kSpillBlock / kWave;
     __shared__ int32_t s_row;
     __shared__ int64_t s_claim[2];   // pool output: the row's first entry and writable length
@@ -1467,7 +1497,7 @@ __global__ void __launch_bounds__(kSpillBlock) spill_kernel(
     // exit is uniform across the workgroup (every barrier below is reached by
     // all waves with all lanes active).
     for (;;) {
-        if (threadIdx.x == 0) s_row = atomicAdd(&ctrl->spill_next, 1);
+        if (threadIdx.x == 0) s_row = atomicAdd(next, 1);
         __syncthreads();
         const int ri = uniform(s_row);
         __syncthreads();

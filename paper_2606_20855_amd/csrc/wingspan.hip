@@ -44,9 +44,10 @@ constexpr int64_t kStructCacheBytes = int64_t(4) << 30;   // dense-row bitmaps k
 // pass, cheaper than a numeric hash table of 2^12 slots or more.
 constexpr int64_t kCachedDenseMin = 2048;
 constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
-constexpr int64_t kPoolBytes = int64_t(256) << 20;
+constexpr int64_t kPoolBytes = int64_t(1) << 30;   // spill pool: at most this, unless one table needs more
 constexpr int64_t kMaxSlabCap = int64_t(1) << 27;
-constexpr int kMaxSlabs = 256;
+constexpr int kMaxSlabs = 256;                      // largest tables the pool holds at once (at most)
+constexpr int64_t kMaxSpillGrid = 8192;             // spill workgroups per size class at most
 constexpr size_t kAlign = 256;
 
 thread_local std::string g_err;
@@ -177,8 +178,8 @@ struct Layout {
     int nwin;          // numeric dense windows per row (0: dense numeric tier unavailable)
     int wcols;         // columns per window of the window table
     bool rank_mode;    // dense numeric rows use the rank-indexed kernel
-    int64_t slab_cap;  // spill slab slots
-    int nslab;
+    int64_t slab_cap;    // slots of the largest spill table (a row beyond slab_cap / 2 entries is refused)
+    int64_t pool_bytes;  // the spill pool
 };
 
 // budget > 0: the layout must fit `budget` bytes (the static scratch of the
@@ -220,12 +221,12 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o, size_t 
     L.off_pool = off;
     L.slab_cap = std::min(kMaxSlabCap, std::max<int64_t>(64, next_pow2(2 * std::max<int64_t>(n, 1))));
     const int64_t slab_bytes = L.slab_cap * 12;
-    L.nslab = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxSlabs, kPoolBytes / slab_bytes)));
+    L.pool_bytes = std::max<int64_t>(slab_bytes, std::min<int64_t>(kPoolBytes, kMaxSlabs * slab_bytes));
     if (budget > 0) {
         const int64_t left = budget > off ? static_cast<int64_t>(budget - off) : 0;
-        L.nslab = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(L.nslab, left / slab_bytes)));
+        L.pool_bytes = std::max<int64_t>(slab_bytes, std::min<int64_t>(L.pool_bytes, left / 256 * 256));
     }
-    off += align_up(static_cast<size_t>(slab_bytes) * L.nslab);
+    off += align_up(static_cast<size_t>(L.pool_bytes));
     // structure cache: the symbolic phase's column bitmaps of dense rows, reused by the rank-indexed numeric
     // kernel; rows beyond kStructCacheBytes run their own structure pass
     L.cache_rows = 0;
@@ -504,8 +505,9 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
     } else if (mode == kModeSymbolic) {
         cfg.dense_ok = !c.o.dense_disabled && B->ncols <= kBitmapMaxCols;
     } else {
-        // the rank kernel writes a pool row once its count is known: rows of one region only (others spill)
-        cfg.dense_ok = c.L.rank_mode && c.L.nwin > 0 && c.L.nwin <= RankShape<float>::REGION_WINS;
+        // the rank kernel writes a pool row once its count is known (a row of several regions counts them
+        // first)
+        cfg.dense_ok = c.L.rank_mode && c.L.nwin > 0;
         // without a structure cache the LDS hash is the cheaper tier wherever it fits
         cfg.dense_min_nnz = c.o.dense_min_explicit ? c.o.dense_min_nnz : INT64_MAX;
     }
@@ -663,6 +665,32 @@ void launch_dense(int wcols, bool sentinel, unsigned grid, hipStream_t st, const
         launch_dense_w<16384, V>(sentinel, grid, st, M, rows, wtab, nwin, ncols, c_rp, c_col, c_val, ctrl);
 }
 
+// The spill tier, one launch per size class (heaviest first). Class k holds
+// rows with fewer than 2^(26-k) products (k >= 1; class 0 is unbounded), whose
+// tables hold nextpow2(2 * min(products, ncols)) slots at most: the class's
+// slabs are that size (or the largest table, slab_cap), and as many
+// workgroups run as the pool holds slabs.
+template <typename V, bool NUM>
+wingspan_status launch_spill(Ctx &c, const Mats<V> &M, const int32_t *perm, int64_t ncols, int32_t *row_nnz,
+                             const RowSink &out, int32_t *c_col, V *c_val, int32_t *launches) {
+    for (int k = 0; k < kNumClasses; ++k) {
+        const int b = kBinSpill0 + k;
+        const int32_t cnt = c.host.bin_count[b];
+        if (!cnt) continue;
+        int64_t slab = c.L.slab_cap;
+        if (k >= 1 && 26 - k < 62) slab = std::min<int64_t>(slab, std::max<int64_t>(64, int64_t(1) << (27 - k)));
+        const int64_t fits = c.L.pool_bytes / (slab * 12);
+        const unsigned grid = static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>({int64_t(cnt), fits,
+                                                                                             kMaxSpillGrid})));
+        spill_kernel<V, NUM><<<grid, kSpillBlock, 0, c.st>>>(M, perm + c.host.bin_offset[b], cnt, c.pref, ncols,
+                                                             c.pool, slab, row_nnz, out, c_col, c_val, c.ctrl,
+                                                             &c.ctrl->spill_next[k]);
+        ++*launches;
+        LAUNCH_CHECK("spill");
+    }
+    return WINGSPAN_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Phases.
 // ---------------------------------------------------------------------------
@@ -721,15 +749,9 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
     if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
 
     if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
-    bin_range(c, kBinSpill0, kNumClasses, &start, &cnt);
-    if (cnt) {
-        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
-        spill_kernel<float, false><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols,
-                                                                  c.pool, c.L.slab_cap, c.row_nnz, RowSink{},
-                                                                  nullptr, nullptr, c.ctrl);
-        stats.launches[WINGSPAN_TIER_SPILL]++;
-        LAUNCH_CHECK("spill symbolic");
-    }
+    s = launch_spill<float, false>(c, M, perm, B->ncols, c.row_nnz, RowSink{}, nullptr, nullptr,
+                                   &stats.launches[WINGSPAN_TIER_SPILL]);
+    if (s != WINGSPAN_OK) return s;
     if ((s = timer_stop(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
 
     s = run_scan(c, CountIn{c.row_nnz}, A->nrows, c_rp);
@@ -853,14 +875,9 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
 
     if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
-    bin_range(c, kBinSpill0, kNumClasses, &start, &cnt);
-    if (cnt) {
-        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
-        spill_kernel<V, true><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols, c.pool,
-                                                             c.L.slab_cap, nullptr, sink, c_col, c_val, c.ctrl);
-        stats.launches[WINGSPAN_TIER_SPILL]++;
-        LAUNCH_CHECK("spill numeric");
-    }
+    s = launch_spill<V, true>(c, M, perm, B->ncols, nullptr, sink, c_col, c_val,
+                              &stats.launches[WINGSPAN_TIER_SPILL]);
+    if (s != WINGSPAN_OK) return s;
     if ((s = timer_stop(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
 
     if (c.o.validate) {
@@ -934,8 +951,8 @@ wingspan_status sharded_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     }
     if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     if (cnt) {
-        // binning sends dense rows here only in rank mode with one region; the column bitmaps come from the
-        // kernel's own structure pass
+        // binning sends dense rows here only in rank mode; the column bitmaps come from the kernel's own
+        // structure pass
         rank_rows<<<blocks_for(cnt, 256), 256, 0, c.st>>>(perm + start, cnt, A->row_ptr, nullptr, nullptr,
                                                             c.rrows);
         LAUNCH_CHECK("rank rows");
@@ -953,23 +970,15 @@ wingspan_status sharded_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
 
     if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
-    bin_range(c, kBinSpill0, kNumClasses, &start, &cnt);
-    if (cnt) {
-        const unsigned grid = static_cast<unsigned>(std::min<int64_t>(c.L.nslab, cnt));
-        spill_kernel<V, true><<<grid, kSpillBlock, 0, c.st>>>(M, perm + start, cnt, c.pref, B->ncols, c.pool,
-                                                             c.L.slab_cap, nullptr, sink, pool_col, pool_val,
-                                                             c.ctrl);
-        stats.launches[WINGSPAN_TIER_SPILL]++;
-        LAUNCH_CHECK("spill single pass");
-    }
+    s = launch_spill<V, true>(c, M, perm, B->ncols, nullptr, sink, pool_col, pool_val,
+                              &stats.launches[WINGSPAN_TIER_SPILL]);
+    if (s != WINGSPAN_OK) return s;
     if ((s = timer_stop(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
 
     HIP_TRY(hipMemcpyAsync(&c.host, c.ctrl, sizeof(Control), hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
     if (c.host.error_flags & kErrProbeExhausted)
         return fail(WINGSPAN_ERR_INCONSISTENT, "a row's hash table filled up (flags %d)", c.host.error_flags);
-    if (c.host.error_flags & kErrPoolLayout)
-        return fail(WINGSPAN_ERR_INCONSISTENT, "a dense row spans several regions (flags %d)", c.host.error_flags);
     const int64_t total = static_cast<int64_t>(c.host.pool_claimed);
     *used = total;
     stats.c_nnz_total = total;

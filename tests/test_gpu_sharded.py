@@ -124,14 +124,52 @@ def test_arrowhead_dense_rows(dtype):
 
 
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
-def test_wide_rows_spill_to_pool(dtype):
-    # 300K columns: more than one rank region, so the single pass sends the
-    # long rows to the spill tier, which claims after its count
+@pytest.mark.parametrize("opts", [None, dict(force_spill=1)], ids=["rank", "spill"])
+def test_wide_rows_to_pool(dtype, opts):
+    # 300K columns: more than one rank region. The rank kernel counts such a
+    # row region by region, claims its pool segment, then writes it region by
+    # region; forced to the spill tier, the row claims after its hash count
     dist = "pm1" if dtype == np.float64 else "open01"
     A = matgen.er(24, 2500, 300, seed=63, dtype=dtype, dist=dist)
     B = matgen.er(2500, 300_000, 30, seed=64, dtype=dtype, dist=dist)
-    S, st, ref = check(A, B, what="wide rows")
-    assert st["rows"]["dense"] == 0 and st["rows"]["spill"] > 0
+    S, st, ref = check(A, B, opts, what="wide rows")
+    if opts is None:
+        assert st["rows"]["dense"] == 24 and st["rows"]["spill"] == 0
+    else:
+        assert st["rows"]["dense"] == 0 and st["rows"]["spill"] > 0
+
+
+def test_wide_rows_pool_too_small():
+    # multi-region rows claim their whole row at once: with the pool a third
+    # of C, the rows that fit are complete and nothing is written past it
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.er(40, 2500, 300, seed=68, dtype=np.float64)
+    B = matgen.er(2500, 600_000, 30, seed=69, dtype=np.float64)
+    ref = oracle.spgemm(A, B)
+    dA, dB = _dev(A), _dev(B)
+    nbytes = ws.wingspan_spgemm_workspace_size(dA.desc(), dB.desc(), ws.F64)
+    wsb = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    m = A.nrows
+    row_off = torch.empty(m, dtype=torch.int64, device="cuda:0")
+    row_nnz = torch.empty(m, dtype=torch.int32, device="cuda:0")
+    cap = ref.nnz // 3
+    guard = 4096
+    pool_col = torch.full((cap + guard,), -7, dtype=torch.int32, device="cuda:0")
+    pool_val = torch.full((cap + guard,), 3.5, dtype=torch.float64, device="cuda:0")
+    st, used = ws.wingspan_spgemm_sharded(dA.desc(), dB.desc(), ws.F64, row_off.data_ptr(), row_nnz.data_ptr(),
+                                          pool_col.data_ptr(), pool_val.data_ptr(), cap, wsb.data_ptr(), nbytes,
+                                          0, None, check=False)
+    torch.cuda.synchronize()
+    assert ws.STATUS[st] == "WINGSPAN_ERR_INSUFFICIENT_CAPACITY"
+    assert used == ref.nnz
+    assert np.array_equal(row_nnz.cpu().numpy(), np.diff(ref.row_ptr))
+    assert torch.all(pool_col[cap:] == -7) and torch.all(pool_val[cap:] == 3.5)
+    off, cnt, col = row_off.cpu().numpy(), row_nnz.cpu().numpy(), pool_col.cpu().numpy()
+    fit = np.nonzero((cnt > 0) & (off + cnt <= cap))[0]
+    assert len(fit) > 0
+    for i in fit:
+        assert np.array_equal(col[off[i]:off[i] + cnt[i]], ref.col_idx[ref.row_ptr[i]:ref.row_ptr[i + 1]])
 
 
 def test_same_structure_as_two_phase():
