@@ -128,6 +128,43 @@ __global__ void __launch_bounds__(256) row_products_kernel(const int32_t *__rest
     if (i < m) out[i] = row_products_of(a_rp, pref, i);
 }
 
+// The same exclusive scan in one workgroup of 1024 threads, for short
+// sequences of cheap inputs (one launch instead of three): thread t sums its
+// contiguous share, the workgroup scans the shares, and each thread writes its
+// share's prefixes. out[n] = total.
+
+template <typename In>
+__global__ void __launch_bounds__(1024) scan_one_block(In in, int64_t n, int64_t *out) {
+    __shared__ int64_t wsum[16];
+    const int64_t per = (n + 1023) / 1024;
+    const int64_t b = static_cast<int64_t>(threadIdx.x) * per;
+    const int64_t e = b + per < n ? b + per : n;
+    int64_t s = 0;
+    for (int64_t i = b; i < e; ++i) s += in(i);
+    const int ln = lane_id();
+    const int w = threadIdx.x / kWave;
+    int64_t incl = s;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int64_t y = __shfl_up(incl, o, kWave);
+        if (ln >= o) incl += y;
+    }
+    if (ln == kWave - 1) wsum[w] = incl;
+    __syncthreads();
+    int64_t run = 0, tot = 0;
+    for (int i = 0; i < 16; ++i) {
+        run += i < w ? wsum[i] : 0;
+        tot += wsum[i];
+    }
+    run += incl - s;
+    for (int64_t i = b; i < e; ++i) {
+        const int64_t v = in(i);
+        out[i] = run;
+        run += v;
+    }
+    if (threadIdx.x == 0) out[n] = tot;
+}
+
 // ---------------------------------------------------------------------------
 // Binning.
 // ---------------------------------------------------------------------------

@@ -16,6 +16,7 @@
 // lengths), so long and short columns balance by themselves.
 #pragma once
 
+#include "analysis.hpp"
 #include "search.hpp"
 
 namespace wsp {
@@ -133,19 +134,65 @@ __global__ void __launch_bounds__(kSvBlock) sv_scatter(const int32_t *__restrict
     }
 }
 
-// Coalesces the map into y: a stored position i goes to y[pos[i]] (pos: the
-// exclusive prefix count of stored positions) when that is below cap; values
-// are rounded once to the value type.
+// The map is coalesced into y tile by tile: kSvTile positions per workgroup.
+// sv_tile_count counts a tile's stored positions (its flags read as 32-bit
+// words); once the counts are scanned (tile_pre, with the total at
+// tile_pre[ntiles]), sv_emit_tiles writes each tile's stored positions to
+// y[tile_pre[t] + rank within the tile] when that is below cap, values rounded
+// once to the value type.
+constexpr int kSvTile = 4096;
+constexpr int kSvTileBlock = 256;
+
+__global__ void __launch_bounds__(kSvTileBlock) sv_tile_count(const uint32_t *__restrict__ flag_words, int64_t m,
+                                                             int32_t *__restrict__ tile_cnt) {
+    __shared__ int32_t red[kSvTileBlock / kWave];
+    const int64_t w0 = static_cast<int64_t>(blockIdx.x) * (kSvTile / 4);
+    const int64_t nw = (m + 3) / 4;
+    int c = 0;
+    for (int k = threadIdx.x; k < kSvTile / 4; k += kSvTileBlock) {
+        const int64_t w = w0 + k;
+        if (w < nw) {
+            const uint32_t f = flag_words[w];   // one flag byte (0 or 1) per position
+            c += static_cast<int>((f & 1u) + ((f >> 8) & 1u) + ((f >> 16) & 1u) + (f >> 24));
+        }
+    }
+    c = block_sum<kSvTileBlock>(c, red);
+    if (threadIdx.x == 0) tile_cnt[blockIdx.x] = c;
+}
+
+struct SvTileIn {
+    const int32_t *cnt;
+    __device__ __forceinline__ int64_t operator()(int64_t t) const { return cnt[t]; }
+};
+
 template <typename V>
-__global__ void __launch_bounds__(256) sv_emit(const uint8_t *__restrict__ flag, const double *__restrict__ yval,
-                                               const int64_t *__restrict__ pos, int64_t m, int64_t cap,
-                                               int32_t *__restrict__ y_idx, V *__restrict__ y_val) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= m || flag[i] == 0) return;
-    const int64_t p = pos[i];
-    if (p < cap) {
-        y_idx[p] = static_cast<int32_t>(i);
-        y_val[p] = static_cast<V>(yval[i]);
+__global__ void __launch_bounds__(kSvTileBlock) sv_emit_tiles(const uint8_t *__restrict__ flag,
+                                                             const double *__restrict__ yval,
+                                                             const int64_t *__restrict__ tile_pre, int64_t m,
+                                                             int64_t cap, int32_t *__restrict__ y_idx,
+                                                             V *__restrict__ y_val) {
+    __shared__ int32_t scratch[kSvTileBlock / kWave];
+    constexpr int PER = kSvTile / kSvTileBlock;   // consecutive positions per thread
+    const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kSvTile + static_cast<int64_t>(threadIdx.x) * PER;
+    bool f[PER];
+    int c = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int64_t i = i0 + k;
+        f[k] = i < m && flag[i] != 0;
+        c += f[k];
+    }
+    int tot;
+    int64_t p = tile_pre[blockIdx.x] + block_excl_scan<kSvTileBlock>(c, &tot, scratch);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        if (f[k]) {
+            if (p < cap) {
+                y_idx[p] = static_cast<int32_t>(i0 + k);
+                y_val[p] = static_cast<V>(yval[i0 + k]);
+            }
+            ++p;
+        }
     }
 }
 

@@ -1108,26 +1108,31 @@ wingspan_status ew_values_impl(Ctx &c, int op, const wingspan_csr *A, const wing
 constexpr int64_t kSvMaxGrid = 8192;   // scatter workgroups at most (grid-stride beyond)
 
 struct SvLayout {
-    size_t off_err, off_pref, off_partials, off_flag, off_yval, off_pos, total;
+    size_t off_pref, off_partials, off_flag, off_yval, off_tiles, off_tile_pre, off_err, total;
+    int64_t ntiles;
 };
 
 SvLayout sv_plan(const wingspan_csr *At, int64_t nnz_x) {
     SvLayout L{};
     const int64_t m = std::max<int64_t>(At->ncols, 1), nx = std::max<int64_t>(nnz_x, 0);
+    L.ntiles = (m + kSvTile - 1) / kSvTile;
     size_t off = 0;
-    L.off_err = off;
-    off += align_up(sizeof(int32_t) * 4);
+    // first the tiles' prefix, its total (y's entry count) last, then the error word: the total and the error
+    // word are read back in one copy. (Measured: the scatter runs about 20% slower with these small arrays
+    // placed just past the map's accumulators.)
+    L.off_tile_pre = off;
+    L.off_err = off + sizeof(int64_t) * (L.ntiles + 1);
+    off += align_up(sizeof(int64_t) * (L.ntiles + 1) + sizeof(int64_t));
+    L.off_tiles = off;
+    off += align_up(sizeof(int32_t) * L.ntiles);
     L.off_pref = off;
     off += align_up(sizeof(int64_t) * (nx + 1));
     L.off_partials = off;
-    const int64_t n = std::max<int64_t>(nx, m + 1);
-    off += align_up(sizeof(int64_t) * ((n + kScanTile - 1) / kScanTile + 2));
+    off += align_up(sizeof(int64_t) * ((nx + kScanTile - 1) / kScanTile + 2));
     L.off_flag = off;
     off += align_up(static_cast<size_t>((m + 3) / 4) * 4);   // cleared as int32 words
     L.off_yval = off;
     off += align_up(sizeof(double) * m);
-    L.off_pos = off;
-    off += align_up(sizeof(int64_t) * (m + 1));
     L.total = off;
     return L;
 }
@@ -1150,7 +1155,8 @@ wingspan_status sv_impl(Ctx &c, const wingspan_csr *At, const SvLayout &L, const
     int64_t *pref = reinterpret_cast<int64_t *>(c.ws + L.off_pref);
     uint8_t *flag = reinterpret_cast<uint8_t *>(c.ws + L.off_flag);
     double *yval = reinterpret_cast<double *>(c.ws + L.off_yval);
-    int64_t *pos = reinterpret_cast<int64_t *>(c.ws + L.off_pos);
+    int32_t *tiles = reinterpret_cast<int32_t *>(c.ws + L.off_tiles);
+    int64_t *tile_pre = reinterpret_cast<int64_t *>(c.ws + L.off_tile_pre);
     *y_nnz = 0;
     if (m == 0) return WINGSPAN_OK;
     // an empty map; x's columns' lengths scanned (checking x on the way); the scatter, sized by At's entries
@@ -1159,34 +1165,39 @@ wingspan_status sv_impl(Ctx &c, const wingspan_csr *At, const SvLayout &L, const
     sv_clear<<<blocks_for(std::max<int64_t>(nwords, m), 256), 256, 0, c.st>>>(
         reinterpret_cast<int32_t *>(flag), nwords, reinterpret_cast<int64_t *>(yval), m, err);
     LAUNCH_CHECK("spmspv clear");
-    if (nnz_x > 0 && At->nnz > 0) {
+    if (nnz_x > 0) {
+        // (the tiled scan: one workgroup walking x would wait on each entry's two dependent loads in turn)
+        c.partials = reinterpret_cast<int64_t *>(c.ws + L.off_partials);
         wingspan_status s = run_scan(c, SvLenIn{At->row_ptr, x_idx, n, err}, nnz_x, pref);
         if (s != WINGSPAN_OK) return s;
-        const int64_t chunks = (At->nnz + kSvChunk - 1) / kSvChunk;
-        sv_scatter<V><<<static_cast<unsigned>(std::min<int64_t>(chunks, kSvMaxGrid)), kSvBlock, 0, c.st>>>(
-            At->row_ptr, At->col_idx, static_cast<const V *>(At->val), x_idx, x_val, static_cast<int>(nnz_x), pref,
-            err, flag, yval);
-        LAUNCH_CHECK("spmspv scatter");
-    } else if (nnz_x > 0) {
-        // no products; x is still checked
-        wingspan_status s = run_scan(c, SvLenIn{At->row_ptr, x_idx, n, err}, nnz_x, pref);
-        if (s != WINGSPAN_OK) return s;
+        if (At->nnz > 0) {
+            const int64_t chunks = (At->nnz + kSvChunk - 1) / kSvChunk;
+            sv_scatter<V><<<static_cast<unsigned>(std::min<int64_t>(chunks, kSvMaxGrid)), kSvBlock, 0, c.st>>>(
+                At->row_ptr, At->col_idx, static_cast<const V *>(At->val), x_idx, x_val, static_cast<int>(nnz_x),
+                pref, err, flag, yval);
+            LAUNCH_CHECK("spmspv scatter");
+        }
     }
-    wingspan_status s = run_scan(c, SvFlagIn{flag}, m, pos);
-    if (s != WINGSPAN_OK) return s;
-    sv_emit<V><<<blocks_for(m, 256), 256, 0, c.st>>>(flag, yval, pos, m, y_cap, y_idx, y_val);
+    // coalesce the map tile by tile: counts, their scan (the total lands next to the error word), then y
+    const unsigned nt = static_cast<unsigned>(L.ntiles);
+    sv_tile_count<<<nt, kSvTileBlock, 0, c.st>>>(reinterpret_cast<const uint32_t *>(flag), m, tiles);
+    scan_one_block<SvTileIn><<<1, 1024, 0, c.st>>>(SvTileIn{tiles}, L.ntiles, tile_pre);
+    sv_emit_tiles<V><<<nt, kSvTileBlock, 0, c.st>>>(flag, yval, tile_pre, m, y_cap, y_idx, y_val);
     LAUNCH_CHECK("spmspv emit");
-    int64_t total = 0;
-    int32_t herr = 0;
-    HIP_TRY(hipMemcpyAsync(&total, pos + m, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
-    HIP_TRY(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, c.st));
+    struct {
+        int64_t total;
+        int32_t err;
+        int32_t pad;
+    } back{};
+    static_assert(sizeof(back) == 16, "total then error word");
+    HIP_TRY(hipMemcpyAsync(&back, tile_pre + L.ntiles, sizeof(back), hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
-    if (herr) return fail(WINGSPAN_ERR_INVALID_MATRIX, "x's indices are not strictly increasing in [0, %lld)",
-                          (long long)n);
-    *y_nnz = total;
-    if (total > y_cap)
-        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "y has %lld entries but y_cap is %lld", (long long)total,
-                    (long long)y_cap);
+    if (back.err) return fail(WINGSPAN_ERR_INVALID_MATRIX, "x's indices are not strictly increasing in [0, %lld)",
+                              (long long)n);
+    *y_nnz = back.total;
+    if (back.total > y_cap)
+        return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "y has %lld entries but y_cap is %lld",
+                    (long long)back.total, (long long)y_cap);
     return WINGSPAN_OK;
 }
 
