@@ -58,7 +58,8 @@ typedef enum {
                                              > pool_capacity (wingspan_spgemm_sharded) */
     WINGSPAN_ERR_INVALID_MATRIX = 6,      /* non-canonical input detected (options->validate) */
     WINGSPAN_ERR_HIP = 7,                 /* a HIP runtime call failed; message has the HIP error */
-    WINGSPAN_ERR_UNSUPPORTED = 8,         /* a row is too long for the global spill pool */
+    WINGSPAN_ERR_UNSUPPORTED = 8,         /* a row is too long for the global spill pool, or the
+                                             outer product has more than 2^31 - 1 products */
     WINGSPAN_ERR_INCONSISTENT = 9         /* numeric found a row whose entry count differs from
                                              C.row_ptr (only reported when options->validate) */
 } wingspan_status;
@@ -365,10 +366,11 @@ wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, co
  * (dtype, shared with At.val and B.val; products and sums in double, rounded
  * once); *c_nnz (host) receives nnz(C). If nnz(C) > c_capacity it returns
  * WINGSPAN_ERR_INSUFFICIENT_CAPACITY with c_row_ptr_dev and *c_nnz valid and
- * the columns and values not written. A row of C that gathers more than 4096
- * partial entries from the workers' partial results, or more than 2^31 - 1
- * products in all, gives WINGSPAN_ERR_UNSUPPORTED (the Gustavson path takes
- * any row). The call synchronizes `stream` twice.
+ * the columns and values not written. Rows of any length are merged: a row
+ * whose partial entries exceed 4096 is sorted as runs of 4096 in LDS that are
+ * then merged pairwise in the workspace. More than 2^31 - 1 products in all
+ * gives WINGSPAN_ERR_UNSUPPORTED (the Gustavson path has no such bound). The
+ * call synchronizes `stream` twice.
  * ------------------------------------------------------------------------ */
 wingspan_status wingspan_outer_workspace_size(const wingspan_csr *At, const wingspan_csr *B, int64_t products,
                                               size_t *bytes);

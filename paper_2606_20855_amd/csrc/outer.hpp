@@ -11,7 +11,10 @@
 //      in LDS and sums equal coordinates: the workgroup's own partial C;
 //   2. coalesce: every partial entry moves to its row's bucket (the partial
 //      C's rows concatenated, in arbitrary order), then each row's bucket is
-//      sorted by column and equal columns summed, in place;
+//      sorted by column and equal columns summed: in registers up to 64
+//      entries, in LDS up to kOpRowCap, and beyond that as runs of kOpRowCap
+//      sorted in LDS then merged pairwise in global memory (merge path, each
+//      output tile merged in LDS);
 //   3. the compacted rows are scanned into C.row_ptr and gathered into CSR.
 // Products are formed and summed in double; values are rounded once.
 #pragma once
@@ -23,8 +26,9 @@ namespace wsp {
 constexpr int kOpChunk = 2048;     // products per workgroup (its partial C)
 constexpr int kOpBlock = 1024;     // threads of the expand kernel
 constexpr int kOpStage = 1024;     // k indices a chunk stages in LDS
-constexpr int kOpRowCap = 4096;    // longest row bucket the coalesce sorts (in LDS)
+constexpr int kOpRowCap = 4096;    // longest row bucket sorted whole in LDS; also the run and merge tile length
 constexpr int kOpRowBlock = 256;   // threads per long row in the coalesce
+constexpr int kOpHugeBlock = 1024; // threads per row past kOpRowCap
 constexpr int64_t kOpNoKey = 0x7fffffffffffffffll;
 
 // Products of rank-1 update k: |At_k| * |B_k|.
@@ -200,12 +204,12 @@ __global__ void __launch_bounds__(256) op_bucket(const int64_t *__restrict__ par
 }
 
 // 2b. Short buckets, S lanes per row (S = 32: buckets of at most 32 entries;
-// S = 64: 33 to 64, and the longer ones are listed for op_merge_long, those
-// beyond kOpRowCap setting kErrUnsupportedRow): sorted in registers (bitonic
-// through lane shuffles within the S-lane group), equal columns summed, written
-// back compacted from the bucket's start (columns in bkt_col, values rounded to
-// V in out_val).
-constexpr int32_t kErrUnsupportedRow = 16;
+// S = 64: 33 to 64, and the longer ones are listed: up to kOpRowCap from the
+// front of long_rows for op_merge_long (count in counters[0]), the rest from
+// its back for op_merge_huge (count in counters[2])): sorted in registers
+// (bitonic through lane shuffles within the S-lane group), equal columns
+// summed, written back compacted from the bucket's start (columns in bkt_col,
+// values rounded to V in out_val).
 
 template <int S, typename V>
 __global__ void __launch_bounds__(256) op_merge_short(const int64_t *__restrict__ bucket_off, int64_t m,
@@ -221,12 +225,10 @@ __global__ void __launch_bounds__(256) op_merge_short(const int64_t *__restrict_
     // this kernel's rows: lengths (S/2, S] (and 0 .. S/2 too when S = 32)
     const bool mine = row < m && len <= S && (S == 32 || len > S / 2);
     if (S == 64 && row < m && len > S && ln == 0) {
-        if (len > kOpRowCap) {
-            atomicOr(&counters[1], kErrUnsupportedRow);
-            row_nnz[row] = 0;
-        } else {
+        if (len > kOpRowCap)
+            long_rows[m - 1 - atomicAdd(&counters[2], 1)] = static_cast<int32_t>(row);
+        else
             long_rows[atomicAdd(&counters[0], 1)] = static_cast<int32_t>(row);
-        }
     }
     // a wave without a row of this kernel is done; in the others every group takes part in the shuffles
     if (ballot(mine) == 0ull) return;
@@ -315,6 +317,161 @@ __global__ void __launch_bounds__(kOpRowBlock) op_merge_long(const int64_t *__re
             ++pos;
         }
         if (threadIdx.x == 0) row_nnz[row] = total;
+        __syncthreads();   // LDS is reused by the next row
+    }
+}
+
+// Merge-path split of the stable merge of sorted a[0, na) and b[0, nb), a's
+// entries first among equal keys: the number of a's entries among the first d
+// outputs, i.e. the least i in [max(0, d - nb), min(d, na)] with
+// i = min(d, na) or a[i] > b[d - i - 1]. One wave (all 64 lanes call it)
+// evaluates 64 candidates per round; every lane returns the split.
+__device__ int64_t wave_merge_split(const int32_t *a, int64_t na, const int32_t *b, int64_t nb, int64_t d) {
+    int64_t lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
+    while (lo < hi) {
+        // lane l probes lo + (hi - lo) l / 64, all in [lo, hi): a[p] and b[d - p - 1] are in range
+        const int64_t span = hi - lo;
+        const int64_t p = lo + span * lane_id() / kWave;
+        const uint64_t t = ballot(a[p] > b[d - p - 1]);
+        if (t == 0ull) {
+            lo += span * (kWave - 1) / kWave + 1;
+        } else {
+            const int l = __ffsll(static_cast<long long>(t)) - 1;
+            hi = lo + span * l / kWave;
+            lo = l == 0 ? lo : lo + span * (l - 1) / kWave + 1;
+        }
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int lds_lower_bound(const int32_t *k, int n, int32_t key) {
+    int lo = 0, hi = n;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (k[mid] < key) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int lds_upper_bound(const int32_t *k, int n, int32_t key) {
+    int lo = 0, hi = n;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (k[mid] <= key) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// 2d. Buckets longer than kOpRowCap, a workgroup per row, rows taken
+// grid-stride from the back of long_rows (op_merge_short lists them there):
+//   runs of kOpRowCap entries are sorted in LDS into buffer X; then runs are
+//   merged pairwise, X to Y and back, doubling their length until one is left:
+//   each output tile of kOpRowCap entries takes its share of the two runs
+//   (merge-path splits at its ends), merges it in LDS by ranks and writes it
+//   out coalesced; last, the sorted row is compacted into the bucket's start
+//   as in the shorter tiers. X and Y hold a column array and a value array
+//   each, indexed like the bucket; y_val is bkt_val itself (the first step has
+//   read the row's bucket before the first merge overwrites it).
+template <typename V>
+__global__ void __launch_bounds__(kOpHugeBlock) op_merge_huge(const int64_t *__restrict__ bucket_off, int64_t m,
+                                                              int32_t *bkt_col, double *bkt_val, V *out_val,
+                                                              int32_t *__restrict__ row_nnz,
+                                                              const int32_t *__restrict__ long_rows,
+                                                              const int32_t *counters, int32_t *x_col, double *x_val,
+                                                              int32_t *y_col) {
+    __shared__ int32_t s_key[kOpRowCap];
+    __shared__ double s_val[kOpRowCap];
+    __shared__ int32_t o_key[kOpRowCap];
+    __shared__ double o_val[kOpRowCap];
+    __shared__ int64_t s_split[2];
+    __shared__ int s_scan[kOpHugeBlock / kWave];
+    const int nrows = counters[2];
+    for (int idx = blockIdx.x; idx < nrows; idx += gridDim.x) {
+        const int row = long_rows[m - 1 - idx];
+        const int64_t lo = bucket_off[row];
+        const int64_t len = bucket_off[row + 1] - lo;
+        // runs sorted in LDS, bucket -> X
+        for (int64_t r0 = 0; r0 < len; r0 += kOpRowCap) {
+            const int n = static_cast<int>(len - r0 < kOpRowCap ? len - r0 : kOpRowCap);
+            int np = kWave * 2;
+            while (np < n) np <<= 1;
+            for (int e = threadIdx.x; e < np; e += blockDim.x) {
+                s_key[e] = e < n ? bkt_col[lo + r0 + e] : 0x7fffffff;
+                s_val[e] = e < n ? bkt_val[lo + r0 + e] : 0.0;
+            }
+            __syncthreads();
+            lds_bitonic(s_key, s_val, np);
+            for (int e = threadIdx.x; e < n; e += blockDim.x) {
+                x_col[lo + r0 + e] = s_key[e];
+                x_val[lo + r0 + e] = s_val[e];
+            }
+            __syncthreads();
+        }
+        // pairwise merges, ping-pong between X and Y
+        int32_t *sc = x_col, *dc = y_col;
+        double *sv = x_val, *dv = bkt_val;
+        for (int64_t w = kOpRowCap; w < len; w <<= 1) {
+            for (int64_t s = 0; s < len; s += 2 * w) {
+                const int64_t na = len - s < w ? len - s : w;
+                const int64_t nb = len - s - na < w ? len - s - na : w;
+                const int32_t *ak = sc + lo + s, *bk = ak + na;
+                const double *av = sv + lo + s, *bv = av + na;
+                for (int64_t d0 = 0; d0 < na + nb; d0 += kOpRowCap) {
+                    const int64_t d1 = na + nb - d0 < kOpRowCap ? na + nb : d0 + kOpRowCap;
+                    if (threadIdx.x < 2 * kWave) {
+                        const int64_t i = wave_merge_split(ak, na, bk, nb, threadIdx.x < kWave ? d0 : d1);
+                        if (lane_id() == 0) s_split[threadIdx.x / kWave] = i;
+                    }
+                    __syncthreads();
+                    const int64_t i0 = s_split[0], i1 = s_split[1];
+                    const int sa = static_cast<int>(i1 - i0), nt = static_cast<int>(d1 - d0);
+                    const int64_t j0 = d0 - i0;
+                    for (int e = threadIdx.x; e < nt; e += blockDim.x) {
+                        s_key[e] = e < sa ? ak[i0 + e] : bk[j0 + (e - sa)];
+                        s_val[e] = e < sa ? av[i0 + e] : bv[j0 + (e - sa)];
+                    }
+                    __syncthreads();
+                    for (int e = threadIdx.x; e < nt; e += blockDim.x) {
+                        const int32_t key = s_key[e];
+                        const int pos = e < sa ? e + lds_lower_bound(s_key + sa, nt - sa, key)
+                                               : (e - sa) + lds_upper_bound(s_key, sa, key);
+                        o_key[pos] = key;
+                        o_val[pos] = s_val[e];
+                    }
+                    __syncthreads();
+                    for (int e = threadIdx.x; e < nt; e += blockDim.x) {
+                        dc[lo + s + d0 + e] = o_key[e];
+                        dv[lo + s + d0 + e] = o_val[e];
+                    }
+                    __syncthreads();   // s_split and the LDS tiles are reused
+                }
+            }
+            int32_t *tc = sc;
+            sc = dc;
+            dc = tc;
+            double *tv = sv;
+            sv = dv;
+            dv = tv;
+        }
+        // compaction of the sorted row (sc, sv) into the bucket's start
+        int64_t base = 0;
+        for (int64_t e0 = 0; e0 < len; e0 += blockDim.x) {
+            const int64_t e = e0 + threadIdx.x;
+            const int32_t key = e < len ? sc[lo + e] : 0;
+            const bool head = e < len && (e == 0 || sc[lo + e - 1] != key);
+            int total = 0;
+            const int pos = block_excl_scan(head ? 1 : 0, s_scan, &total);
+            if (head) {
+                double sum = 0.0;
+                for (int64_t f = e; f < len && sc[lo + f] == key; ++f) sum += sv[lo + f];
+                bkt_col[lo + base + pos] = key;
+                out_val[lo + base + pos] = static_cast<V>(sum);
+            }
+            base += total;
+        }
+        if (threadIdx.x == 0) row_nnz[row] = static_cast<int32_t>(base);
         __syncthreads();   // LDS is reused by the next row
     }
 }

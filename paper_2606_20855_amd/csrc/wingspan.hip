@@ -1206,6 +1206,7 @@ wingspan_status sv_impl(Ctx &c, const wingspan_csr *At, const SvLayout &L, const
 // first, at offsets that do not depend on the product count P.
 // ---------------------------------------------------------------------------
 constexpr int64_t kOpLongGrid = 2048;   // coalesce workgroups for long rows at most (grid-stride beyond)
+constexpr int64_t kOpHugeGrid = 512;    // the same for rows past kOpRowCap (one or two workgroups per CU)
 
 struct OpLayout {
     size_t off_ctr, off_pref, off_partials, off_part_key, off_part_val, off_part_len, off_row_cnt, off_row_fill,
@@ -1224,7 +1225,7 @@ OpLayout op_plan(const wingspan_csr *At, const wingspan_csr *B, int64_t P) {
     L.off_partials = off;
     const int64_t n = std::max<int64_t>(K, m) + 1;
     off += align_up(sizeof(int64_t) * ((n + kScanTile - 1) / kScanTile + 2));
-    L.off_part_key = off;
+    L.off_part_key = off;   // after the bucket step: two int32 column arrays of p for the long-row merge
     off += align_up(sizeof(int64_t) * p);
     L.off_part_val = off;
     off += align_up(sizeof(double) * p);
@@ -1333,15 +1334,18 @@ wingspan_status op_impl(Ctx &c, const wingspan_csr *At, const wingspan_csr *B, c
                                                                       long_rows, ctr);
     op_merge_long<V><<<static_cast<unsigned>(std::min<int64_t>(m, kOpLongGrid)), kOpRowBlock, 0, c.st>>>(
         bucket, bkt_col, bkt_val, out_val, row_nnz, long_rows, ctr);
+    // rows past kOpRowCap: the partial Cs are no longer needed, so their arrays
+    // hold the sorted runs (X: columns in part_key's first half, values in
+    // part_val; Y: columns in its second half, values in bkt_val)
+    int32_t *run_col = reinterpret_cast<int32_t *>(part_key);
+    op_merge_huge<V><<<static_cast<unsigned>(std::min<int64_t>(m, kOpHugeGrid)), kOpHugeBlock, 0, c.st>>>(
+        bucket, m, bkt_col, bkt_val, out_val, row_nnz, long_rows, ctr, run_col, part_val,
+        run_col + std::max<int64_t>(P, 1));
     LAUNCH_CHECK("outer merge");
     // 3. C.row_ptr, then the rows gathered into CSR
     if ((s = run_scan(c, CountIn{row_nnz}, m, c_rp)) != WINGSPAN_OK) return s;
-    int32_t herr = 0;
     HIP_TRY(hipMemcpyAsync(c_nnz, c_rp + m, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
-    HIP_TRY(hipMemcpyAsync(&herr, ctr + 1, sizeof(int32_t), hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
-    if (herr & kErrUnsupportedRow)
-        return fail(WINGSPAN_ERR_UNSUPPORTED, "a row of C gathers more than %d partial entries", kOpRowCap);
     if (*c_nnz > c_cap)
         return fail(WINGSPAN_ERR_INSUFFICIENT_CAPACITY, "C has %lld entries but c_capacity is %lld",
                     (long long)*c_nnz, (long long)c_cap);

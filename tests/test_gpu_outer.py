@@ -78,24 +78,68 @@ def test_identity_and_permutation_exact():
     check(P, A, "permutation")
 
 
-def test_row_too_long_is_reported():
+def test_rows_past_the_lds_cap_exact():
+    # every row of the arrowhead's square gathers about n partial entries (n > 4096):
+    # runs sorted in LDS, one merge pass; integer sums are exact whatever the order
+    A = matgen.arrowhead(5000)
+    got, ref = check(A, A, "arrowhead 5000")
+    assert np.array_equal(got.val, ref.val)
+    assert int(np.diff(ref.row_ptr).min()) == A.nrows
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_long_row_of_few_columns(dtype):
+    # row 0 of A is full over K = 200000 and B's rows have 3 of 50 columns: row 0 of C
+    # gathers ~50 entries from each of ~290 partial Cs, so runs of equal columns span
+    # merge tiles and compaction blocks
+    K = 200000
+    rng = np.random.default_rng(81)
+    a_rows = [np.zeros(K, np.int64), np.full(5, 1, np.int64), np.full(3, 2, np.int64)]
+    a_cols = [np.arange(K), np.sort(rng.choice(K, 5, replace=False)), np.sort(rng.choice(K, 3, replace=False))]
+    rows, cols = np.concatenate(a_rows), np.concatenate(a_cols)
+    A = matgen.CSR(3, K, np.array([0, K, K + 5, K + 8], np.int32), cols.astype(np.int32),
+                   rng.uniform(-1, 1, len(cols)).astype(dtype))
+    assert np.array_equal(np.repeat(np.arange(3), np.diff(A.row_ptr)), rows)
+    B = matgen.er(K, 50, 3, 82, dtype)
+    got, ref = check(A, B, "one long row")
+    assert ref.row_ptr[1] == 50
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+def test_rmat14_square(dtype):
+    # heavy-tailed rows: the largest gathers ~165 K partial entries (six merge passes)
+    A = matgen.rmat(14, 16, seed=3, dtype=dtype)
+    ref_prods = oracle.row_products(A, A)
+    assert int(ref_prods.max()) > 100000 and int((ref_prods > 4096).sum()) > 500
+    check(A, A, f"rmat14 {np.dtype(dtype).name}")
+
+
+@pytest.mark.slow
+def test_er_rect_full_size():
+    """The rectangular Erdos-Renyi product at full size (A 1,000,000 x 500,000
+    and B 500,000 x 1,000,000, 8 per row, fp64) through the outer product,
+    every row checked against the oracle block by block."""
+    import os
     import torch
     from paper_2606_20855_amd import wingspan as ws
-    # the arrowhead's first row gathers one partial entry per column from every k: far past the cap
-    A = matgen.arrowhead(6000)
+    from gpu_util import check_rows_blockwise
+    A, B = matgen.config("er_rect")
+    print(f"outer er_rect: A {A.nrows}x{A.ncols} B {B.nrows}x{B.ncols}", flush=True)
     dAt = ws.DeviceCSR.from_host(matgen.transpose(A), "cuda:0")
-    dB = ws.DeviceCSR.from_host(A, "cuda:0")
-    Atd, Bd = dAt.desc(), dB.desc()
-    n0 = ws.wingspan_outer_workspace_size(Atd, Bd, 0)
-    w0 = torch.empty(n0, dtype=torch.uint8, device="cuda:0")
-    P = ws.wingspan_outer_products(Atd, Bd, w0.data_ptr(), n0)
-    assert P == int((np.diff(A.row_ptr).astype(np.int64) ** 2).sum())   # symmetric A: P = sum of squared degrees
-    nbytes = ws.wingspan_outer_workspace_size(Atd, Bd, P)
-    wsb = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
-    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device="cuda:0")
-    st, _ = ws.wingspan_spgemm_outer(Atd, Bd, ws.F64, c_rp.data_ptr(), 0, 0, 0, wsb.data_ptr(), nbytes,
-                                     check=False)
-    assert ws.STATUS[st] == "WINGSPAN_ERR_UNSUPPORTED"
+    dB = ws.DeviceCSR.from_host(B, "cuda:0")
+    C = ws.spgemm_outer(dAt, dB)
+    torch.cuda.synchronize()
+    rp = C.row_ptr.cpu().numpy()
+    print(f"outer er_rect: nnz(C) = {int(rp[-1])}", flush=True)
+
+    def fetch(a: int, b: int):
+        return C.col_idx[a:b].cpu().numpy(), C.val[a:b].cpu().numpy()
+
+    res = check_rows_blockwise(A, B, rp, fetch, workers=min(16, os.cpu_count() or 1),
+                               log=lambda m: print(m, flush=True))
+    assert res["rows"] == A.nrows and res["entries"] == int(rp[-1]) and res["products"] == 64_000_000
+    print(f"outer er_rect: every row checked, worst |d|/M = {res['worst']:.2e}", flush=True)
 
 
 def test_capacity_and_workspace_errors():
