@@ -293,10 +293,13 @@ wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_
  * wingspan_elementwise_structure writes c_row_ptr_dev (A.nrows+1 entries) and
  * *c_nnz (host); it synchronizes `stream` once, to return *c_nnz. A.val and
  * B.val are not read. wingspan_elementwise_values then fills c_col_idx_dev
- * (int32) and c_val_dev for that c_row_ptr_dev and the same A and B patterns
- * (so it can be re-run for new values); it is asynchronous. Both take the
- * workspace wingspan_elementwise_workspace_size gives (pure host code, a
- * function of the sizes only).
+ * (int32) and c_val_dev, nnz(C) entries in C's row-major order, for the same
+ * A and B patterns (so it can be re-run for new values); c_row_ptr_dev is the
+ * array the structure call wrote, and the placement it describes is found
+ * again from the patterns, so the array itself is not read. The call is
+ * asynchronous. Both take the workspace wingspan_elementwise_workspace_size
+ * gives (pure host code, a function of the sizes only: O(nrows + (nnz(A) +
+ * nnz(B)) / 2048) bytes).
  * ------------------------------------------------------------------------ */
 typedef enum { WINGSPAN_OP_ADD = 0, WINGSPAN_OP_HADAMARD = 1 } wingspan_ew_op;
 

@@ -140,7 +140,13 @@ __global__ void __launch_bounds__(1024) scan_one_block(In in, int64_t n, int64_t
     const int64_t b = static_cast<int64_t>(threadIdx.x) * per;
     const int64_t e = b + per < n ? b + per : n;
     int64_t s = 0;
-    for (int64_t i = b; i < e; ++i) s += in(i);
+    for (int64_t i0 = b; i0 < e; i0 += 8) {   // eight loads in flight at a time
+        int64_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = i0 + u < e ? in(i0 + u) : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
     const int ln = lane_id();
     const int w = threadIdx.x / kWave;
     int64_t incl = s;
@@ -157,10 +163,15 @@ __global__ void __launch_bounds__(1024) scan_one_block(In in, int64_t n, int64_t
         tot += wsum[i];
     }
     run += incl - s;
-    for (int64_t i = b; i < e; ++i) {
-        const int64_t v = in(i);
-        out[i] = run;
-        run += v;
+    for (int64_t i0 = b; i0 < e; i0 += 8) {
+        int64_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = i0 + u < e ? in(i0 + u) : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (i0 + u < e) out[i0 + u] = run;
+            run += v[u];
+        }
     }
     if (threadIdx.x == 0) out[n] = tot;
 }

@@ -4,135 +4,291 @@
 // the sum (an entry stored on both sides takes a + b, including an exact
 // zero) and the intersection for the product.
 //
-// The merge is done per entry, flat over the entries: a thread takes one
-// entry of A (or B), finds its row, and finds its column among the same row
-// of the other matrix by binary search. That rank gives the entry's place in
-// the merged row directly (the entries of the other row before it), and
-// equality tells whether both sides store the column. Workgroups take chunks
-// of kEwChunk consecutive entries, so long and short rows balance by
-// themselves and every load and store of the entry arrays is coalesced.
+// A and B are read as one merged sequence: all entries of both in row-major
+// (row, column) order, A's entry first where both store a coordinate. The
+// sequence is cut into tiles of kEwTile entries by merge-path splits
+// (ew_tile_splits: the row holding a boundary found on the summed row
+// pointers, then a split of that row's two column lists), a boundary that
+// would separate the two entries of a common coordinate taking the B entry
+// along. A tile's shares of A and of B are contiguous runs of their entry
+// arrays, so a workgroup loads both with coalesced reads into LDS as
+// (row, column) keys and matches them there:
+//   ew_tile_count: the coordinates both sides store, per tile (and per row,
+//                  for C's row pointer);
+//   ew_tile_write: each entry's place in C, from its rank among the other
+//                  side's share and the common coordinates before it, after
+//                  the tile's first place (a scan of the tiles' counts).
+// Long and short rows balance by themselves; nothing but the entries, the
+// row pointers and C is read or written at the size of the inputs.
 #pragma once
 
-#include "device_common.hpp"
+#include "search.hpp"
 
 namespace wsp {
 
-constexpr int kEwChunk = 1024;   // entries per workgroup
-constexpr int kEwRows = 1024;    // rows a chunk stages in LDS
+constexpr int kEwTile = 2048;    // merged entries per tile (one more when a common coordinate straddles)
 constexpr int kEwBlock = 256;
+constexpr int kEwRows = 1024;    // rows whose common coordinates a tile counts in LDS (more: global atomics)
+constexpr int kEwPer = (kEwTile + 1 + kEwBlock - 1) / kEwBlock;   // consecutive tile positions per thread
 enum EwOp { kEwAdd = 0, kEwMul = 1 };
+constexpr int64_t kEwEnd = 0x7fffffffffffffffll;   // above every (row, column) key
 
-// Last row r in [0, nrows) with rp[r] <= e (the row holding entry e when
-// e < rp[nrows]). All 64 lanes of one wave take part.
-__device__ __forceinline__ int wave_find_row32(const int32_t *__restrict__ rp, int nrows, int64_t e) {
-    int lo = 0, hi = nrows - 1;   // rp[lo] <= e holds throughout
+// Last r in [lo, hi] with f(r) <= q, for a non-decreasing f with f(lo) <= q:
+// a 64-ary search in which all 64 lanes of one wave take part.
+template <typename F>
+__device__ __forceinline__ int wave_last_le(F f, int lo, int hi, int64_t q) {
     while (hi > lo) {
-        const int step = (hi - lo + kWave) / kWave;
-        const int idx = lo + lane_id() * step;
-        const bool le = idx <= hi && rp[idx] <= e;
-        const uint64_t m = ballot(le);
-        lo = lo + (63 - __clzll(m)) * step;   // lane 0 always qualifies
-        const int h = lo + step - 1;
-        hi = h < hi ? h : hi;
+        const int64_t step = (static_cast<int64_t>(hi) - lo + kWave) / kWave;
+        const int64_t idx = lo + lane_id() * step;
+        const bool le = idx <= hi && f(static_cast<int>(idx)) <= q;
+        const uint64_t m = ballot(le);   // lane 0 always qualifies
+        lo = static_cast<int>(lo + (63 - __clzll(m)) * step);
+        const int64_t h = lo + step - 1;
+        hi = h < hi ? static_cast<int>(h) : hi;
     }
     return lo;
 }
 
-// The rows of a chunk of entries [e0, e1): staged row pointers when there are
-// at most kEwRows of them, else searched in the global row pointer.
-struct ChunkRows {
-    const int32_t *rp;
-    const int32_t *s_rp;   // rp[r0 .. r0 + nr] when staged
-    int r0, nr;
-    bool staged;
-    __device__ __forceinline__ int row_of(int64_t e) const {
-        int lo = 0, hi = nr - 1;
-        if (staged) {
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (s_rp[mid] <= e) lo = mid;
-                else hi = mid - 1;
-            }
-        } else {
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (rp[r0 + mid] <= e) lo = mid;
-                else hi = mid - 1;
-            }
-        }
-        return r0 + lo;
+// Tile boundaries, one wave each: for t in [0, ntiles], d = min(t kEwTile,
+// nnz(A) + nnz(B)); split_a[t] and split_b[t] count the A and B entries before
+// boundary t and split_r[t] is the row holding it (nrows - 1 at the end).
+// nrows >= 1.
+__global__ void __launch_bounds__(256) ew_tile_splits(const int32_t *__restrict__ a_rp,
+                                                      const int32_t *__restrict__ a_col,
+                                                      const int32_t *__restrict__ b_rp,
+                                                      const int32_t *__restrict__ b_col, int nrows, int64_t ntiles,
+                                                      int64_t *__restrict__ split_a, int64_t *__restrict__ split_b,
+                                                      int32_t *__restrict__ split_r) {
+    const int64_t t = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
+    if (t > ntiles) return;   // whole wave
+    const int64_t na_all = a_rp[nrows], nb_all = b_rp[nrows];
+    const int64_t total = na_all + nb_all;
+    const int64_t d = t * kEwTile < total ? t * kEwTile : total;
+    int64_t ia = na_all, ib = nb_all;
+    int r = nrows - 1;
+    if (d < total) {
+        r = wave_last_le([=](int k) { return static_cast<int64_t>(a_rp[k]) + b_rp[k]; }, 0, nrows - 1, d);
+        const int64_t ar = a_rp[r], br = b_rp[r];
+        const int64_t na = a_rp[r + 1] - ar, nb = b_rp[r + 1] - br;
+        const int64_t dd = d - ar - br;   // < na + nb: row r holds position d
+        const int64_t i = wave_merge_split(a_col + ar, na, b_col + br, nb, dd);
+        int64_t j = dd - i;
+        if (i > 0 && j < nb && a_col[ar + i - 1] == b_col[br + j]) ++j;   // keep a common pair together
+        ia = ar + i;
+        ib = br + j;
     }
+    if (lane_id() == 0) {
+        split_a[t] = ia;
+        split_b[t] = ib;
+        split_r[t] = r;
+    }
+}
+
+// A tile's shares and rows: A entries [ia0, ia0 + na), B entries
+// [ib0, ib0 + nb), all in rows [r0, r0 + nr).
+struct EwTile {
+    int64_t ia0, ib0;
+    int na, nb, r0, nr;
 };
 
-// All threads of the workgroup call it (it has barriers). nrows >= 1 and
-// e0 < e1 <= rp[nrows].
-__device__ __forceinline__ ChunkRows load_chunk_rows(const int32_t *__restrict__ rp, int nrows, int64_t e0,
-                                                     int64_t e1, int32_t *s_rp, int *s_r) {
-    if (threadIdx.x < kWave) {
-        const int r0 = wave_find_row32(rp, nrows, e0);
-        const int r1 = wave_find_row32(rp, nrows, e1 - 1);
-        if (threadIdx.x == 0) {
-            s_r[0] = r0;
-            s_r[1] = r1;
+__device__ __forceinline__ EwTile ew_tile_of(const int64_t *__restrict__ split_a, const int64_t *__restrict__ split_b,
+                                             const int32_t *__restrict__ split_r) {
+    const int t = blockIdx.x;
+    EwTile T;
+    T.ia0 = split_a[t];
+    T.ib0 = split_b[t];
+    T.na = static_cast<int>(split_a[t + 1] - T.ia0);
+    T.nb = static_cast<int>(split_b[t + 1] - T.ib0);
+    T.r0 = split_r[t];
+    T.nr = split_r[t + 1] - T.r0 + 1;
+    return T;
+}
+
+// A DPP lane move of an unsigned value; lanes with no source read 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, ROW_MASK, 0xf, false));
+}
+
+// Inclusive wave max-scan of unsigned values (identity 0): row shifts within
+// 16-lane rows, then row broadcasts of lanes 15 and 31.
+__device__ __forceinline__ uint32_t wave_incl_umax(uint32_t v) {
+    v = max(v, dpp_u32<kDppRowShr1, 0xf>(v));
+    v = max(v, dpp_u32<kDppRowShr2, 0xf>(v));
+    v = max(v, dpp_u32<kDppRowShr4, 0xf>(v));
+    v = max(v, dpp_u32<kDppRowShr8, 0xf>(v));
+    v = max(v, dpp_u32<kDppRowBcast15, 0xa>(v));
+    v = max(v, dpp_u32<kDppRowBcast31, 0xc>(v));
+    return v;
+}
+
+// Exclusive block-wide max-scan of unsigned values (0 for thread 0).
+// `scratch` holds BLOCK/64 ints.
+template <int BLOCK>
+__device__ __forceinline__ uint32_t block_excl_umax(uint32_t x, int *scratch) {
+    constexpr int NW = BLOCK / kWave;
+    const uint32_t incl = wave_incl_umax(x);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) scratch[w] = static_cast<int>(incl);
+    __syncthreads();
+    uint32_t before = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) before = i < w ? max(before, static_cast<uint32_t>(scratch[i])) : before;
+    __syncthreads();
+    const uint32_t prev = static_cast<uint32_t>(__shfl_up(static_cast<int>(incl), 1, kWave));
+    return max(before, lane_id() == 0 ? 0u : prev);
+}
+
+// Loads a tile as (row, column) keys in LDS, A's share at [0, na) and B's at
+// [na, na + nb) (with VALS, values in double beside them): the columns, with
+// coalesced reads, into the keys' low halves, and, at the same time, the row
+// pointers of the tile's rows. Then each row that starts inside a share marks
+// its first position in the key's high half (row r0 + k as k + 1 in A's
+// share, nr + k + 1 in B's, so one max-scan over both shares serves and B's
+// marks exceed all of A's), and an exclusive max-scan over the positions,
+// kEwPer consecutive ones per thread, replaces the marks by the rows. All
+// threads call it.
+template <bool VALS, typename V>
+__device__ __forceinline__ void ew_load_tile(const EwTile &T, const int32_t *__restrict__ a_rp,
+                                             const int32_t *__restrict__ a_col, const V *__restrict__ a_val,
+                                             const int32_t *__restrict__ b_rp, const int32_t *__restrict__ b_col,
+                                             const V *__restrict__ b_val, int64_t *s_key, double *s_val,
+                                             int *scratch) {
+    uint32_t *half = reinterpret_cast<uint32_t *>(s_key);   // [2p] column, [2p + 1] mark, then row
+    const int n = T.na + T.nb;
+    const uint32_t nr = static_cast<uint32_t>(T.nr);
+    // the first kEwBlock rows' pointers, read beside the columns
+    const int k0 = threadIdx.x;
+    int64_t sa0 = -1, ea0 = -1, sb0 = -1, eb0 = -1;
+    if (k0 < T.nr) {
+        sa0 = a_rp[T.r0 + k0] - T.ia0;
+        ea0 = a_rp[T.r0 + k0 + 1] - T.ia0;
+        sb0 = b_rp[T.r0 + k0] - T.ib0;
+        eb0 = b_rp[T.r0 + k0 + 1] - T.ib0;
+    }
+    // position p of the tile (A's share, then B's), kEwPer per thread strided by the block: all loads
+    // issued before the first is waited for
+    int32_t col[kEwPer];
+    double val[kEwPer];
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        const int p = threadIdx.x + u * kEwBlock;
+        col[u] = 0;
+        val[u] = 0.0;
+        if (p < T.na) {
+            col[u] = a_col[T.ia0 + p];
+            if (VALS) val[u] = to_d(a_val[T.ia0 + p]);
+        } else if (p < n) {
+            col[u] = b_col[T.ib0 + (p - T.na)];
+            if (VALS) val[u] = to_d(b_val[T.ib0 + (p - T.na)]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        const int p = threadIdx.x + u * kEwBlock;
+        if (p < n) {
+            s_key[p] = static_cast<uint32_t>(col[u]);
+            if (VALS) s_val[p] = val[u];
         }
     }
     __syncthreads();
-    ChunkRows cr;
-    cr.rp = rp;
-    cr.s_rp = s_rp;
-    cr.r0 = s_r[0];
-    cr.nr = s_r[1] - s_r[0] + 1;
-    cr.staged = cr.nr <= kEwRows;
-    if (cr.staged) {
-        for (int i = threadIdx.x; i <= cr.nr; i += blockDim.x) s_rp[i] = rp[cr.r0 + i];
+    // a non-empty row starting inside a share is the only one to mark that position
+    if (k0 < T.nr) {
+        if (sa0 >= 0 && sa0 < T.na && ea0 > sa0) half[2 * sa0 + 1] = static_cast<uint32_t>(k0) + 1u;
+        if (sb0 >= 0 && sb0 < T.nb && eb0 > sb0) half[2 * (T.na + sb0) + 1] = nr + static_cast<uint32_t>(k0) + 1u;
+    }
+    for (int k = k0 + blockDim.x; k < T.nr; k += blockDim.x) {   // tiles over many empty rows
+        const int64_t sa = a_rp[T.r0 + k] - T.ia0, ea = a_rp[T.r0 + k + 1] - T.ia0;
+        if (sa >= 0 && sa < T.na && ea > sa) half[2 * sa + 1] = static_cast<uint32_t>(k) + 1u;
+        const int64_t sb = b_rp[T.r0 + k] - T.ib0, eb = b_rp[T.r0 + k + 1] - T.ib0;
+        if (sb >= 0 && sb < T.nb && eb > sb) half[2 * (T.na + sb) + 1] = nr + static_cast<uint32_t>(k) + 1u;
     }
     __syncthreads();
-    return cr;
+    const int p0 = threadIdx.x * kEwPer;
+    uint32_t mk[kEwPer];
+    uint32_t x = 0;
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        const int p = p0 + u;
+        uint32_t v = p < n ? half[2 * p + 1] : 0u;
+        if (p == 0 && T.na > 0) v = max(v, 1u);             // A's share starts in row r0
+        if (p == T.na && T.nb > 0) v = max(v, nr + 1u);     // and so does B's
+        mk[u] = v;
+        x = max(x, v);
+    }
+    uint32_t run = block_excl_umax<kEwBlock>(x, scratch);
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        const int p = p0 + u;
+        run = max(run, mk[u]);
+        if (p < n) half[2 * p + 1] = static_cast<uint32_t>(T.r0) + (p < T.na ? run - 1u : run - nr - 1u);
+    }
+    __syncthreads();
 }
 
-// First position p in [lo, hi) with col[p] >= key (hi if none).
-__device__ __forceinline__ int lower_bound32(const int32_t *__restrict__ col, int lo, int hi, int key) {
+// Merge-path split inside a tile: the number of A's share among the first d
+// entries of the tile's merged order (A first on equal keys).
+__device__ __forceinline__ int ew_split(const int64_t *s_key, int na, int nb, int d) {
+    int lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
     while (lo < hi) {
-        const int mid = lo + ((hi - lo) >> 1);
-        if (col[mid] < key) lo = mid + 1;
-        else hi = mid;
+        const int mid = (lo + hi) >> 1;
+        if (s_key[mid] > s_key[na + d - mid - 1]) hi = mid;
+        else lo = mid + 1;
     }
     return lo;
 }
 
-// When dups is not null, the per-row count of the entries of A that B also
-// stores (dups zeroed by the caller); when rank is not null, each A entry's
-// rank in B's row, with the sign bit set when B stores the same column.
-__global__ void __launch_bounds__(kEwBlock) ew_match(const int32_t *__restrict__ a_rp,
-                                                     const int32_t *__restrict__ a_col,
-                                                     const int32_t *__restrict__ b_rp,
-                                                     const int32_t *__restrict__ b_col, int nrows, int64_t nnz_a,
-                                                     int32_t *__restrict__ dups, int32_t *__restrict__ rank) {
-    __shared__ int32_t s_rp[kEwRows + 1];
-    __shared__ int32_t s_cnt[kEwRows];
-    __shared__ int s_r[2];
-    const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kEwChunk;
-    if (e0 >= nnz_a) return;   // whole workgroup
-    const int64_t e1 = nnz_a - e0 < kEwChunk ? nnz_a : e0 + kEwChunk;
-    for (int i = threadIdx.x; i < kEwRows; i += blockDim.x) s_cnt[i] = 0;
-    const ChunkRows cr = load_chunk_rows(a_rp, nrows, e0, e1, s_rp, s_r);
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-        const int r = cr.row_of(e);
-        const int c = a_col[e];
-        const int blo = b_rp[r], bhi = b_rp[r + 1];
-        const int p = lower_bound32(b_col, blo, bhi, c);
-        const bool dup = p < bhi && b_col[p] == c;
-        if (rank) rank[e] = (p - blo) | (dup ? static_cast<int32_t>(0x80000000u) : 0);
-        if (dup && dups) {
-            if (cr.staged) atomicAdd(&s_cnt[r - cr.r0], 1);
-            else atomicAdd(&dups[r], 1);
+// Per tile: tile_cnt[t] = C's entries from the tile (the shares' sizes less
+// the common coordinates for the sum, the common coordinates for the
+// product). With PER_ROW, also each row's common coordinates added to
+// dups[row] (zeroed by the caller).
+template <bool PER_ROW>
+__global__ void __launch_bounds__(kEwBlock) ew_tile_count(const int32_t *__restrict__ a_rp,
+                                                          const int32_t *__restrict__ a_col,
+                                                          const int32_t *__restrict__ b_rp,
+                                                          const int32_t *__restrict__ b_col,
+                                                          const int64_t *__restrict__ split_a,
+                                                          const int64_t *__restrict__ split_b,
+                                                          const int32_t *__restrict__ split_r, int op,
+                                                          int32_t *__restrict__ tile_cnt, int32_t *__restrict__ dups) {
+    __shared__ int64_t s_key[kEwTile + 1];
+    __shared__ int32_t s_cnt[PER_ROW ? kEwRows : 1];
+    __shared__ int32_t scratch[kEwBlock / kWave];
+    const EwTile T = ew_tile_of(split_a, split_b, split_r);
+    const bool local = PER_ROW && T.nr <= kEwRows;
+    if (local)
+        for (int k = threadIdx.x; k < T.nr; k += blockDim.x) s_cnt[k] = 0;
+    ew_load_tile<false, float>(T, a_rp, a_col, nullptr, b_rp, b_col, nullptr, s_key, nullptr, scratch);
+    const int n = T.na + T.nb;
+    const int d = threadIdx.x * kEwPer;
+    int c = 0;
+    if (d < n) {
+        int i = ew_split(s_key, T.na, T.nb, d), j = d - i;
+        int64_t ka = i < T.na ? s_key[i] : kEwEnd, kb = j < T.nb ? s_key[T.na + j] : kEwEnd;
+        const int steps = n - d < kEwPer ? n - d : kEwPer;
+        for (int u = 0; u < steps; ++u) {
+            if (ka <= kb) {
+                if (ka == kb) {
+                    ++c;
+                    if (PER_ROW) {
+                        const int row = static_cast<int>(ka >> 32);
+                        if (local) atomicAdd(&s_cnt[row - T.r0], 1);
+                        else atomicAdd(&dups[row], 1);
+                    }
+                }
+                ++i;
+                ka = i < T.na ? s_key[i] : kEwEnd;
+            } else {
+                ++j;
+                kb = j < T.nb ? s_key[T.na + j] : kEwEnd;
+            }
         }
     }
-    __syncthreads();
-    if (dups && cr.staged) {
-        for (int i = threadIdx.x; i < cr.nr; i += blockDim.x)
-            if (s_cnt[i]) atomicAdd(&dups[cr.r0 + i], s_cnt[i]);
-    }
+    c = block_sum<kEwBlock>(c, scratch);   // (its barriers also order the LDS counts)
+    if (threadIdx.x == 0) tile_cnt[blockIdx.x] = op == kEwAdd ? n - c : c;
+    if (local)
+        for (int k = threadIdx.x; k < T.nr; k += blockDim.x)
+            if (s_cnt[k]) atomicAdd(&dups[T.r0 + k], s_cnt[k]);
 }
 
 // Entries of C's rows: |A_r| + |B_r| - dups_r (sum) or dups_r (product).
@@ -145,101 +301,91 @@ struct EwCountIn {
     }
 };
 
-// 1 for an A entry that B also stores (from ew_match's rank).
-struct EwDupIn {
-    const int32_t *rank;
-    __device__ __forceinline__ int64_t operator()(int64_t i) const { return rank[i] < 0 ? 1 : 0; }
+struct EwTileIn {
+    const int32_t *cnt;
+    __device__ __forceinline__ int64_t operator()(int64_t t) const { return cnt[t]; }
 };
 
-// Sum. The place of an entry in its merged row is its index in its own row,
-// plus the entries of the other row before its column, minus the columns both
-// rows store before it (counted once). dscan is the exclusive prefix count, over
-// A's entries, of those A also finds in B (ew_match's sign bit), so the common
-// columns of row r before A's position q number dscan[q] - dscan[A.rp[r]].
-// A's entries (rank from ew_match) write a, or a + b for a common column.
-// Values are formed in double and rounded once.
-template <typename V>
-__global__ void __launch_bounds__(kEwBlock) ew_add_a(const int32_t *__restrict__ a_rp,
-                                                     const int32_t *__restrict__ a_col,
-                                                     const V *__restrict__ a_val,
-                                                     const int32_t *__restrict__ b_rp,
-                                                     const V *__restrict__ b_val, int nrows, int64_t nnz_a,
-                                                     const int32_t *__restrict__ rank,
-                                                     const int64_t *__restrict__ dscan,
-                                                     const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col,
-                                                     V *__restrict__ c_val) {
-    __shared__ int32_t s_rp[kEwRows + 1];
-    __shared__ int s_r[2];
-    const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kEwChunk;
-    if (e0 >= nnz_a) return;
-    const int64_t e1 = nnz_a - e0 < kEwChunk ? nnz_a : e0 + kEwChunk;
-    const ChunkRows cr = load_chunk_rows(a_rp, nrows, e0, e1, s_rp, s_r);
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-        const int r = cr.row_of(e);
-        const int32_t k = rank[e];
-        const int rb = k & 0x7fffffff;   // entries of B's row before this column
-        const int ar = a_rp[r];
-        const int64_t pos = c_rp[r] + (e - ar) + rb - (dscan[e] - dscan[ar]);
-        double v = to_d(a_val[e]);
-        if (k < 0) v += to_d(b_val[b_rp[r] + rb]);
-        c_col[pos] = a_col[e];
-        c_val[pos] = static_cast<V>(v);
+// C's entries from a tile, from tile_off[t] on: each thread walks kEwPer
+// consecutive positions of the tile's merged order (from a merge-path split),
+// keeping, for the sum, every entry but the B half of a common coordinate (the
+// A half takes a + b) and, for the product, the A half of each common
+// coordinate (a * b). The kept entries' values are then read (all loads of a
+// thread issued together, overlapping the scan of the kept counts that places
+// them), formed in double and rounded once.
+template <typename V, int OP>
+__global__ void __launch_bounds__(kEwBlock) ew_tile_write(const int32_t *__restrict__ a_rp,
+                                                          const int32_t *__restrict__ a_col,
+                                                          const V *__restrict__ a_val,
+                                                          const int32_t *__restrict__ b_rp,
+                                                          const int32_t *__restrict__ b_col,
+                                                          const V *__restrict__ b_val,
+                                                          const int64_t *__restrict__ split_a,
+                                                          const int64_t *__restrict__ split_b,
+                                                          const int32_t *__restrict__ split_r,
+                                                          const int64_t *__restrict__ tile_off,
+                                                          int32_t *__restrict__ c_col, V *__restrict__ c_val) {
+    __shared__ int64_t s_key[kEwTile + 1];
+    __shared__ int32_t scratch[kEwBlock / kWave];
+    const EwTile T = ew_tile_of(split_a, split_b, split_r);
+    ew_load_tile<false, V>(T, a_rp, a_col, nullptr, b_rp, b_col, nullptr, s_key, nullptr, scratch);
+    const int n = T.na + T.nb;
+    const int d = threadIdx.x * kEwPer;
+    int32_t oc[kEwPer];
+    int ai[kEwPer], bi[kEwPer];   // the kept entry's A and B share indices (-1: that side stores nothing)
+    int c = 0;
+    int i = 0, j = 0;
+    if (d < n) {
+        i = ew_split(s_key, T.na, T.nb, d);
+        j = d - i;
     }
-}
-
-// Sum, B's entries: those A does not store write b (the common ones are A's).
-template <typename V>
-__global__ void __launch_bounds__(kEwBlock) ew_add_b(const int32_t *__restrict__ a_rp,
-                                                     const int32_t *__restrict__ a_col,
-                                                     const int32_t *__restrict__ b_rp,
-                                                     const int32_t *__restrict__ b_col,
-                                                     const V *__restrict__ b_val, int nrows, int64_t nnz_b,
-                                                     const int64_t *__restrict__ dscan,
-                                                     const int64_t *__restrict__ c_rp, int32_t *__restrict__ c_col,
-                                                     V *__restrict__ c_val) {
-    __shared__ int32_t s_rp[kEwRows + 1];
-    __shared__ int s_r[2];
-    const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kEwChunk;
-    if (e0 >= nnz_b) return;
-    const int64_t e1 = nnz_b - e0 < kEwChunk ? nnz_b : e0 + kEwChunk;
-    const ChunkRows cr = load_chunk_rows(b_rp, nrows, e0, e1, s_rp, s_r);
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-        const int r = cr.row_of(e);
-        const int c = b_col[e];
-        const int alo = a_rp[r], ahi = a_rp[r + 1];
-        const int q = lower_bound32(a_col, alo, ahi, c);   // A's entries of the row before this column end at q
-        if (q < ahi && a_col[q] == c) continue;
-        const int64_t pos = c_rp[r] + (e - b_rp[r]) + (q - alo) - (dscan[q] - dscan[alo]);
-        c_col[pos] = c;
-        c_val[pos] = b_val[e];
+    // the current A and B keys (kEwEnd past a share's end) and the last A key before j's entry
+    int64_t ka = i < T.na ? s_key[i] : kEwEnd, kb = j < T.nb ? s_key[T.na + j] : kEwEnd;
+    int64_t prev_a = i > 0 ? s_key[i - 1] : -1;
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        oc[u] = 0;
+        ai[u] = -1;
+        bi[u] = -1;
+        bool keep = false;
+        if (d + u < n) {
+            if (ka <= kb) {
+                const bool common = ka == kb;
+                keep = OP == kEwAdd || common;
+                oc[u] = static_cast<int32_t>(ka & 0xffffffffll);
+                ai[u] = keep ? i : -1;
+                bi[u] = keep && common ? j : -1;
+                prev_a = ka;
+                ++i;
+                ka = i < T.na ? s_key[i] : kEwEnd;
+            } else {
+                keep = OP == kEwAdd && prev_a != kb;   // else the B half of a common coordinate
+                oc[u] = static_cast<int32_t>(kb & 0xffffffffll);
+                bi[u] = keep ? j : -1;
+                ++j;
+                kb = j < T.nb ? s_key[T.na + j] : kEwEnd;
+            }
+        }
+        c += keep;
     }
-}
-
-// Product: an A entry that B also stores goes to pos[e] (the exclusive prefix
-// count of such entries over A, which C's row-major order makes its place).
-template <typename V>
-__global__ void __launch_bounds__(kEwBlock) ew_mul_write(const int32_t *__restrict__ a_rp,
-                                                         const int32_t *__restrict__ a_col,
-                                                         const V *__restrict__ a_val,
-                                                         const int32_t *__restrict__ b_rp,
-                                                         const V *__restrict__ b_val, int nrows, int64_t nnz_a,
-                                                         const int32_t *__restrict__ rank,
-                                                         const int64_t *__restrict__ pos, int32_t *__restrict__ c_col,
-                                                         V *__restrict__ c_val) {
-    __shared__ int32_t s_rp[kEwRows + 1];
-    __shared__ int s_r[2];
-    const int64_t e0 = static_cast<int64_t>(blockIdx.x) * kEwChunk;
-    if (e0 >= nnz_a) return;
-    const int64_t e1 = nnz_a - e0 < kEwChunk ? nnz_a : e0 + kEwChunk;
-    const ChunkRows cr = load_chunk_rows(a_rp, nrows, e0, e1, s_rp, s_r);
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-        const int32_t k = rank[e];
-        if (k >= 0) continue;
-        const int r = cr.row_of(e);
-        const int p = b_rp[r] + (k & 0x7fffffff);
-        const int64_t q = pos[e];
-        c_col[q] = a_col[e];
-        c_val[q] = static_cast<V>(to_d(a_val[e]) * to_d(b_val[p]));
+    double av[kEwPer], bv[kEwPer];
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        av[u] = ai[u] >= 0 ? to_d(a_val[T.ia0 + ai[u]]) : 0.0;
+        bv[u] = bi[u] >= 0 ? to_d(b_val[T.ib0 + bi[u]]) : 0.0;
+    }
+    int tot;
+    int64_t p = tile_off[blockIdx.x] + block_excl_scan<kEwBlock>(c, &tot, scratch);
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        if (ai[u] >= 0 || bi[u] >= 0) {
+            double v;
+            if (OP == kEwMul) v = av[u] * bv[u];
+            else v = ai[u] >= 0 && bi[u] >= 0 ? av[u] + bv[u] : (ai[u] >= 0 ? av[u] : bv[u]);
+            c_col[p] = oc[u];
+            c_val[p] = static_cast<V>(v);
+            ++p;
+        }
     }
 }
 

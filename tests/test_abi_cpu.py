@@ -220,7 +220,7 @@ def test_elementwise_argument_errors():
     A, B = desc(10, 12, 5), desc(10, 12, 7)
     need = ws.wingspan_elementwise_workspace_size(A, B)
     assert need > 0 and need % 256 == 0
-    assert ws.wingspan_elementwise_workspace_size(desc(10, 12, 5000), B) > need
+    assert ws.wingspan_elementwise_workspace_size(desc(10, 12, 5_000_000), B) > need   # one boundary per 2048 entries
     got, _ = status_of(ws.wingspan_elementwise_workspace_size, A, desc(10, 13, 7))
     assert got == "WINGSPAN_ERR_DIMENSION_MISMATCH"
     got, _ = status_of(ws.wingspan_elementwise_structure, ws.OP_ADD, A, desc(11, 12, 7), FAKE, FAKE, need, 0)

@@ -74,6 +74,24 @@ def test_dense_rows(op):
 
 
 @pytest.mark.parametrize("op", ["add", "hadamard"])
+def test_common_coordinates_across_tile_boundaries(op):
+    # long rows where B stores all of A's coordinates, or every other one: the
+    # merged sequence's tiles (2048 entries) would end between the two entries
+    # of a common coordinate at nearly every boundary
+    A = matgen.random_sparse(40, 30000, 0.4, 45)
+    rng = np.random.default_rng(46)
+    B = matgen.CSR(A.nrows, A.ncols, A.row_ptr, A.col_idx, rng.uniform(-1, 1, A.nnz))
+    check(op, A, B, what=f"{op} same pattern")
+    rows = np.repeat(np.arange(A.nrows), np.diff(A.row_ptr))
+    keep = np.arange(A.nnz) % 2 == 0
+    rp = np.zeros(A.nrows + 1, np.int64)
+    np.cumsum(np.bincount(rows[keep], minlength=A.nrows), out=rp[1:])
+    H = matgen.CSR(A.nrows, A.ncols, rp.astype(np.int32), A.col_idx[keep], A.val[keep] * 3.0)
+    check(op, A, H, what=f"{op} half the pattern")
+    check(op, H, A, what=f"{op} half the pattern, swapped")
+
+
+@pytest.mark.parametrize("op", ["add", "hadamard"])
 def test_chunks_over_many_empty_rows(op):
     # 200K rows, 95% empty: a chunk of entries spans more rows than it stages (1024)
     # and finds rows in the global row pointer
