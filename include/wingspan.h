@@ -300,6 +300,14 @@ wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_
  * asynchronous. Both take the workspace wingspan_elementwise_workspace_size
  * gives (pure host code, a function of the sizes only: O(nrows + (nnz(A) +
  * nnz(B)) / 2048) bytes).
+ *
+ * The structure call leaves its tiling of A and B (tile boundaries and each
+ * tile's place in C) in the workspace, and the library remembers that on the
+ * host: a values call with the same operation, descriptors (dimensions, nnz
+ * and pattern pointers; values may differ) and workspace then skips
+ * recomputing it. Any other call of this library given memory that overlaps
+ * the workspace forgets it. The caller must not write into the workspace, or
+ * change the patterns in place, between the two calls.
  * ------------------------------------------------------------------------ */
 typedef enum { WINGSPAN_OP_ADD = 0, WINGSPAN_OP_HADAMARD = 1 } wingspan_ew_op;
 

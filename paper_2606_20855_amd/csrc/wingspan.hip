@@ -1019,6 +1019,58 @@ wingspan_status setup(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, cons
 // ---------------------------------------------------------------------------
 // Elementwise operations (SpAdd, Hadamard): workspace layout and checks.
 // ---------------------------------------------------------------------------
+// The tiling an elementwise structure call leaves in its workspace (tile
+// boundaries and each tile's first place in C), remembered on the host so a
+// values call with the same operation, patterns and workspace skips
+// recomputing it. Every call of this library that is handed a workspace
+// forgets the plans kept in the memory it covers.
+struct EwPlanKey {
+    const char *ws;
+    size_t bytes;
+    int op;
+    int64_t m, n, a_nnz, b_nnz;
+    const int32_t *a_rp, *a_col, *b_rp, *b_col;
+    bool same(const EwPlanKey &o) const {
+        return ws == o.ws && op == o.op && m == o.m && n == o.n && a_nnz == o.a_nnz && b_nnz == o.b_nnz &&
+               a_rp == o.a_rp && a_col == o.a_col && b_rp == o.b_rp && b_col == o.b_col;
+    }
+    bool overlaps(const char *lo, size_t len) const { return ws < lo + len && lo < ws + bytes; }
+};
+
+std::mutex g_ew_mu;
+std::vector<EwPlanKey> g_ew_plans;
+constexpr size_t kEwMaxPlans = 16;
+
+EwPlanKey ew_key_of(int op, const wingspan_csr *A, const wingspan_csr *B, void *ws, size_t bytes) {
+    return EwPlanKey{static_cast<const char *>(ws), bytes, op, A->nrows, A->ncols, A->nnz, B->nnz,
+                     A->row_ptr, A->col_idx, B->row_ptr, B->col_idx};
+}
+
+void ew_forget(const void *ws, size_t bytes) {
+    if (!ws) return;
+    const char *lo = static_cast<const char *>(ws);
+    std::lock_guard<std::mutex> lk(g_ew_mu);
+    g_ew_plans.erase(std::remove_if(g_ew_plans.begin(), g_ew_plans.end(),
+                                    [&](const EwPlanKey &k) { return k.overlaps(lo, bytes); }),
+                     g_ew_plans.end());
+}
+
+bool ew_known(const EwPlanKey &key) {
+    std::lock_guard<std::mutex> lk(g_ew_mu);
+    for (const EwPlanKey &k : g_ew_plans)
+        if (k.same(key)) return true;
+    return false;
+}
+
+void ew_remember(const EwPlanKey &key) {
+    std::lock_guard<std::mutex> lk(g_ew_mu);
+    g_ew_plans.erase(std::remove_if(g_ew_plans.begin(), g_ew_plans.end(),
+                                    [&](const EwPlanKey &k) { return k.overlaps(key.ws, key.bytes); }),
+                     g_ew_plans.end());
+    if (g_ew_plans.size() >= kEwMaxPlans) g_ew_plans.erase(g_ew_plans.begin());
+    g_ew_plans.push_back(key);
+}
+
 struct EwLayout {
     size_t off_dups, off_split_a, off_split_b, off_split_r, off_tile_cnt, off_tile_off, off_partials, total;
     int64_t ntiles;
@@ -1108,21 +1160,29 @@ wingspan_status ew_count_tiles(Ctx &c, int op, const wingspan_csr *A, const wing
     return WINGSPAN_OK;
 }
 
-template <typename V>
-wingspan_status ew_values_impl(Ctx &c, int op, const wingspan_csr *A, const wingspan_csr *B, const EwLayout &L,
-                               int32_t *c_col, V *c_val) {
-    if (A->nrows == 0 || L.ntiles == 0) return WINGSPAN_OK;
-    if (op == WINGSPAN_OP_HADAMARD && (A->nnz == 0 || B->nnz == 0)) return WINGSPAN_OK;   // C is empty
-    const EwTiles T = ew_arrays(c, L);
-    wingspan_status s = ew_count_tiles<false>(c, op, A, B, L, T);
-    if (s != WINGSPAN_OK) return s;
-    // each tile's first place in C: one workgroup scans a few thousand tile counts, the tiled scan more
-    // (measured: 25 us for 16 K counts in one workgroup)
+// Each tile's first place in C, from the tile counts.
+wingspan_status ew_scan_tiles(Ctx &c, const EwLayout &L, const EwTiles &T) {
+    // one workgroup scans a few thousand tile counts, the tiled scan more (measured: 25 us for 16 K counts in
+    // one workgroup)
     if (L.ntiles <= 2048) {
         scan_one_block<EwTileIn><<<1, 1024, 0, c.st>>>(EwTileIn{T.tile_cnt}, L.ntiles, T.tile_off);
         LAUNCH_CHECK("elementwise tile scan");
-    } else if ((s = run_scan(c, EwTileIn{T.tile_cnt}, L.ntiles, T.tile_off)) != WINGSPAN_OK) {
-        return s;
+        return WINGSPAN_OK;
+    }
+    return run_scan(c, EwTileIn{T.tile_cnt}, L.ntiles, T.tile_off);
+}
+
+// The values; `planned`: the workspace holds this problem's tiling from an earlier call.
+template <typename V>
+wingspan_status ew_values_impl(Ctx &c, int op, const wingspan_csr *A, const wingspan_csr *B, const EwLayout &L,
+                               int32_t *c_col, V *c_val, bool planned) {
+    if (A->nrows == 0 || L.ntiles == 0) return WINGSPAN_OK;
+    if (op == WINGSPAN_OP_HADAMARD && (A->nnz == 0 || B->nnz == 0)) return WINGSPAN_OK;   // C is empty
+    const EwTiles T = ew_arrays(c, L);
+    wingspan_status s;
+    if (!planned) {
+        if ((s = ew_count_tiles<false>(c, op, A, B, L, T)) != WINGSPAN_OK) return s;
+        if ((s = ew_scan_tiles(c, L, T)) != WINGSPAN_OK) return s;
     }
     const V *av = static_cast<const V *>(A->val), *bv = static_cast<const V *>(B->val);
     const unsigned grid = static_cast<unsigned>(L.ntiles);
@@ -1478,6 +1538,7 @@ wingspan_status wingspan_spgemm_symbolic(const wingspan_csr *A, const wingspan_c
                                          int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
                                          void *stream, const wingspan_options *options) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     Ctx c{};
     return symbolic_entry(A, B, c_row_ptr_dev, c_nnz, workspace_dev, workspace_bytes, stream, options, c);
 }
@@ -1509,6 +1570,7 @@ wingspan_status wingspan_spgemm_numeric(const wingspan_csr *A, const wingspan_cs
                                         void *workspace_dev, size_t workspace_bytes, void *stream,
                                         const wingspan_options *options) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     Ctx c{};
     return numeric_entry(A, B, dtype, c_row_ptr_dev, c_col_idx_dev, c_val_dev, workspace_dev, workspace_bytes,
                          stream, options, false, c);
@@ -1519,6 +1581,7 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
                                 int64_t c_capacity, int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
                                 void *stream, const wingspan_options *options) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
         return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "dtype must be WINGSPAN_F32 or WINGSPAN_F64");
     if (c_capacity < 0) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "c_capacity is negative");
@@ -1574,6 +1637,7 @@ wingspan_status wingspan_spgemm_row_products(const wingspan_csr *A, const wingsp
                                              int64_t *row_products_dev, void *workspace_dev, size_t workspace_bytes,
                                              void *stream) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     wingspan_status s = check_pair(A, B);
     if (s != WINGSPAN_OK) return s;
     if (A->nrows > 0 && !row_products_dev) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "row_products_dev is NULL");
@@ -1593,6 +1657,7 @@ wingspan_status wingspan_spgemm_sharded(const wingspan_csr *A, const wingspan_cs
                                         void *workspace_dev, size_t workspace_bytes, void *stream,
                                         const wingspan_options *options) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     wingspan_status s = check_pair(A, B);
     if (s != WINGSPAN_OK) return s;
     if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
@@ -1631,6 +1696,7 @@ wingspan_status wingspan_sharded_to_csr(int64_t nrows, int64_t nnz, const int64_
                                         int64_t *c_row_ptr_dev, int32_t *c_col_idx_dev, void *c_val_dev,
                                         void *workspace_dev, size_t workspace_bytes, void *stream) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     size_t need = 0;
     wingspan_status s = wingspan_sharded_to_csr_workspace_size(nrows, &need);
     if (s != WINGSPAN_OK) return s;
@@ -1690,11 +1756,17 @@ wingspan_status wingspan_elementwise_structure(wingspan_ew_op op, const wingspan
     c.ws = static_cast<char *>(workspace_dev);
     const EwTiles T = ew_arrays(c, L);
     const int m = static_cast<int>(A->nrows);
+    bool planned = false;
+    ew_forget(workspace_dev, workspace_bytes);
     if (m > 0) {
         fill_i32<<<blocks_for(m, 256), 256, 0, c.st>>>(T.dups, m, 0);
         LAUNCH_CHECK("elementwise clear");
-        // per-row common coordinates (none when a side is empty)
-        if (A->nnz > 0 && B->nnz > 0 && (s = ew_count_tiles<true>(c, op, A, B, L, T)) != WINGSPAN_OK) return s;
+        // per-row common coordinates (none when a side is empty), and the tiles' places in C for the values
+        if (A->nnz > 0 && B->nnz > 0) {
+            if ((s = ew_count_tiles<true>(c, op, A, B, L, T)) != WINGSPAN_OK) return s;
+            if ((s = ew_scan_tiles(c, L, T)) != WINGSPAN_OK) return s;
+            planned = true;
+        }
     }
     if ((s = run_scan(c, EwCountIn{A->row_ptr, B->row_ptr, T.dups, static_cast<int>(op)}, m, c_row_ptr_dev)) !=
         WINGSPAN_OK)
@@ -1703,6 +1775,7 @@ wingspan_status wingspan_elementwise_structure(wingspan_ew_op op, const wingspan
     HIP_TRY(hipMemcpyAsync(&total, c_row_ptr_dev + m, sizeof(int64_t), hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
     *c_nnz = total;
+    if (planned) ew_remember(ew_key_of(op, A, B, workspace_dev, workspace_bytes));
     return WINGSPAN_OK;
 }
 
@@ -1723,9 +1796,16 @@ wingspan_status wingspan_elementwise_values(wingspan_ew_op op, const wingspan_cs
     Ctx c{};
     c.st = static_cast<hipStream_t>(stream);
     c.ws = static_cast<char *>(workspace_dev);
-    if (dtype == WINGSPAN_F32)
-        return ew_values_impl<float>(c, op, A, B, L, c_col_idx_dev, static_cast<float *>(c_val_dev));
-    return ew_values_impl<double>(c, op, A, B, L, c_col_idx_dev, static_cast<double *>(c_val_dev));
+    const EwPlanKey key = ew_key_of(op, A, B, workspace_dev, workspace_bytes);
+    const bool planned = ew_known(key);
+    if (!planned) ew_forget(workspace_dev, workspace_bytes);
+    s = dtype == WINGSPAN_F32
+            ? ew_values_impl<float>(c, op, A, B, L, c_col_idx_dev, static_cast<float *>(c_val_dev), planned)
+            : ew_values_impl<double>(c, op, A, B, L, c_col_idx_dev, static_cast<double *>(c_val_dev), planned);
+    if (s == WINGSPAN_OK && !planned && A->nrows > 0 && L.ntiles > 0 &&
+        !(op == WINGSPAN_OP_HADAMARD && (A->nnz == 0 || B->nnz == 0)))
+        ew_remember(key);
+    return s;
 }
 
 wingspan_status wingspan_spmspv_workspace_size(const wingspan_csr *At, int64_t nnz_x, size_t *bytes) {
@@ -1742,6 +1822,7 @@ wingspan_status wingspan_spmspv(const wingspan_csr *At, wingspan_dtype dtype, co
                                 int64_t y_cap, int64_t *y_nnz, void *workspace_dev, size_t workspace_bytes,
                                 void *stream) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     wingspan_status s = sv_check(At, nnz_x);
     if (s != WINGSPAN_OK) return s;
     if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)
@@ -1784,6 +1865,7 @@ wingspan_status wingspan_outer_workspace_size(const wingspan_csr *At, const wing
 wingspan_status wingspan_outer_products(const wingspan_csr *At, const wingspan_csr *B, int64_t *products,
                                         void *workspace_dev, size_t workspace_bytes, void *stream) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     wingspan_status s = op_check(At, B);
     if (s != WINGSPAN_OK) return s;
     if (!products) return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "products is NULL");
@@ -1800,6 +1882,7 @@ wingspan_status wingspan_spgemm_outer(const wingspan_csr *At, const wingspan_csr
                                       int64_t c_capacity, int64_t *c_nnz, void *workspace_dev, size_t workspace_bytes,
                                       void *stream) {
     g_err.clear();
+    ew_forget(workspace_dev, workspace_bytes);   // a kept elementwise tiling is overwritten
     wingspan_status s = op_check(At, B);
     if (s != WINGSPAN_OK) return s;
     if (dtype != WINGSPAN_F32 && dtype != WINGSPAN_F64)

@@ -129,3 +129,43 @@ def test_values_rerun_with_new_values():
             ref = OPS[op](A2, B)
             assert np.array_equal(col[:nnz].cpu().numpy(), ref.col_idx)
             assert np.array_equal(val[:nnz].cpu().numpy(), ref.val), f"{op} scale {scale}"
+
+
+def test_values_after_the_workspace_served_another_call():
+    # the values call reuses the tiling a structure call left in the workspace only while nothing else has
+    # used that workspace: after an SpGEMM (or the other operation's structure) on the same memory it tiles
+    # again, and after a values call of another operation it tiles for its own
+    import torch
+    from paper_2606_20855_amd import wingspan as ws
+    A = matgen.rmat(11, 8, seed=47, dtype=np.float64)
+    B = matgen.shuffled_copy(A, 48)
+    dA, dB = ws.DeviceCSR.from_host(A, "cuda:0"), ws.DeviceCSR.from_host(B, "cuda:0")
+    Ad, Bd = dA.desc(), dB.desc()
+    need = max(ws.wingspan_elementwise_workspace_size(Ad, Bd), ws.wingspan_spgemm_workspace_size(Ad, Ad, ws.F64))
+    wsb = torch.empty(need, dtype=torch.uint8, device="cuda:0")
+    refs = {ws.OP_ADD: ew_oracle.spadd(A, B), ws.OP_HADAMARD: ew_oracle.hadamard(A, B)}
+    rps = {}
+    for code in refs:
+        rps[code] = torch.empty(A.nrows + 1, dtype=torch.int64, device="cuda:0")
+        assert ws.wingspan_elementwise_structure(code, Ad, Bd, rps[code].data_ptr(), wsb.data_ptr(),
+                                                 need) == refs[code].nnz
+
+    def values(code):
+        ref = refs[code]
+        col = torch.full((max(ref.nnz, 1),), -1, dtype=torch.int32, device="cuda:0")
+        val = torch.full((max(ref.nnz, 1),), np.nan, dtype=torch.float64, device="cuda:0")
+        ws.wingspan_elementwise_values(code, Ad, Bd, ws.F64, rps[code].data_ptr(), col.data_ptr(), val.data_ptr(),
+                                       wsb.data_ptr(), need)
+        torch.cuda.synchronize()
+        assert np.array_equal(col[:ref.nnz].cpu().numpy(), ref.col_idx)
+        assert np.array_equal(val[:ref.nnz].cpu().numpy().view(np.uint8), ref.val.view(np.uint8))
+
+    values(ws.OP_ADD)          # the workspace holds the product's tiling: tiles again
+    values(ws.OP_HADAMARD)     # the sum's tiling is there now
+    values(ws.OP_HADAMARD)     # its own, kept
+    c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device="cuda:0")
+    ws.wingspan_spgemm_symbolic(Ad, Ad, c_rp.data_ptr(), wsb.data_ptr(), need)
+    values(ws.OP_HADAMARD)     # overwritten by the SpGEMM
+    assert ws.wingspan_elementwise_structure(ws.OP_ADD, Ad, Bd, rps[ws.OP_ADD].data_ptr(), wsb.data_ptr(),
+                                             need) == refs[ws.OP_ADD].nnz
+    values(ws.OP_ADD)          # kept from the structure call
