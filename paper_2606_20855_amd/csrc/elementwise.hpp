@@ -312,7 +312,8 @@ struct EwTileIn {
 // A half takes a + b) and, for the product, the A half of each common
 // coordinate (a * b). The kept entries' values are then read (all loads of a
 // thread issued together, overlapping the scan of the kept counts that places
-// them), formed in double and rounded once.
+// them), formed in double and rounded once, and the tile's part of C is
+// staged in LDS and written with coalesced stores.
 template <typename V, int OP>
 __global__ void __launch_bounds__(kEwBlock) ew_tile_write(const int32_t *__restrict__ a_rp,
                                                           const int32_t *__restrict__ a_col,
@@ -326,6 +327,7 @@ __global__ void __launch_bounds__(kEwBlock) ew_tile_write(const int32_t *__restr
                                                           const int64_t *__restrict__ tile_off,
                                                           int32_t *__restrict__ c_col, V *__restrict__ c_val) {
     __shared__ int64_t s_key[kEwTile + 1];
+    __shared__ int32_t s_ocol[kEwTile + 1];
     __shared__ int32_t scratch[kEwBlock / kWave];
     const EwTile T = ew_tile_of(split_a, split_b, split_r);
     ew_load_tile<false, V>(T, a_rp, a_col, nullptr, b_rp, b_col, nullptr, s_key, nullptr, scratch);
@@ -375,16 +377,28 @@ __global__ void __launch_bounds__(kEwBlock) ew_tile_write(const int32_t *__restr
         bv[u] = bi[u] >= 0 ? to_d(b_val[T.ib0 + bi[u]]) : 0.0;
     }
     int tot;
-    int64_t p = tile_off[blockIdx.x] + block_excl_scan<kEwBlock>(c, &tot, scratch);
+    int p = block_excl_scan<kEwBlock>(c, &tot, scratch);   // (its barriers end every thread's walk)
+    // the tile's entries of C staged in LDS in order (values over the keys), then written coalesced
+    V *s_oval = reinterpret_cast<V *>(s_key);
 #pragma unroll
     for (int u = 0; u < kEwPer; ++u) {
         if (ai[u] >= 0 || bi[u] >= 0) {
             double v;
             if (OP == kEwMul) v = av[u] * bv[u];
             else v = ai[u] >= 0 && bi[u] >= 0 ? av[u] + bv[u] : (ai[u] >= 0 ? av[u] : bv[u]);
-            c_col[p] = oc[u];
-            c_val[p] = static_cast<V>(v);
+            s_ocol[p] = oc[u];
+            s_oval[p] = static_cast<V>(v);
             ++p;
+        }
+    }
+    __syncthreads();
+    const int64_t base = tile_off[blockIdx.x];
+#pragma unroll
+    for (int u = 0; u < kEwPer; ++u) {
+        const int e = threadIdx.x + u * kEwBlock;
+        if (e < tot) {
+            c_col[base + e] = s_ocol[e];
+            c_val[base + e] = s_oval[e];
         }
     }
 }
