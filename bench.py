@@ -521,7 +521,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="rmat18")
-    ap.add_argument("--cpu-fraction", type=float, default=0.2)
+    ap.add_argument("--cpu-fraction", type=float, default=0.3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES")
     ap.add_argument("--no-sharded", action="store_true", help="skip the single-pass (sharded output) timing")
