@@ -318,16 +318,115 @@ __device__ int64_t rank_emit_regs(const int32_t (&kk)[PER], const double (&vv)[P
     return out;
 }
 
+// Writes the entries a workgroup holds in registers (thread t: keys kk[j] and
+// sums vv[j], kEmptyKey where none; distinct columns) to C[cb + ...] in
+// increasing column order, at a cost that follows the entries, not the column
+// range. The columns are cut into nb buckets of W = 2^sh columns; each entry
+// counts itself into its bucket (an LDS atomic that also gives it a place in
+// the bucket); one exclusive scan gives every bucket its first output position
+// and numbers the heavy buckets (more than H = max(8, W/16) entries); the
+// entries are staged bucket by bucket. An entry's position is its bucket's
+// first plus its rank in the bucket: in a light bucket, the staged entries
+// with a smaller column (at most H to compare); in a heavy bucket, the set
+// bits below it in the bucket's own bitmap of W bits (heavy buckets number at
+// most entries / H, so their bitmaps take at most half an int per entry).
+// mem holds nb + 1 ints of counts and then the heavy buckets' bitmaps; stage
+// one int per entry. Entries number at most 65535. Writes never reach past
+// C[cb + seg). Returns the number of entries (uniform).
+template <int BLOCK, int PER, typename V>
+__device__ int64_t bucket_emit_regs(const int32_t (&kk)[PER], const double (&vv)[PER], int sh, int nb,
+                                    int32_t *mem, int32_t *stage, int32_t *scratch, int32_t *__restrict__ c_col,
+                                    V *__restrict__ c_val, int64_t cb, int64_t seg) {
+    int32_t *cnt = mem;
+    uint32_t *bm = reinterpret_cast<uint32_t *>(mem + nb + 1);
+    const int W = 1 << sh;
+    const int WB = W > 32 ? W >> 5 : 1;   // bitmap words per heavy bucket
+    const int H = W / 16 > 8 ? W / 16 : 8;
+    for (int i = threadIdx.x; i <= nb; i += BLOCK) cnt[i] = 0;
+    __syncthreads();
+    int q[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) q[j] = kk[j] != kEmptyKey ? atomicAdd(&cnt[kk[j] >> sh], 1) : 0;
+    __syncthreads();
+    // exclusive scan, in place, of count | (heavy << 16): low half the bucket's first position, high half its
+    // heavy-bucket index; cnt[nb] receives the totals
+    const int per = (nb + BLOCK - 1) / BLOCK;
+    const int b0 = static_cast<int>(threadIdx.x) * per;
+    int part = 0;
+    for (int i = 0; i < per; ++i) {
+        const int c = b0 + i < nb ? cnt[b0 + i] : 0;
+        part += c | (c > H ? 1 << 16 : 0);
+    }
+    int total;
+    int run = block_excl_scan<BLOCK>(part, &total, scratch);
+    for (int i = 0; i < per; ++i) {
+        if (b0 + i < nb) {
+            const int c = cnt[b0 + i];
+            cnt[b0 + i] = run;
+            run += c | (c > H ? 1 << 16 : 0);
+        }
+    }
+    if (threadIdx.x == 0) cnt[nb] = total;
+    __syncthreads();
+    const int nwords = (total >> 16) * WB;
+    for (int i = threadIdx.x; i < nwords; i += BLOCK) bm[i] = 0u;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        if (kk[j] != kEmptyKey) stage[(cnt[kk[j] >> sh] & 0xffff) + q[j]] = kk[j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int k = kk[j];
+        if (k == kEmptyKey) continue;
+        const int b = k >> sh;
+        const int lo = cnt[b], hi = cnt[b + 1];
+        if ((hi & 0xffff) - (lo & 0xffff) > H) {
+            const int rel = k - (b << sh);
+            atomicOr(&bm[(lo >> 16) * WB + (rel >> 5)], 1u << (rel & 31));
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int k = kk[j];
+        if (k == kEmptyKey) continue;
+        const int b = k >> sh;
+        const int lo = cnt[b], hi = cnt[b + 1];
+        const int first = lo & 0xffff, last = hi & 0xffff;
+        int r = 0;
+        if (last - first > H) {
+            const int rel = k - (b << sh);
+            const uint32_t *w = bm + (lo >> 16) * WB;
+            for (int i = 0; i < (rel >> 5); ++i) r += __popc(w[i]);
+            r += __popc(w[rel >> 5] & ((1u << (rel & 31)) - 1u));
+        } else {
+            for (int i = first; i < last; ++i) r += stage[i] < k;
+        }
+        const int64_t pos = first + r;
+        if (pos < seg) {
+            c_col[cb + pos] = k;
+            c_val[cb + pos] = static_cast<V>(vv[j]);
+        }
+    }
+    return total & 0xffff;
+}
+
 // ---------------------------------------------------------------------------
 // Hash tier: one workgroup per row, an LDS table of 2^LOG2T slots.
 // Symbolic keeps keys only and counts first insertions. Numeric also adds the
-// product into the slot's double, then writes the row in column order: tables
-// of 1024 slots and more by rank emission (the slots move to registers and the
-// table's memory takes the presence bitmap; popcount ranks, no sort) when the
-// column space takes at most kMaxRankWindows bitmap windows, otherwise (and
-// for smaller tables) by compacting the slots and bitonic-sorting them in LDS.
+// product into the slot's double, then writes the row in column order, the
+// slots moved to registers and the table's memory reused, without a sort:
+// tables of 1024 slots and more by rank over a presence bitmap of the columns
+// when it takes at most kBitmapEmitMaxWindows windows of the table's memory;
+// otherwise tables of 512 slots and more by column buckets (bucket_emit_regs)
+// while a bucket spans at most 2^kBucketEmitMaxLog2Width columns, then the
+// bitmap again up to kMaxRankWindows windows. Smaller tables, and wider
+// column ranges, compact the slots and bitonic-sort them in LDS.
 // ---------------------------------------------------------------------------
 constexpr int kMaxRankWindows = 4;
+constexpr int kBucketEmitMinLog2 = 9;        // tables this large or larger emit by column buckets
+constexpr int kBitmapEmitMaxWindows = 2;     // ... unless the column bitmap takes at most this many windows
+constexpr int kBucketEmitMaxLog2Width = 9;   // ... while a bucket spans at most 512 columns
 
 template <int LOG2T>
 struct HashShape {
@@ -406,6 +505,21 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
         kk[j] = keys[s2];
         vv[j] = vals[s2];
         cnt += kk[j] != kEmptyKey;
+    }
+    if constexpr (LOG2T >= kBucketEmitMinLog2) {
+        // buckets of 2^sh columns, at most T of them (the doubles' memory holds their counts and the heavy
+        // buckets' bitmaps, the keys' the staged entries); where the column range takes at most
+        // kBitmapEmitMaxWindows windows of the table's bitmap, rank emission over the bitmap is cheaper
+        const int sh = uniform(ceil_log2(ncols) > LOG2T ? ceil_log2(ncols) - LOG2T : 0);
+        const int64_t nbw = BWW > 0 ? (ncols + int64_t(BWW) * 32 - 1) / (int64_t(BWW) * 32) : INT64_MAX;
+        if (sh <= kBucketEmitMaxLog2Width && nbw > kBitmapEmitMaxWindows) {
+            __syncthreads();   // every slot is read: the table's memory takes the counts and the staged keys
+            const int nb = static_cast<int>((ncols + (int64_t(1) << sh) - 1) >> sh);
+            const int64_t total = bucket_emit_regs<BLOCK, PER, V>(kk, vv, sh, nb, reinterpret_cast<int32_t *>(vals),
+                                                                  keys, scratch, c_col, c_val, cb, seg);
+            if (threadIdx.x == 0 && !out.pooled() && total != seg) atomicOr(&ctrl->error_flags, kErrRowMismatch);
+            return;
+        }
     }
     if constexpr (BWW > 0) {
         const int64_t nbw = (ncols + int64_t(BWW) * 32 - 1) / (int64_t(BWW) * 32);

@@ -186,6 +186,31 @@ def test_hash_rows_rank_emission_windows(r, dtype):
     assert num["rows"]["hash"] == 64
 
 
+@pytest.mark.parametrize("ncols,r", [(1_000_000, 25), (1_000_000, 50), (1_000_000, 90), (3_000_000, 50),
+                                     (20_000, 40)])
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_hash_rows_bucket_emission(ncols, r, dtype):
+    # hash rows over wide column ranges: tables of 512 to 4096 slots write their rows by column buckets of
+    # up to 512 columns, wider buckets fall back to the bitmap or a sort (3 M columns)
+    dist = "pm1" if dtype == np.float64 else "open01"
+    A = matgen.er(64, 3000, r, seed=80 + r, dtype=dtype, dist=dist)
+    B = matgen.er(3000, ncols, 20, seed=79, dtype=dtype, dist=dist)
+    got, sym, num, ref = check(A, B, None, what=f"hash buckets n={ncols} r={r}")
+    assert num["rows"]["hash"] == 64
+
+
+@pytest.mark.parametrize("r", [8, 20, 60])
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_hash_rows_bucket_emission_skewed_columns(r, dtype):
+    # B's columns are R-MAT's (heavy-tailed toward low indices), so the rows' low-column buckets hold many
+    # entries and take their ranks from per-bucket bitmaps
+    dist = "pm1" if dtype == np.float64 else "open01"
+    B = matgen.rmat(14, 16, seed=84, dtype=dtype, dist=dist)
+    A = matgen.er(200, B.nrows, r, seed=85 + r, dtype=dtype, dist=dist)
+    got, sym, num, ref = check(A, B, None, what=f"hash buckets skewed r={r}")
+    assert num["rows"]["hash"] > 0
+
+
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
 def test_dense_rows_beyond_entry_cache(dtype):
     # 400 A entries per row, more than the 256 whose bounds the rank kernel
