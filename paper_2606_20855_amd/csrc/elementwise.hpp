@@ -33,22 +33,6 @@ constexpr int kEwPer = (kEwTile + 1 + kEwBlock - 1) / kEwBlock;   // consecutive
 enum EwOp { kEwAdd = 0, kEwMul = 1 };
 constexpr int64_t kEwEnd = 0x7fffffffffffffffll;   // above every (row, column) key
 
-// Last r in [lo, hi] with f(r) <= q, for a non-decreasing f with f(lo) <= q:
-// a 64-ary search in which all 64 lanes of one wave take part.
-template <typename F>
-__device__ __forceinline__ int wave_last_le(F f, int lo, int hi, int64_t q) {
-    while (hi > lo) {
-        const int64_t step = (static_cast<int64_t>(hi) - lo + kWave) / kWave;
-        const int64_t idx = lo + lane_id() * step;
-        const bool le = idx <= hi && f(static_cast<int>(idx)) <= q;
-        const uint64_t m = ballot(le);   // lane 0 always qualifies
-        lo = static_cast<int>(lo + (63 - __clzll(m)) * step);
-        const int64_t h = lo + step - 1;
-        hi = h < hi ? static_cast<int>(h) : hi;
-    }
-    return lo;
-}
-
 // Tile boundaries, one wave each: for t in [0, ntiles], d = min(t kEwTile,
 // nnz(A) + nnz(B)); split_a[t] and split_b[t] count the A and B entries before
 // boundary t and split_r[t] is the row holding it (nrows - 1 at the end).

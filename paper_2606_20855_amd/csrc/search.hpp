@@ -34,6 +34,22 @@ __device__ __forceinline__ int lds_find_entry(const int64_t *s, int n, int64_t q
     return lo;
 }
 
+// Last r in [lo, hi] with f(r) <= q, for a non-decreasing f with f(lo) <= q:
+// a 64-ary search in which all 64 lanes of one wave take part.
+template <typename F>
+__device__ __forceinline__ int wave_last_le(F f, int lo, int hi, int64_t q) {
+    while (hi > lo) {
+        const int64_t step = (static_cast<int64_t>(hi) - lo + kWave) / kWave;
+        const int64_t idx = lo + lane_id() * step;
+        const bool le = idx <= hi && f(static_cast<int>(idx)) <= q;
+        const uint64_t m = ballot(le);   // lane 0 always qualifies
+        lo = static_cast<int>(lo + (63 - __clzll(m)) * step);
+        const int64_t h = lo + step - 1;
+        hi = h < hi ? static_cast<int>(h) : hi;
+    }
+    return lo;
+}
+
 // Merge-path split of the stable merge of sorted a[0, na) and b[0, nb), a's
 // entries first among equal keys: the number of a's entries among the first d
 // outputs, i.e. the least i in [max(0, d - nb), min(d, na)] with

@@ -134,6 +134,383 @@ __global__ void __launch_bounds__(kSvBlock) sv_scatter(const int32_t *__restrict
     }
 }
 
+// Bucketed scatter: the products are sorted by the range of kSvRange = 4096
+// positions of y their row falls in (a range is an emission tile), so each
+// range can be summed in LDS by workgroups of its own, with no global atomics
+// where one workgroup holds a whole range.
+//   sv_bin:   a workgroup forms kSvBin products (as sv_scatter does), sorts them
+//             by range in LDS (counting sort) and writes them back to its chunk
+//             of tmp; tab[r * nc + c] receives chunk c's count of range r;
+//   (scan):   the exclusive scan of tab in range-major order gives every
+//             (range, chunk) run its place in the range-sorted order, gpos;
+//   sv_place: each chunk copies its runs to their places (coalesced runs);
+//   (scan):   each range is cut into pieces of at most kSvPieceMax products;
+//   sv_accumulate: a workgroup takes a piece, sums it in an LDS accumulator
+//             over the range's positions, and writes the sums: with plain
+//             stores for a range of one piece, with global double atomics for
+//             the rows it touched of a range of several, setting the flags.
+constexpr int kSvRangeShift = 12;
+constexpr int kSvRange = 1 << kSvRangeShift;
+constexpr int kSvBin = 4096;
+constexpr int kSvBinBlock = 256;
+constexpr int kSvBinPer = kSvBin / kSvBinBlock;
+constexpr int kSvBinStage = 2048;     // x entries a binning chunk stages in LDS
+constexpr int kSvMaxRanges = 2048;    // y of at most 8 M positions takes the bucketed scatter
+constexpr int kSvPieceMax = 16384;   // sorted products per accumulating workgroup at most
+constexpr int kSvAccBlock = 256;
+constexpr int kSvAccPer = 16;                       // products per thread and pass
+
+// Product q's row of y and value, for a chunk whose x entries [t0, t0 + nt)
+// are staged (s_pref, s_base, s_x) when nt <= kSvBinStage, else looked up in
+// global memory.
+template <typename V>
+__device__ __forceinline__ void sv_product(const int32_t *__restrict__ at_rp, const int32_t *__restrict__ at_row,
+                                           const V *__restrict__ at_val, const int32_t *__restrict__ x_idx,
+                                           const V *__restrict__ x_val, const int64_t *__restrict__ pref,
+                                           const int64_t *s_pref, const int64_t *s_base, const double *s_x, int t0,
+                                           int nt, bool staged, int64_t q, int *row, double *v) {
+    int64_t pos;
+    double xv;
+    if (staged) {
+        int lo = 0, hi = nt - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_pref[mid] <= q) lo = mid;
+            else hi = mid - 1;
+        }
+        pos = s_base[lo] + q;
+        xv = s_x[lo];
+    } else {
+        int lo = t0, hi = t0 + nt - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (pref[mid] <= q) lo = mid;
+            else hi = mid - 1;
+        }
+        pos = static_cast<int64_t>(at_rp[x_idx[lo]]) + (q - pref[lo]);
+        xv = to_d(x_val[lo]);
+    }
+    *row = at_row[pos];
+    *v = to_d(at_val[pos]) * xv;
+}
+
+template <typename V>
+__global__ void __launch_bounds__(kSvBinBlock) sv_bin(const int32_t *__restrict__ at_rp,
+                                                      const int32_t *__restrict__ at_row,
+                                                      const V *__restrict__ at_val,
+                                                      const int32_t *__restrict__ x_idx,
+                                                      const V *__restrict__ x_val, int nnz_x,
+                                                      const int64_t *__restrict__ pref, const int32_t *err,
+                                                      int nranges, int64_t nc, int32_t *__restrict__ tab,
+                                                      int32_t *__restrict__ tmp_row, double *__restrict__ tmp_val) {
+    __shared__ int32_t s_cnt[kSvMaxRanges + 1];
+    __shared__ int32_t s_own[kSvBin];   // each product's x entry (relative to the chunk's first)
+    // x entries staged while the products are formed, then the chunk's products sorted by range
+    __shared__ __align__(16) char s_mem[kSvBin * (sizeof(int32_t) + sizeof(double))];
+    __shared__ int s_t[2];
+    __shared__ int32_t scratch[kSvBinBlock / kWave];
+    double *s_x = reinterpret_cast<double *>(s_mem);                          // kSvBinStage entries
+    int32_t *s_base = reinterpret_cast<int32_t *>(s_x + kSvBinStage);         // at_rp[x_idx[t]] - pref[t]
+    int32_t *s_row = reinterpret_cast<int32_t *>(s_mem);
+    double *s_val = reinterpret_cast<double *>(s_mem + kSvBin * sizeof(int32_t));
+    if (*err != 0) return;   // whole grid
+    const int64_t P = pref[nnz_x];
+    // chunks taken grid-stride: the grid is sized for the most products x could select
+    for (int64_t c = blockIdx.x; c * kSvBin < P; c += gridDim.x) {
+    const int64_t q0 = c * kSvBin;
+    const int64_t q1 = P - q0 < kSvBin ? P : q0 + kSvBin;
+    const int n = static_cast<int>(q1 - q0);
+    if (threadIdx.x < kWave) {
+        const int t0 = wave_find_entry(pref, nnz_x, q0);
+        const int t1 = wave_find_entry(pref, nnz_x, q1 - 1);
+        if (threadIdx.x == 0) {
+            s_t[0] = t0;
+            s_t[1] = t1;
+        }
+    }
+    for (int r = threadIdx.x; r < nranges; r += kSvBinBlock) s_cnt[r] = 0;
+    for (int e = threadIdx.x; e < kSvBin; e += kSvBinBlock) s_own[e] = -1;
+    __syncthreads();
+    const int t0 = s_t[0];
+    const int nt = s_t[1] - t0 + 1;
+    const bool staged = nt <= kSvBinStage;
+    // each x entry of the chunk with products marks the first of them in the chunk (the chunk's first
+    // product belongs to entry t0), staging its column start and value when the entries fit
+    for (int k0 = 0; k0 < nt; k0 += kSvBinBlock * 4) {
+        int64_t pa[4], pb[4];
+        int xi[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int k = k0 + static_cast<int>(threadIdx.x) + u * kSvBinBlock;
+            const int t = t0 + (k < nt ? k : 0);
+            pa[u] = pref[t];
+            pb[u] = pref[t + 1];
+            xi[u] = x_idx[t];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int k = k0 + static_cast<int>(threadIdx.x) + u * kSvBinBlock;
+            if (k < nt) {
+                if (pb[u] > pa[u] && pa[u] >= q0) s_own[pa[u] - q0] = k;
+                if (staged) {
+                    s_base[k] = static_cast<int32_t>(at_rp[xi[u]] - pa[u]);
+                    s_x[k] = to_d(x_val[t0 + k]);
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // the owners by an exclusive max-scan over the chunk's products, kSvBinPer consecutive ones per thread
+    {
+        const int e0 = static_cast<int>(threadIdx.x) * kSvBinPer;
+        int mk[kSvBinPer];
+        int x = -1;
+#pragma unroll
+        for (int u = 0; u < kSvBinPer; ++u) {
+            mk[u] = e0 + u == 0 ? 0 : s_own[e0 + u];
+            x = x > mk[u] ? x : mk[u];
+        }
+        int incl = wave_incl_max(x);
+        const int w = threadIdx.x / kWave;
+        if (lane_id() == kWave - 1) scratch[w] = incl;
+        __syncthreads();
+        int before = -1;
+#pragma unroll
+        for (int i = 0; i < kSvBinBlock / kWave; ++i) before = i < w && scratch[i] > before ? scratch[i] : before;
+        int prev = __shfl_up(incl, 1, kWave);
+        int run = lane_id() == 0 ? before : (prev > before ? prev : before);
+#pragma unroll
+        for (int u = 0; u < kSvBinPer; ++u) {
+            run = run > mk[u] ? run : mk[u];
+            s_own[e0 + u] = run;
+        }
+    }
+    __syncthreads();
+    int row[kSvBinPer], slot[kSvBinPer];
+    double v[kSvBinPer];
+    {
+        // every product's A entry loaded before the first is used
+        int64_t pos[kSvBinPer];
+        double xv[kSvBinPer];
+        if (staged) {
+#pragma unroll
+            for (int u = 0; u < kSvBinPer; ++u) {
+                const int e = threadIdx.x + u * kSvBinBlock;
+                const int k = s_own[e < n ? e : 0];
+                pos[u] = static_cast<int64_t>(s_base[k]) + q0 + (e < n ? e : 0);
+                xv[u] = s_x[k];
+            }
+        } else {
+            int jx[kSvBinPer];
+            int64_t pk[kSvBinPer];
+#pragma unroll
+            for (int u = 0; u < kSvBinPer; ++u) {
+                const int e = threadIdx.x + u * kSvBinBlock;
+                const int t = t0 + s_own[e < n ? e : 0];
+                jx[u] = x_idx[t];
+                pk[u] = pref[t];
+                xv[u] = to_d(x_val[t]);
+            }
+#pragma unroll
+            for (int u = 0; u < kSvBinPer; ++u) {
+                const int e = threadIdx.x + u * kSvBinBlock;
+                pos[u] = static_cast<int64_t>(at_rp[jx[u]]) + (q0 + (e < n ? e : 0) - pk[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kSvBinPer; ++u) {
+            row[u] = at_row[pos[u]];
+            v[u] = to_d(at_val[pos[u]]) * xv[u];
+        }
+#pragma unroll
+        for (int u = 0; u < kSvBinPer; ++u) {
+            const int e = threadIdx.x + u * kSvBinBlock;
+            if (e >= n) row[u] = -1;
+            slot[u] = row[u] >= 0 ? atomicAdd(&s_cnt[row[u] >> kSvRangeShift], 1) : 0;
+        }
+    }
+    __syncthreads();   // every count is in, and the x staging is read no more
+    // the counts to the table, then their exclusive scan in place (contiguous shares per thread)
+    const int per = (nranges + kSvBinBlock - 1) / kSvBinBlock;
+    const int r0 = static_cast<int>(threadIdx.x) * per;
+    int part = 0;
+    for (int i = 0; i < per; ++i) {
+        const int r = r0 + i;
+        if (r < nranges) {
+            const int cnt = s_cnt[r];
+            tab[static_cast<int64_t>(r) * nc + c] = cnt;
+            part += cnt;
+        }
+    }
+    int total;
+    int run = block_excl_scan<kSvBinBlock>(part, &total, scratch);
+    for (int i = 0; i < per; ++i) {
+        const int r = r0 + i;
+        if (r < nranges) {
+            const int cnt = s_cnt[r];
+            s_cnt[r] = run;
+            run += cnt;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kSvBinPer; ++u) {
+        if (row[u] >= 0) {
+            const int k = s_cnt[row[u] >> kSvRangeShift] + slot[u];
+            s_row[k] = row[u];
+            s_val[k] = v[u];
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < n; e += kSvBinBlock) {
+        tmp_row[q0 + e] = s_row[e];
+        tmp_val[q0 + e] = s_val[e];
+    }
+    __syncthreads();   // LDS is reused by the next chunk
+    }
+}
+
+// tab read in range-major order for the scan; chunks past the product count
+// (the grid is sized by At's entries) count nothing.
+struct SvTabIn {
+    const int32_t *tab;
+    const int64_t *pref;
+    int nnz_x;
+    int64_t nc;
+    __device__ __forceinline__ int64_t operator()(int64_t i) const {
+        const int64_t c = i % nc;
+        return c * kSvBin < pref[nnz_x] ? tab[i] : 0;
+    }
+};
+
+// Chunk c's runs to their places in the range-sorted order: entry e of the
+// chunk (range r = its row's range) goes to gpos[r nc + c] + e - (the chunk's
+// entries before range r).
+__global__ void __launch_bounds__(kSvBinBlock) sv_place(const int32_t *__restrict__ tmp_row,
+                                                        const double *__restrict__ tmp_val,
+                                                        const int64_t *__restrict__ pref, int nnz_x,
+                                                        const int32_t *err, int nranges, int64_t nc,
+                                                        const int32_t *__restrict__ tab,
+                                                        const int64_t *__restrict__ gpos,
+                                                        int32_t *__restrict__ s_row_out,
+                                                        double *__restrict__ s_val_out) {
+    __shared__ int64_t s_dst[kSvMaxRanges];   // gpos of each range's run minus its first entry in the chunk
+    __shared__ int32_t scratch[kSvBinBlock / kWave];
+    if (*err != 0) return;
+    const int64_t P = pref[nnz_x];
+    for (int64_t c = blockIdx.x; c * kSvBin < P; c += gridDim.x) {
+    const int64_t q0 = c * kSvBin;
+    const int n = static_cast<int>(P - q0 < kSvBin ? P - q0 : kSvBin);
+    const int per = (nranges + kSvBinBlock - 1) / kSvBinBlock;
+    const int r0 = static_cast<int>(threadIdx.x) * per;
+    int part = 0;
+    for (int i = 0; i < per; ++i)
+        if (r0 + i < nranges) part += tab[static_cast<int64_t>(r0 + i) * nc + c];
+    int total;
+    int run = block_excl_scan<kSvBinBlock>(part, &total, scratch);
+    for (int i = 0; i < per; ++i) {
+        const int r = r0 + i;
+        if (r < nranges) {
+            const int64_t k = static_cast<int64_t>(r) * nc + c;
+            s_dst[r] = gpos[k] - run;
+            run += tab[k];
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < n; e += kSvBinBlock) {
+        const int row = tmp_row[q0 + e];
+        const int64_t d = s_dst[row >> kSvRangeShift] + e;
+        s_row_out[d] = row;
+        s_val_out[d] = tmp_val[q0 + e];
+    }
+    __syncthreads();   // s_dst is reused by the next chunk
+    }
+}
+
+// Range r's first place in the sorted order (r = nranges: the product count).
+struct SvRangeStart {
+    const int64_t *gpos;
+    int64_t nc;
+    __device__ __forceinline__ int64_t operator()(int r) const { return gpos[static_cast<int64_t>(r) * nc]; }
+};
+
+// The pieces of range r: its sorted products cut into runs of kSvPieceMax.
+struct SvPiecesIn {
+    const int64_t *gpos;
+    int64_t nc;
+    __device__ __forceinline__ int64_t operator()(int64_t r) const {
+        const int64_t len = gpos[(r + 1) * nc] - gpos[r * nc];
+        return (len + kSvPieceMax - 1) / kSvPieceMax;
+    }
+};
+
+// Piece g (of piece_pre[nranges], grid-stride): range r's products
+// [start + k kSvPieceMax, ...) summed in LDS, then written: with plain stores
+// when the range is one piece, else its touched rows added with global double
+// atomics; the flags set. yval and the flags start at zero.
+__global__ void __launch_bounds__(kSvAccBlock) sv_accumulate(const int32_t *__restrict__ s_row_in,
+                                                             const double *__restrict__ s_val_in,
+                                                             const int32_t *err, int nranges, int64_t nc,
+                                                             const int64_t *__restrict__ gpos,
+                                                             const int64_t *__restrict__ piece_pre,
+                                                             uint8_t *__restrict__ flag, double *__restrict__ yval) {
+    __shared__ double acc[kSvRange];
+    __shared__ uint8_t touched[kSvRange];
+    __shared__ int s_r;
+    if (*err != 0) return;
+    const int64_t npieces = piece_pre[nranges];
+    for (int t = threadIdx.x; t < kSvRange; t += kSvAccBlock) {
+        acc[t] = 0.0;
+        touched[t] = 0;
+    }
+    const SvRangeStart rs{gpos, nc};
+    for (int64_t g = blockIdx.x; g < npieces; g += gridDim.x) {
+        if (threadIdx.x < kWave) {
+            // the range holding piece g (a range without pieces starts where the next one does)
+            const int r = wave_last_le([=](int k) { return piece_pre[k]; }, 0, nranges - 1, g);
+            if (threadIdx.x == 0) s_r = r;
+        }
+        __syncthreads();
+        const int r = s_r;
+        const int64_t b0 = rs(r), b1 = rs(r + 1);
+        const int64_t k = g - piece_pre[r];
+        const int64_t lo = b0 + k * kSvPieceMax;
+        const int64_t hi = b1 - lo < kSvPieceMax ? b1 : lo + kSvPieceMax;
+        const bool owner = piece_pre[r + 1] - piece_pre[r] == 1;
+        for (int64_t k0 = lo; k0 < hi; k0 += kSvAccBlock * kSvAccPer) {
+            // kSvAccPer products per thread loaded before the first is added
+            int rw[kSvAccPer];
+            double vl[kSvAccPer];
+#pragma unroll
+            for (int u = 0; u < kSvAccPer; ++u) {
+                const int64_t q = k0 + threadIdx.x + u * kSvAccBlock;
+                rw[u] = q < hi ? s_row_in[q] : -1;
+                vl[u] = q < hi ? s_val_in[q] : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < kSvAccPer; ++u) {
+                if (rw[u] >= 0) {
+                    const int t = rw[u] & (kSvRange - 1);
+                    atomicAdd(&acc[t], vl[u]);
+                    touched[t] = 1;
+                }
+            }
+        }
+        __syncthreads();
+        const int64_t y0 = static_cast<int64_t>(r) << kSvRangeShift;
+        for (int t = threadIdx.x; t < kSvRange; t += kSvAccBlock) {
+            if (touched[t]) {
+                if (owner) yval[y0 + t] = acc[t];
+                else unsafeAtomicAdd(&yval[y0 + t], acc[t]);
+                flag[y0 + t] = 1;
+                acc[t] = 0.0;
+                touched[t] = 0;
+            }
+        }
+        __syncthreads();   // the accumulator is clear for the next piece, s_r rewritable
+    }
+}
+
 // The map is coalesced into y tile by tile: kSvTile positions per workgroup.
 // sv_tile_count counts a tile's stored positions (its flags read as 32-bit
 // words); once the counts are scanned (tile_pre, with the total at

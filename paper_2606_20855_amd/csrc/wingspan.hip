@@ -1203,9 +1203,15 @@ wingspan_status ew_values_impl(Ctx &c, int op, const wingspan_csr *A, const wing
 // ---------------------------------------------------------------------------
 constexpr int64_t kSvMaxGrid = 8192;   // scatter workgroups at most (grid-stride beyond)
 
+constexpr int64_t kSvMaxTable = int64_t(1) << 25;   // (range, chunk) counts of the bucketed scatter at most
+constexpr int64_t kSvBucketGrid = 512;              // its workgroups at most (grid-stride beyond)
+
 struct SvLayout {
     size_t off_pref, off_partials, off_flag, off_yval, off_tiles, off_tile_pre, off_err, total;
+    size_t off_tab, off_gpos, off_piece_pre, off_tmp_row, off_tmp_val, off_srt_row, off_srt_val;
     int64_t ntiles;
+    int64_t nchunks;   // binning chunks (bounded by At's entries)
+    bool bucketed;     // the bucketed scatter (else the atomic one)
 };
 
 SvLayout sv_plan(const wingspan_csr *At, int64_t nnz_x) {
@@ -1223,12 +1229,34 @@ SvLayout sv_plan(const wingspan_csr *At, int64_t nnz_x) {
     off += align_up(sizeof(int32_t) * L.ntiles);
     L.off_pref = off;
     off += align_up(sizeof(int64_t) * (nx + 1));
+    // the bucketed scatter: ranges of y are the emission tiles; its buffers are sized by At's entries (the
+    // product count is known on the device only)
+    const int64_t nnz = std::max<int64_t>(At->nnz, 1);
+    L.nchunks = (nnz + kSvBin - 1) / kSvBin;
+    L.bucketed = L.ntiles <= kSvMaxRanges && L.ntiles * L.nchunks <= kSvMaxTable;
+    const int64_t ntab = L.bucketed ? L.ntiles * L.nchunks : 0;
     L.off_partials = off;
-    off += align_up(sizeof(int64_t) * ((nx + kScanTile - 1) / kScanTile + 2));
+    off += align_up(sizeof(int64_t) * ((std::max<int64_t>(nx, ntab) + kScanTile - 1) / kScanTile + 2));
     L.off_flag = off;
     off += align_up(static_cast<size_t>((m + 3) / 4) * 4);   // cleared as int32 words
     L.off_yval = off;
     off += align_up(sizeof(double) * m);
+    if (L.bucketed) {
+        L.off_tab = off;
+        off += align_up(sizeof(int32_t) * ntab);
+        L.off_gpos = off;
+        off += align_up(sizeof(int64_t) * (ntab + 1));
+        L.off_piece_pre = off;
+        off += align_up(sizeof(int64_t) * (L.ntiles + 1));
+        L.off_tmp_row = off;
+        off += align_up(sizeof(int32_t) * nnz);
+        L.off_tmp_val = off;
+        off += align_up(sizeof(double) * nnz);
+        L.off_srt_row = off;
+        off += align_up(sizeof(int32_t) * nnz);
+        L.off_srt_val = off;
+        off += align_up(sizeof(double) * nnz);
+    }
     L.total = off;
     return L;
 }
@@ -1266,7 +1294,33 @@ wingspan_status sv_impl(Ctx &c, const wingspan_csr *At, const SvLayout &L, const
         c.partials = reinterpret_cast<int64_t *>(c.ws + L.off_partials);
         wingspan_status s = run_scan(c, SvLenIn{At->row_ptr, x_idx, n, err}, nnz_x, pref);
         if (s != WINGSPAN_OK) return s;
-        if (At->nnz > 0) {
+        if (At->nnz > 0 && L.bucketed) {
+            // products sorted by range of y, then each range summed in LDS (grids sized by At's entries; the
+            // kernels read the product count on the device)
+            const int nr = static_cast<int>(L.ntiles);
+            const int64_t nc = L.nchunks;
+            int32_t *tab = reinterpret_cast<int32_t *>(c.ws + L.off_tab);
+            int64_t *gpos = reinterpret_cast<int64_t *>(c.ws + L.off_gpos);
+            int32_t *tmp_row = reinterpret_cast<int32_t *>(c.ws + L.off_tmp_row);
+            double *tmp_val = reinterpret_cast<double *>(c.ws + L.off_tmp_val);
+            int32_t *srt_row = reinterpret_cast<int32_t *>(c.ws + L.off_srt_row);
+            double *srt_val = reinterpret_cast<double *>(c.ws + L.off_srt_val);
+            const unsigned grid = static_cast<unsigned>(std::min<int64_t>(nc, kSvBucketGrid));
+            sv_bin<V><<<grid, kSvBinBlock, 0, c.st>>>(At->row_ptr, At->col_idx, static_cast<const V *>(At->val),
+                                                      x_idx, x_val, static_cast<int>(nnz_x), pref, err, nr, nc, tab,
+                                                      tmp_row, tmp_val);
+            LAUNCH_CHECK("spmspv bin");
+            if ((s = run_scan(c, SvTabIn{tab, pref, static_cast<int>(nnz_x), nc}, nr * nc, gpos)) != WINGSPAN_OK)
+                return s;
+            sv_place<<<grid, kSvBinBlock, 0, c.st>>>(tmp_row, tmp_val, pref, static_cast<int>(nnz_x), err, nr, nc,
+                                                     tab, gpos, srt_row, srt_val);
+            int64_t *piece_pre = reinterpret_cast<int64_t *>(c.ws + L.off_piece_pre);
+            scan_one_block<SvPiecesIn><<<1, 1024, 0, c.st>>>(SvPiecesIn{gpos, nc}, nr, piece_pre);
+            const int64_t pieces = nr + (At->nnz + kSvPieceMax - 1) / kSvPieceMax;   // at most
+            sv_accumulate<<<static_cast<unsigned>(std::min<int64_t>(pieces, kSvBucketGrid)), kSvAccBlock, 0, c.st>>>(
+                srt_row, srt_val, err, nr, nc, gpos, piece_pre, flag, yval);
+            LAUNCH_CHECK("spmspv accumulate");
+        } else if (At->nnz > 0) {
             const int64_t chunks = (At->nnz + kSvChunk - 1) / kSvChunk;
             sv_scatter<V><<<static_cast<unsigned>(std::min<int64_t>(chunks, kSvMaxGrid)), kSvBlock, 0, c.st>>>(
                 At->row_ptr, At->col_idx, static_cast<const V *>(At->val), x_idx, x_val, static_cast<int>(nnz_x),

@@ -138,3 +138,38 @@ def test_rerun_with_new_x():
     for seed in (64, 65):
         xi, xv = matgen.sparse_vector(A.ncols, 0.1, seed, np.float32)
         check(A, xi, xv, f"x seed {seed}")
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_one_range_over_many_pieces(dtype):
+    # y has 3,000 positions (one range of 4096) and 200 K products: the range's sorted products span ~50
+    # pieces of 4096, each summing its share in LDS and adding it to y with atomics
+    A = matgen.random_sparse(3000, 2000, 0.05, 57, dtype)
+    xi, xv = matgen.sparse_vector(2000, 0.7, 58, dtype)
+    _, _, ref = check(A, xi, xv, "one range")
+    assert int(sv.spmspv(A, xi, xv).nnz) == ref.nnz
+
+
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_rmat18_ranges_and_pieces(dtype):
+    # 64 ranges of y; R-MAT's low rows gather many products (a range over several pieces) while most ranges
+    # sit inside one piece and are written with plain stores
+    A = matgen.rmat(18, 8, seed=59, dtype=dtype, dist="open01" if dtype == np.float32 else "pm1")
+    xi, xv = matgen.sparse_vector(A.ncols, 0.1, 60, dtype)
+    check(A, xi, xv, "rmat18")
+
+
+def test_wide_y_takes_the_atomic_scatter():
+    # y of 9 M positions (more ranges than the bucketed scatter's table takes): the atomic scatter
+    rng = np.random.default_rng(61)
+    m, n = 9_000_000, 300
+    rows = np.sort(rng.choice(m, 20000, replace=False))
+    cols = rng.integers(0, n, len(rows))
+    order = np.lexsort((cols, rows))
+    keys = np.unique(rows[order].astype(np.int64) * n + cols[order])
+    r, c = keys // n, keys % n
+    rp = np.zeros(m + 1, np.int64)
+    np.cumsum(np.bincount(r, minlength=m), out=rp[1:])
+    A = matgen.CSR(m, n, rp.astype(np.int32), c.astype(np.int32), rng.uniform(-1, 1, len(c)))
+    xi, xv = matgen.sparse_vector(n, 0.5, 62, np.float64)
+    check(A, xi, xv, "wide y")
