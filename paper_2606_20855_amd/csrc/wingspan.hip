@@ -271,6 +271,7 @@ struct Ctx {
     const int32_t *bins;      // numeric phase: the row ids grouped by bin it uses (perm or perm_num)
     bool wtab_ready = false;  // numeric phase: the window table is the one the symbolic phase built
     bool rrows_ready = false; // numeric phase: the dense rows' descriptions are the symbolic phase's
+    bool side_ok = true;      // the numeric phase may run the light tiers on this thread's side stream
     Control host;
     Stamp host_stamp;
 };
@@ -380,6 +381,34 @@ wingspan_status timer_begin(bool on) {
 }
 
 constexpr int kSlotAnalysis = WINGSPAN_NUM_TIERS;
+
+// A second stream per thread and device (default priority) with a fork and a
+// join event, so the numeric phase's light tiers can run beside the dense
+// kernel: they start where the dense kernel's workgroups leave CUs free.
+struct SideStream {
+    int dev = -1;
+    hipStream_t st = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+thread_local std::vector<SideStream> g_side;
+
+wingspan_status side_stream(SideStream **out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    for (SideStream &s : g_side)
+        if (s.dev == dev) {
+            *out = &s;
+            return WINGSPAN_OK;
+        }
+    SideStream s;
+    s.dev = dev;
+    HIP_TRY(hipStreamCreateWithFlags(&s.st, hipStreamNonBlocking));
+    HIP_TRY(hipEventCreateWithFlags(&s.fork, hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&s.join, hipEventDisableTiming));
+    g_side.push_back(s);
+    *out = &g_side.back();
+    return WINGSPAN_OK;
+}
 
 template <typename In>
 wingspan_status run_scan(Ctx &c, In in, int64_t n, int64_t *out) {
@@ -703,38 +732,62 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
     const Mats<float> M{A->row_ptr, A->col_idx, static_cast<const float *>(A->val),
                         B->row_ptr, B->col_idx, static_cast<const float *>(B->val)};
     const int32_t *perm = c.perm;
-
-    if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
-    for (int i = 0; i < kNumTiny; ++i) {
-        const int b = kBinTiny0 + i;
-        const int32_t cnt = c.host.bin_count[b];
-        if (!cnt) continue;
-        const int S = 8 << i;
-        launch_tiny<float, false>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b],
-                                  cnt, c.row_nnz, RowSink{}, nullptr, nullptr, c.ctrl);
-        stats.launches[WINGSPAN_TIER_TINY]++;
-    }
-    LAUNCH_CHECK("tiny symbolic");
-    if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
-
-    if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
-    for (int i = 0; i < kNumHash; ++i) {
-        const int b = kBinHash0 + i;
-        const int32_t cnt = c.host.bin_count[b];
-        if (!cnt) continue;
-        launch_hash<float, false>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M,
-                                  perm + c.host.bin_offset[b], B->ncols, c.row_nnz, RowSink{}, nullptr, nullptr,
-                                  c.ctrl);
-        stats.launches[WINGSPAN_TIER_HASH]++;
-    }
-    LAUNCH_CHECK("hash symbolic");
-    if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
-
     int32_t start, cnt;
-    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
     const bool caching = c.L.cache_rows > 0;
     const int64_t cnt_dense = cnt;
+    // B's window table for the numeric phase's dense rows (it depends on B only)
+    const bool wtab = caching && cnt_dense > 0 && c.L.nwin > 0;
+    int32_t light = 0;
+    for (int b = kBinTiny0; b < kBinTiny0 + kNumTiny; ++b) light += c.host.bin_count[b];
+    for (int b = kBinHash0; b < kBinHash0 + kNumHash; ++b) light += c.host.bin_count[b];
+    // untimed, the tiny and hash tiers (and the window table) run on a side stream beside the dense kernel,
+    // joined before the spill tier; timed, every tier runs in turn on the caller's stream
+    SideStream *side = nullptr;
+    if (!g_timer.on && c.side_ok && cnt && (light || wtab)) {
+        if ((s = side_stream(&side)) != WINGSPAN_OK) return s;
+        HIP_TRY(hipEventRecord(side->fork, c.st));
+    }
+    const hipStream_t light_st = side ? side->st : c.st;
+    auto light_tiers = [&]() -> wingspan_status {
+        if (side) HIP_TRY(hipStreamWaitEvent(side->st, side->fork, 0));
+        if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+        for (int i = 0; i < kNumTiny; ++i) {
+            const int b = kBinTiny0 + i;
+            const int32_t nb = c.host.bin_count[b];
+            if (!nb) continue;
+            const int S = 8 << i;
+            launch_tiny<float, false>(i, blocks_for(int64_t(nb) * S, 256), light_st, M, perm + c.host.bin_offset[b],
+                                      nb, c.row_nnz, RowSink{}, nullptr, nullptr, c.ctrl);
+            stats.launches[WINGSPAN_TIER_TINY]++;
+        }
+        LAUNCH_CHECK("tiny symbolic");
+        if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+
+        if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+        for (int i = 0; i < kNumHash; ++i) {
+            const int b = kBinHash0 + i;
+            const int32_t nb = c.host.bin_count[b];
+            if (!nb) continue;
+            launch_hash<float, false>(kHashLog2Min + i, static_cast<unsigned>(nb), light_st, M,
+                                      perm + c.host.bin_offset[b], B->ncols, c.row_nnz, RowSink{}, nullptr, nullptr,
+                                      c.ctrl);
+            stats.launches[WINGSPAN_TIER_HASH]++;
+        }
+        LAUNCH_CHECK("hash symbolic");
+        if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+        if (wtab) {
+            const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
+            build_window_table<<<blocks_for(entries, 256), 256, 0, light_st>>>(B->row_ptr, B->col_idx, B->nrows,
+                                                                               c.L.nwin, c.L.wcols, c.wtab);
+            LAUNCH_CHECK("build_window_table");
+        }
+        if (side) HIP_TRY(hipEventRecord(side->join, side->st));
+        return WINGSPAN_OK;
+    };
+    if (!side && (s = light_tiers()) != WINGSPAN_OK) return s;
+
+    if ((s = timer_start(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
     if (caching) {
         fill_i32<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(c.slot_of_row, A->nrows, -1);
         LAUNCH_CHECK("fill slots");
@@ -747,6 +800,10 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
         LAUNCH_CHECK("bitmap symbolic");
     }
     if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+    if (side) {
+        if ((s = light_tiers()) != WINGSPAN_OK) return s;
+        HIP_TRY(hipStreamWaitEvent(c.st, side->join, 0));
+    }
 
     if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
     s = launch_spill<float, false>(c, M, perm, B->ncols, c.row_nnz, RowSink{}, nullptr, nullptr,
@@ -769,15 +826,12 @@ wingspan_status symbolic_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr 
         bin_scatter<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, A->nrows, ncfg,
                                                                    c.ctrl_num, c.perm_num);
         LAUNCH_CHECK("numeric binning");
-        const bool wtab = cnt_dense > 0 && c.L.nwin > 0;
         if (wtab) {
-            const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
-            build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows,
-                                                                           c.L.nwin, c.L.wcols, c.wtab);
-            // and the descriptions of the numeric phase's dense rows (their cache slots are this phase's)
+            // (the window table was built beside the tiers) and the descriptions of the numeric phase's dense
+            // rows (their cache slots are this phase's)
             rank_rows_of_bins<<<blocks_for(A->nrows, 256), 256, 0, c.st>>>(c.perm_num, c.ctrl_num, A->row_ptr, c_rp,
                                                                            c.slot_of_row, c.rrows);
-            LAUNCH_CHECK("build_window_table");
+            LAUNCH_CHECK("rank rows of bins");
         }
         // the cache is complete: stamp it with the inputs, the layout, the bins' settings and C.row_ptr's
         // checksum
@@ -815,33 +869,52 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
     RowSink sink;
     sink.c_rp = c_rp;
 
-    if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
-    for (int i = 0; i < kNumTiny; ++i) {
-        const int b = kBinTiny0 + i;
-        const int32_t cnt = c.host.bin_count[b];
-        if (!cnt) continue;
-        const int S = 8 << i;
-        launch_tiny<V, true>(i, blocks_for(int64_t(cnt) * S, 256), c.st, M, perm + c.host.bin_offset[b], cnt,
-                             nullptr, sink, c_col, c_val, c.ctrl);
-        stats.launches[WINGSPAN_TIER_TINY]++;
-    }
-    LAUNCH_CHECK("tiny numeric");
-    if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
-
-    if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
-    for (int i = 0; i < kNumHash; ++i) {
-        const int b = kBinHash0 + i;
-        const int32_t cnt = c.host.bin_count[b];
-        if (!cnt) continue;
-        launch_hash<V, true>(kHashLog2Min + i, static_cast<unsigned>(cnt), c.st, M, perm + c.host.bin_offset[b],
-                             B->ncols, nullptr, sink, c_col, c_val, c.ctrl);
-        stats.launches[WINGSPAN_TIER_HASH]++;
-    }
-    LAUNCH_CHECK("hash numeric");
-    if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
-
     int32_t start, cnt;
     bin_range(c, kBinDense0, kNumClasses, &start, &cnt);
+    int32_t light = 0;
+    for (int b = kBinTiny0; b < kBinTiny0 + kNumTiny; ++b) light += c.host.bin_count[b];
+    for (int b = kBinHash0; b < kBinHash0 + kNumHash; ++b) light += c.host.bin_count[b];
+    // untimed, the tiny and hash tiers run on a side stream beside the dense kernel (forked after the analysis,
+    // joined before the spill tier); timed, every tier runs in turn on the caller's stream
+    SideStream *side = nullptr;
+    if (!g_timer.on && c.side_ok && cnt && light) {
+        if ((s = side_stream(&side)) != WINGSPAN_OK) return s;
+        HIP_TRY(hipEventRecord(side->fork, c.st));
+    }
+    const hipStream_t light_st = side ? side->st : c.st;
+    auto light_tiers = [&]() -> wingspan_status {
+        if (side) HIP_TRY(hipStreamWaitEvent(side->st, side->fork, 0));
+        if ((s = timer_start(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+        for (int i = 0; i < kNumTiny; ++i) {
+            const int b = kBinTiny0 + i;
+            const int32_t nb = c.host.bin_count[b];
+            if (!nb) continue;
+            const int S = 8 << i;
+            launch_tiny<V, true>(i, blocks_for(int64_t(nb) * S, 256), light_st, M, perm + c.host.bin_offset[b], nb,
+                                 nullptr, sink, c_col, c_val, c.ctrl);
+            stats.launches[WINGSPAN_TIER_TINY]++;
+        }
+        LAUNCH_CHECK("tiny numeric");
+        if ((s = timer_stop(c, WINGSPAN_TIER_TINY)) != WINGSPAN_OK) return s;
+
+        if ((s = timer_start(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+        for (int i = 0; i < kNumHash; ++i) {
+            const int b = kBinHash0 + i;
+            const int32_t nb = c.host.bin_count[b];
+            if (!nb) continue;
+            launch_hash<V, true>(kHashLog2Min + i, static_cast<unsigned>(nb), light_st, M, perm + c.host.bin_offset[b],
+                                 B->ncols, nullptr, sink, c_col, c_val, c.ctrl);
+            stats.launches[WINGSPAN_TIER_HASH]++;
+        }
+        LAUNCH_CHECK("hash numeric");
+        if ((s = timer_stop(c, WINGSPAN_TIER_HASH)) != WINGSPAN_OK) return s;
+        if (side) {
+            HIP_TRY(hipEventRecord(side->join, side->st));
+        }
+        return WINGSPAN_OK;
+    };
+    if (!side && (s = light_tiers()) != WINGSPAN_OK) return s;
+
     if (cnt && !c.wtab_ready) {
         const int64_t entries = B->nrows * static_cast<int64_t>(c.L.nwin + 1);
         build_window_table<<<blocks_for(entries, 256), 256, 0, c.st>>>(B->row_ptr, B->col_idx, B->nrows, c.L.nwin,
@@ -873,6 +946,10 @@ wingspan_status numeric_impl(Ctx &c, const wingspan_csr *A, const wingspan_csr *
         LAUNCH_CHECK("dense numeric");
     }
     if ((s = timer_stop(c, WINGSPAN_TIER_DENSE)) != WINGSPAN_OK) return s;
+    if (side) {
+        if ((s = light_tiers()) != WINGSPAN_OK) return s;
+        HIP_TRY(hipStreamWaitEvent(c.st, side->join, 0));
+    }
 
     if ((s = timer_start(c, WINGSPAN_TIER_SPILL)) != WINGSPAN_OK) return s;
     s = launch_spill<V, true>(c, M, perm, B->ncols, nullptr, sink, c_col, c_val,
@@ -1676,6 +1753,7 @@ wingspan_status wingspan_spgemm_noalloc(const wingspan_csr *A, const wingspan_cs
     void *scratch = nullptr;
     if ((s = static_scratch(&scratch)) != WINGSPAN_OK) return s;
     Ctx c{};
+    c.side_ok = false;   // a side stream and its events would be created on first use
     s = symbolic_entry(A, B, c_row_ptr_dev, c_nnz, scratch, cap, stream, options, c, cap);
     if (s != WINGSPAN_OK) return s;
     if (*c_nnz > c_capacity)
