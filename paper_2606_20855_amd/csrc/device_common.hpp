@@ -220,6 +220,7 @@ constexpr int kDppRowShr4 = 0x114;
 constexpr int kDppRowShr8 = 0x118;
 constexpr int kDppRowBcast15 = 0x142;
 constexpr int kDppRowBcast31 = 0x143;
+constexpr int kDppWaveShr1 = 0x138;   // whole-wave shift right by one lane
 
 __device__ __forceinline__ int wave_incl_sum(int v) {
     v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr1, 0xf, 0xf, false);

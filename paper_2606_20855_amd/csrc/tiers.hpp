@@ -1328,8 +1328,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                         }
                         // slot i0 + 1's word: the last mark up to it; slot i0's: the last mark up to i0 - 1, or its own
                         const int w1 = wave_incl_max(mk1 > mk0 ? mk1 : mk0);
-                        int w0 = __shfl_up(w1, 1, kWave);
-                        w0 = ln == 0 ? -1 : w0;
+                        // (a DPP shift of the whole wave by one lane: lane 0 keeps -1)
+                        int w0 = __builtin_amdgcn_update_dpp(-1, w1, kDppWaveShr1, 0xf, 0xf, false);
                         w0 = mk0 > w0 ? mk0 : w0;
                         if (i0 < n) {
                             const uint2 e0 = bw[w0];
