@@ -312,7 +312,7 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
         if (lb + SB <= lb1) {
             const int base = lb * kWave;
             const uint64_t before = ballot(start <= base);
-            const int o = before ? 63 - __clzll(before) : 0;
+            const int o = 63 - __clzll(before | 1ull);
             // the entry's products reach past the span's last one (so the span is also below tot)
             if (__builtin_amdgcn_readlane(incl, o) > base + SB * kWave - 1) {
                 const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(boff, o)) + base;
@@ -365,10 +365,10 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
                 aval[u] = 0.0;
                 if (lb + u >= lb1) continue;
                 const uint64_t bf = ballot(start <= base);
-                const int ob = bf ? 63 - __clzll(bf) : 0;
+                const int ob = 63 - __clzll(bf | 1ull);
                 const int last = (base + kWave < tot ? base + kWave : tot) - 1;
                 const uint64_t bl = ballot(start <= last);
-                const int oe = bl ? 63 - __clzll(bl) : 0;
+                const int oe = 63 - __clzll(bl | 1ull);
                 if (oe - ob < kScalarOwners) {
                     int bo = __builtin_amdgcn_readlane(boff, ob);
                     double a = VALUES ? readlane_d(av, ob) : 0.0;
@@ -406,7 +406,7 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
             for (int u = 0; u < U; ++u) {
                 const int base = (lb + u) * kWave;
                 const uint64_t before = ballot(start <= base);
-                ob[u] = before ? 63 - __clzll(before) : 0;
+                ob[u] = 63 - __clzll(before | 1ull);
                 const int last = (base + kWave < tot ? base + kWave : tot) - 1;
                 fast = fast && (lb + u >= lb1 || __builtin_amdgcn_readlane(incl, ob[u]) > last);
             }
@@ -499,7 +499,7 @@ __device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len,
     const int bfirst = nblk > 0 ? bstart : 0x7fffffff;
     for (int lb = lb0; lb < lb1;) {
         const uint64_t m0 = ballot(bfirst <= lb);
-        const int o = m0 ? 63 - __clzll(m0) : 0;
+        const int o = 63 - __clzll(m0 | 1ull);
         const int k = lb - __builtin_amdgcn_readlane(bstart, o);   // block of entry o
         if (lb + SB <= lb1 && (k + SB) * kWave <= __builtin_amdgcn_readlane(len, o)) {
             const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(bs, o)) + k * kWave;
@@ -544,7 +544,7 @@ __device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len,
             aval[u] = 0.0;
             if (b < lb1) {
                 const uint64_t m = ballot(bfirst <= b);
-                const int e = m ? 63 - __clzll(m) : 0;
+                const int e = 63 - __clzll(m | 1ull);
                 const int p = (b - __builtin_amdgcn_readlane(bstart, e)) * kWave + ln;
                 live[u] = p < __builtin_amdgcn_readlane(len, e);
                 ix[u] = __builtin_amdgcn_readlane(bs, e) + (live[u] ? p : 0);

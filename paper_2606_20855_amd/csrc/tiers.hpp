@@ -1174,6 +1174,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             // 2. exclusive popcount prefix (lane-contiguous rows, so free of bank conflicts); each word is
             //    stored with its prefix. A 64-word row holds at most 2048 columns, so two rows' counts share
             //    one scan as the 16-bit halves of a word; the wave's total comes from the same scans.
+            int region_total = 0;
             {
                 static_assert(WROWS % 2 == 0 && kWave * 32 < 65536, "rows scanned in pairs of 16-bit counts");
                 uint32_t cnt[WROWS];
@@ -1191,9 +1192,11 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 if (ln == 0) scratch[wv] = wtot;
                 if (threadIdx.x == 0 && rg0 == 0) s_next = claimed;
                 __syncthreads();
-                int run = 0;
-#pragma unroll
-                for (int i = 0; i < NW; ++i) run += i < wv ? scratch[i] : 0;
+                // one scan of the waves' totals gives this wave's first rank and the region's entry count
+                const int wt = ln < NW ? scratch[ln] : 0;
+                const int wincl = wave_incl_sum(wt);
+                region_total = __builtin_amdgcn_readlane(wincl, NW - 1);
+                int run = __builtin_amdgcn_readlane(wincl, wv) - __builtin_amdgcn_readlane(wt, wv);
 #pragma unroll
                 for (int h = 0; h < WROWS / 2; ++h) {
                     const uint32_t t = __builtin_amdgcn_readlane(inc2[h], kWave - 1);
@@ -1216,10 +1219,6 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                     n_hi = reinterpret_cast<const longlong2 *>(d)[1];
                 }
             }
-            int region_total = 0;
-#pragma unroll
-            for (int i = 0; i < NW; ++i) region_total += scratch[i];
-            region_total = uniform(region_total);
             if (POOL && !multi_region && threadIdx.x == 0) s_claim[0] = out.claim(row, region_total, &s_claim[1]);
             __syncthreads();
             if (POOL && !multi_region) {
@@ -1227,8 +1226,9 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 seg = uniform(s_claim[1]);
             }
             // 3. rank slices: whole windows while they fit CAP entries; a window denser than CAP is taken in
-            //    slices of CAP ranks. Lane jw holds the first rank of window jw (one LDS read for all windows),
-            //    and the greedy grouping reads them with scalar lane reads.
+            //    slices of CAP ranks. Lane jw holds the first rank of window jw (one LDS read for all windows).
+            //    Window start ranks do not decrease, so the windows starting within CAP ranks of a slice's
+            //    first rank are a prefix of the lanes: one ballot finds the slice's last window.
             const int nwr = rg1 - rg0;
             const int win_rank = ln <= nwr && ln * WIN_WORDS < nwords ? static_cast<int>(bw[ln * WIN_WORDS].y)
                                                                        : region_total;
@@ -1237,8 +1237,10 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
             int r0 = 0;              // first rank of the current slice
             int pj = 0, pj2 = nwr;   // windows of the slices the entry cache holds (first: the whole region)
             while (j < nwr) {
-                int j2 = j + 1;
-                while (j2 < nwr && rank_at_window(j2 + 1) - r0 <= CAP) ++j2;
+                const uint64_t fit = ballot(ln <= nwr && win_rank - r0 <= CAP);
+                const int last_fit = 63 - static_cast<int>(__builtin_clzll(fit | 1ull));
+                int j2 = last_fit < nwr ? last_fit : nwr;
+                j2 = j2 > j + 1 ? j2 : j + 1;
                 const int rend_w = rank_at_window(j2);
                 const int r1 = rend_w - r0 > CAP ? r0 + CAP : rend_w;   // this slice covers ranks [r0, r1)
                 // the row's last slice: the next row's loads go out while it is staged and copied
