@@ -232,14 +232,17 @@ __device__ __forceinline__ int wave_incl_sum(int v) {
     return v;
 }
 
-// Inclusive max-scan of values >= -1 (identity -1).
+// Inclusive max-scan. Lanes a DPP step does not feed read INT_MIN, the identity
+// of signed max, which lets the compiler fuse each step into one max with a DPP
+// operand.
+constexpr int kMaxIdentity = static_cast<int>(0x80000000u);
 __device__ __forceinline__ int wave_incl_max(int v) {
-    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr1, 0xf, 0xf, false));
-    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr2, 0xf, 0xf, false));
-    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr4, 0xf, 0xf, false));
-    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowShr8, 0xf, 0xf, false));
-    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowBcast15, 0xa, 0xf, false));
-    v = max(v, __builtin_amdgcn_update_dpp(-1, v, kDppRowBcast31, 0xc, 0xf, false));
+    v = max(__builtin_amdgcn_update_dpp(kMaxIdentity, v, kDppRowShr1, 0xf, 0xf, false), v);
+    v = max(__builtin_amdgcn_update_dpp(kMaxIdentity, v, kDppRowShr2, 0xf, 0xf, false), v);
+    v = max(__builtin_amdgcn_update_dpp(kMaxIdentity, v, kDppRowShr4, 0xf, 0xf, false), v);
+    v = max(__builtin_amdgcn_update_dpp(kMaxIdentity, v, kDppRowShr8, 0xf, 0xf, false), v);
+    v = max(__builtin_amdgcn_update_dpp(kMaxIdentity, v, kDppRowBcast15, 0xa, 0xf, false), v);
+    v = max(__builtin_amdgcn_update_dpp(kMaxIdentity, v, kDppRowBcast31, 0xc, 0xf, false), v);
     return v;
 }
 
@@ -308,43 +311,48 @@ __device__ __forceinline__ void chunk_blocks(int boff, double av, int len, int i
     // first product of the lane's entry, or INT_MAX for an entry without products: "an entry with products
     // starts at or before q" is then one compare
     const int start = len > 0 ? excl : 0x7fffffff;
+    // the span step from block lb: returns false (doing nothing) when blocks lb .. lb + SB - 1 are not all
+    // inside one entry's slice
+    auto span_step = [&](int lb) -> bool {
+        constexpr int NB = SB;
+        const int base = lb * kWave;
+        const uint64_t before = ballot(start <= base);
+        const int o = 63 - __clzll(before | 1ull);
+        // the entry's products reach past the span's last one (so the span is also below tot)
+        if (__builtin_amdgcn_readlane(incl, o) <= base + NB * kWave - 1) return false;
+        const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(boff, o)) + base;
+        const int32_t *cp = b_col + b0 + ln;
+        const V *vp = b_val + b0 + ln;
+        const double a = VALUES ? readlane_d(av, o) : 0.0;
+        int c[NB];
+        V v[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            c[u] = cp[u * kWave];
+            if (VALUES) v[u] = vp[u * kWave];
+        }
+        // keep the compiler from sinking a load into its use
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            asm volatile("" : "+v"(c[u]));
+            if (VALUES) asm volatile("" : "+v"(v[u]));
+        }
+        if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
+            int k[NB];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) k[u] = visit.pre(c[u]);
+#pragma unroll
+            for (int u = 0; u < NB; ++u) visit.post(k[u], VALUES ? a * to_d(v[u]) : 0.0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < NB; ++u) visit(c[u], VALUES ? a * to_d(v[u]) : 0.0);
+        }
+        return true;
+    };
     for (int lb = lb0; lb < lb1;) {
-        if (lb + SB <= lb1) {
-            const int base = lb * kWave;
-            const uint64_t before = ballot(start <= base);
-            const int o = 63 - __clzll(before | 1ull);
-            // the entry's products reach past the span's last one (so the span is also below tot)
-            if (__builtin_amdgcn_readlane(incl, o) > base + SB * kWave - 1) {
-                const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(boff, o)) + base;
-                const int32_t *cp = b_col + b0 + ln;
-                const V *vp = b_val + b0 + ln;
-                const double a = VALUES ? readlane_d(av, o) : 0.0;
-                int c[SB];
-                V v[SB];
-#pragma unroll
-                for (int u = 0; u < SB; ++u) {
-                    c[u] = cp[u * kWave];
-                    if (VALUES) v[u] = vp[u * kWave];
-                }
-                // keep the compiler from sinking a load into its use
-#pragma unroll
-                for (int u = 0; u < SB; ++u) {
-                    asm volatile("" : "+v"(c[u]));
-                    if (VALUES) asm volatile("" : "+v"(v[u]));
-                }
-                if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
-                    int k[SB];
-#pragma unroll
-                    for (int u = 0; u < SB; ++u) k[u] = visit.pre(c[u]);
-#pragma unroll
-                    for (int u = 0; u < SB; ++u) visit.post(k[u], VALUES ? a * to_d(v[u]) : 0.0);
-                } else {
-#pragma unroll
-                    for (int u = 0; u < SB; ++u) visit(c[u], VALUES ? a * to_d(v[u]) : 0.0);
-                }
-                lb += SB;
-                continue;
-            }
+        if (lb + SB <= lb1 && span_step(lb)) {
+            lb += SB;
+            continue;
         }
         // general step: U blocks
         int ix[U];

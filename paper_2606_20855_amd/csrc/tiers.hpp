@@ -1046,9 +1046,11 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
         fetch_words(a_lo, a_hi, slot);
         fetch_bounds(a_lo, a_hi);
     }
-    int claimed = 0;   // thread 0: the row after the next one
+    // thread 0: the row after the next one, claimed a row ahead of its use so that the claim's round trip
+    // overlaps a row's work
+    int claimed = 0;
+    if (threadIdx.x == 0) claimed = atomicAdd(&ctrl->rank_next, 1);
     while (true) {
-        if (threadIdx.x == 0) claimed = atomicAdd(&ctrl->rank_next, 1);
         // CSR output: the row's place from C.row_ptr. Pool output: claimed once the region's entry count is
         // known
         int64_t cb = row_cb, seg = row_seg;
@@ -1190,7 +1192,10 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                     wtot += static_cast<int>((t & 0xffffu) + (t >> 16));
                 }
                 if (ln == 0) scratch[wv] = wtot;
-                if (threadIdx.x == 0 && rg0 == 0) s_next = claimed;
+                if (threadIdx.x == 0 && rg0 == 0) {
+                    s_next = claimed;
+                    claimed = atomicAdd(&ctrl->rank_next, 1);
+                }
                 __syncthreads();
                 // one scan of the waves' totals gives this wave's first rank and the region's entry count
                 const int wt = ln < NW ? scratch[ln] : 0;
@@ -1330,9 +1335,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                         }
                         // slot i0 + 1's word: the last mark up to it; slot i0's: the last mark up to i0 - 1, or its own
                         const int w1 = wave_incl_max(mk1 > mk0 ? mk1 : mk0);
-                        // (a DPP shift of the whole wave by one lane: lane 0 keeps -1)
-                        int w0 = __builtin_amdgcn_update_dpp(-1, w1, kDppWaveShr1, 0xf, 0xf, false);
-                        w0 = mk0 > w0 ? mk0 : w0;
+                        // (a DPP shift of the whole wave by one lane: lane 0 reads the identity)
+                        const int w0 = max(__builtin_amdgcn_update_dpp(kMaxIdentity, w1, kDppWaveShr1, 0xf, 0xf, false), mk0);
                         if (i0 < n) {
                             const uint2 e0 = bw[w0];
                             const int p0 = select_set_bit(e0.x, r0 + i0 - static_cast<int>(e0.y));
