@@ -582,6 +582,8 @@ __global__ void __launch_bounds__(HashShape<LOG2T>::BLOCK) hash_kernel(Mats<V> M
 // Dense tier, symbolic: an LDS bitmap over all NWORDS*32 columns, one
 // workgroup per row. The row's entry count is the bitmap's population count.
 // ---------------------------------------------------------------------------
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 // Row i of the structure cache (when cache is not null) receives the bitmap
 // of the row handled by workgroup i < cache_rows, and slot_of_row[row] = i.
 template <int NWORDS, int BLOCK>
@@ -593,13 +595,16 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
                                                            uint32_t *__restrict__ cache, int64_t row_words,
                                                            int64_t cache_rows) {
     constexpr int NW = BLOCK / kWave;
-    __shared__ uint32_t bm[NWORDS];
+    __shared__ __align__(16) uint32_t bm[NWORDS];
     __shared__ int32_t scratch[NW];
     __shared__ int32_t marks[NW * kMarkIntsLong];
     __shared__ int32_t ctot[kCtotInts];
     __shared__ int32_t e_col[kCacheEntries], e_bs[kCacheEntries], e_len[kCacheEntries];
     const int row = rows[blockIdx.x];
-    for (int i = threadIdx.x; i < nwords_used; i += BLOCK) bm[i] = 0u;
+    static_assert(NWORDS % 4 == 0, "the bitmap is cleared, counted and copied in 16-byte pieces");
+    const int nq = (nwords_used + 3) >> 2;   // 16-byte pieces in use (the words past nwords_used stay zero)
+    uint4 *const bq = reinterpret_cast<uint4 *>(bm);
+    for (int i = threadIdx.x; i < nq; i += BLOCK) bq[i] = make_uint4(0u, 0u, 0u, 0u);
     const int wv = uniform(static_cast<int>(threadIdx.x) / kWave);
     int32_t *mark = marks + wv * kMarkIntsLong;
     init_marks(mark, kMarkIntsLong);
@@ -610,12 +615,16 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
         EntryCache{e_col, e_bs, e_len, nullptr, false});
     __syncthreads();
     int cnt = 0;
-    for (int i = threadIdx.x; i < nwords_used; i += BLOCK) cnt += __popc(bm[i]);
-    if (cache != nullptr && blockIdx.x < cache_rows) {
-        uint32_t *dst = cache + static_cast<int64_t>(blockIdx.x) * row_words;
-        for (int i = threadIdx.x; i < nwords_used; i += BLOCK) __builtin_nontemporal_store(bm[i], &dst[i]);
-        if (threadIdx.x == 0) slot_of_row[row] = static_cast<int32_t>(blockIdx.x);
+    const bool caching = cache != nullptr && blockIdx.x < cache_rows;
+    uint32_t *const dst = caching ? cache + static_cast<int64_t>(blockIdx.x) * row_words : nullptr;
+    for (int i = threadIdx.x; i < nq; i += BLOCK) {
+        const uint4 q = bq[i];
+        cnt += __popc(q.x) + __popc(q.y) + __popc(q.z) + __popc(q.w);
+        // (a cache row holds row_words >= 4 nq words, 16-byte aligned; the words past nwords_used are zero)
+        if (caching)
+            __builtin_nontemporal_store(u32x4{q.x, q.y, q.z, q.w}, reinterpret_cast<u32x4 *>(dst + 4 * i));
     }
+    if (caching && threadIdx.x == 0) slot_of_row[row] = static_cast<int32_t>(blockIdx.x);
     const int total = block_sum<BLOCK>(cnt, scratch);
     if (threadIdx.x == 0) row_nnz[row] = total;
 }
