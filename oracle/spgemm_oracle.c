@@ -1,13 +1,14 @@
 /*
- * Test infrastructure only -- the CPU oracle for C = A * B with A, B and C all
- * sparse, the sparse matrix product of Section 5.1 of the WingSpan paper.
+ * Test infrastructure only -- the CPU oracle for the sparse-times-sparse
+ * product C = A * B (both inputs and the result in compressed rows), the
+ * SpGEMM of Section 5.1 of the WingSpan paper.
  *
  * Nothing in the GPU library includes, links or calls this file. Only the
  * tests, the smoke check and the benchmark's CPU-baseline leg load it. It is
  * deliberately plain, single-threaded and slow.
  *
  * Algorithm: Gustavson's algorithm as written in the paper's SpGEMM program
- * figure (Section 5.1, "Gustavson's Algorithm"): for every output fiber,
+ * figure (Section 5.1, Gustavson's algorithm): for every output fiber,
  * clear a dense workspace w (a SparseByteMap: dense values plus a record of
  * which positions were touched), then for each k in the input fiber and each
  * entry of the matching fiber of the other operand do w[j] += a * b, then
