@@ -968,7 +968,7 @@ __device__ __forceinline__ int opaque_zero() {
 
 // Rank-indexed dense rows. The grid is persistent (one workgroup per CU, the
 // LDS allows no more): workgroups claim rows from a counter in the order of
-// `rr` (heaviest first), one row ahead, and while a row's last slice is staged
+// `rr` (heaviest first), two rows ahead, and while a row's last slice is staged
 // and copied they load the next row's description, its cached bitmap words and
 // its entry-cache entries, so a row starts without a round trip to memory.
 // When `cache` is not null, a row with slot >= 0 takes its column bitmap from
