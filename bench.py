@@ -46,6 +46,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "SpGEMM GFLOP/s (2×products/s) + effective HBM GB/s vs peak, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
+DEFAULT_CACHE_BYTES = 4096 << 20   # the library's structure-cache budget when options.cache_mib is 0
 KERNEL_SOURCES = ["paper_2606_20855_amd/csrc/tiers.hpp", "paper_2606_20855_amd/csrc/device_common.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "numeric_dense_rmat18_traffic.md")
 KERNEL_NAMES = {
@@ -393,21 +394,32 @@ def host_description() -> dict:
 def measure_spgemm(ws, torch, A, B, dev, steps, warmup, tier_steps=3):
     """One SpGEMM workload: `steps` timed steps (symbolic phase, then numeric
     phase into a preallocated C), HIP events around each phase on the
-    library's stream, options at their defaults (no per-tier timing inside the
-    calls); then `tier_steps` more steps with the library's per-tier HIP events
-    (options.timing) for the kernel breakdown and the dominant kernel's
-    roofline. Returns the measurements (and the device arrays' sizes)."""
+    library's stream, no per-tier timing inside the calls; then `tier_steps`
+    more steps with the library's per-tier HIP events (options.timing) for the
+    kernel breakdown and the dominant kernel's roofline. Options are the
+    defaults, except that a workload whose dense rows' column bitmaps exceed
+    the default structure-cache budget gets a budget (options.cache_mib) that
+    holds them all. Returns the measurements (and the device arrays)."""
     dA = ws.DeviceCSR.from_host(A, dev)
     dB = dA if B is A else ws.DeviceCSR.from_host(B, dev)
     Ad, Bd = dA.desc(), dB.desc()
     dt = dA.dtype_code
     s = 4 if dt == ws.F32 else 8
-    timing = ws.make_options(timing=1)
-    wsb, nbytes = ws.allocate_workspace(dA, dB)
     stream = torch.cuda.current_stream()
     h = stream.cuda_stream
     c_rp = torch.empty(A.nrows + 1, dtype=torch.int64, device=dev)
+    base, cache_mib = None, 0
+    wsb, nbytes = ws.allocate_workspace(dA, dB)
     nnz = ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, None)
+    need = ws.wingspan_last_stats(0)["rows"]["dense"] * (-(-B.ncols // 2048) * 256)
+    if need > DEFAULT_CACHE_BYTES:
+        cache_mib = -(-need // 2**20)
+        base = ws.make_options(cache_mib=cache_mib)
+        del wsb
+        torch.cuda.empty_cache()
+        wsb, nbytes = ws.allocate_workspace(dA, dB, base)
+        nnz = ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, base)
+    timing = ws.make_options(timing=1, cache_mib=cache_mib)
     c_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
     c_val = torch.empty(max(nnz, 1), dtype=dA.val.dtype, device=dev)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -421,12 +433,12 @@ def measure_spgemm(ws, torch, A, B, dev, steps, warmup, tier_steps=3):
         ev[2].record(stream)
 
     for _ in range(warmup):
-        step(None)
+        step(base)
     torch.cuda.synchronize()
     sym_ms, num_ms = [], []
     t_start = time.perf_counter()
     for _ in range(steps):
-        step(None)
+        step(base)
         ev[2].synchronize()
         sym_ms.append(ev[0].elapsed_time(ev[1]))
         num_ms.append(ev[1].elapsed_time(ev[2]))
@@ -470,7 +482,8 @@ def measure_spgemm(ws, torch, A, B, dev, steps, warmup, tier_steps=3):
         numeric_analysis_ms=round(float(np.mean(ana_ms)), 4),
         numeric_tier_rows={t: int(num["rows"][t]) for t in ws.TIERS},
         numeric_tier_products={t: int(num["products"][t]) for t in ws.TIERS},
-        workspace_MiB=round(nbytes / 2**20, 1),
+        workspace_MiB=round(nbytes / 2**20, 1), cache_mib=cache_mib,
+        structure_cache_rows=int(num["structure_cache_rows"]),
     )
     return out, (dA, dB)
 

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define WINGSPAN_ABI_VERSION 4
+#define WINGSPAN_ABI_VERSION 5
 
 typedef enum { WINGSPAN_F32 = 0, WINGSPAN_F64 = 1 } wingspan_dtype;
 
@@ -98,6 +98,13 @@ typedef struct {
     int32_t wide_offsets;   /* 1: the dense tier forms B's entry offsets in 64 bits even
                                where 32 bits hold them (the path B takes when nnz(B) times
                                the value size exceeds 2^32); a test switch, results equal */
+    int32_t cache_mib;      /* workspace budget of the structure cache, in MiB: the symbolic
+                               phase keeps the column bitmaps of up to that many bytes' worth
+                               of dense rows (ceil(B.ncols / 2048) * 256 bytes each) and the
+                               numeric phase of the same A and B reads them instead of
+                               gathering B's column indices again. 0 means 4096; -1 keeps
+                               none. It changes wingspan_spgemm_workspace_size, and both
+                               phases must be given the same value to share the cache. */
 } wingspan_options;
 
 /* Tiers a row can be assigned to. */
@@ -124,8 +131,9 @@ typedef struct {
     float analysis_ms;                   /* product counting, binning, scans */
     int64_t total_products;
     int64_t c_nnz_total;
-    int64_t structure_cache_rows;        /* numeric phase only: rows whose column sets were taken
-                                            from the symbolic phase's structure cache (0: not used) */
+    int64_t structure_cache_rows;        /* numeric phase only: dense rows whose column bitmaps the
+                                            symbolic phase kept in the structure cache, which this
+                                            phase's dense tier read (0: cache not used) */
 } wingspan_phase_stats;
 
 /* Bytes of device workspace the calls below need for this A, B and options.

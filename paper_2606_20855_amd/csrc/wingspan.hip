@@ -37,7 +37,8 @@ constexpr int kHashLog2MaxSym = 14;           // 16K int32 keys = 64 KB of LDS
 constexpr int kHashLog2MaxNum = 13;           // 8K keys + 8K doubles = 96 KB of LDS
 constexpr int64_t kBitmapMaxCols = 36864 * 32; // 144 KB LDS bitmap (plus per-wave marks)
 constexpr int kMaxWindows = 128;              // dense numeric tier: windows per row
-constexpr int64_t kStructCacheBytes = int64_t(4) << 30;   // dense-row bitmaps kept from symbolic to numeric
+constexpr int64_t kStructCacheBytes = int64_t(4) << 30;   // default budget of the dense-row bitmaps kept from
+                                                           // the symbolic to the numeric phase
 // With the structure cache, rows from this many entries (products, in the symbolic phase) up take the
 // bitmap / rank-indexed path even when they would fit an LDS hash table: the symbolic bitmap kernel is
 // cheaper than a large LDS hash, and the rank-indexed numeric kernel, which then skips its structure
@@ -98,6 +99,7 @@ struct Opts {
     int tiny_max = 64;
     int64_t dense_min_nnz = INT64_MAX;
     bool dense_min_explicit = false;   // dense_min_nnz given (otherwise chosen from the layout)
+    int64_t cache_bytes = kStructCacheBytes;   // structure cache budget
 };
 
 wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
@@ -141,6 +143,10 @@ wingspan_status parse_opts(const wingspan_options *o, Opts *out) {
             r.dense_min_nnz = o->dense_min_nnz;
             r.dense_min_explicit = true;
         }
+        if (o->cache_mib == -1) r.cache_bytes = 0;
+        else if (o->cache_mib < -1)
+            return fail(WINGSPAN_ERR_INVALID_ARGUMENT, "options->cache_mib must be >= -1, got %d", o->cache_mib);
+        else if (o->cache_mib > 0) r.cache_bytes = static_cast<int64_t>(o->cache_mib) << 20;
     }
     *out = r;
     return WINGSPAN_OK;
@@ -228,13 +234,13 @@ Layout plan(const wingspan_csr *A, const wingspan_csr *B, const Opts &o, size_t 
     }
     off += align_up(static_cast<size_t>(L.pool_bytes));
     // structure cache: the symbolic phase's column bitmaps of dense rows, reused by the rank-indexed numeric
-    // kernel; rows beyond kStructCacheBytes run their own structure pass
+    // kernel; rows beyond the budget (options.cache_mib) run their own structure pass
     L.cache_rows = 0;
     L.row_words = 0;
     if (budget == 0 && L.rank_mode && L.nwin > 0 && !o.dense_disabled && n > 0 && n <= kBitmapMaxCols && m > 0) {
         L.row_words = (n + 31) / 32;
         L.row_words = (L.row_words + 63) / 64 * 64;
-        L.cache_rows = std::min<int64_t>(m, kStructCacheBytes / (L.row_words * 4));
+        L.cache_rows = std::min<int64_t>(m, o.cache_bytes / (L.row_words * 4));
     }
     L.off_perm_num = off;
     if (L.cache_rows > 0) off += align_up(sizeof(int32_t) * m);

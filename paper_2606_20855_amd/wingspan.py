@@ -19,7 +19,7 @@ import numpy as np
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libwingspan.so")
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 F32, F64 = 0, 1
 OP_ADD, OP_HADAMARD = 0, 1
 TIERS = ("tiny", "hash", "dense", "spill")
@@ -68,6 +68,7 @@ class wingspan_options(ctypes.Structure):
         ("dense_min_nnz", ctypes.c_int32),
         ("timing", ctypes.c_int32),
         ("wide_offsets", ctypes.c_int32),
+        ("cache_mib", ctypes.c_int32),
     ]
 
 

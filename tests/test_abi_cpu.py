@@ -44,13 +44,13 @@ def test_library_exports_every_header_function():
 
 
 def test_abi_version():
-    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 4
+    assert ws.wingspan_abi_version() == ws.ABI_VERSION == 5
 
 
 def test_struct_layouts_match_header():
     # sizes the C side sees (x86-64 SysV)
     assert ctypes.sizeof(ws.wingspan_csr) == 48
-    assert ctypes.sizeof(ws.wingspan_options) == 36
+    assert ctypes.sizeof(ws.wingspan_options) == 40
     assert ctypes.sizeof(ws.wingspan_phase_stats) == 4 * 8 * 4 + 4 * 4 + 4 * 4 + 4 + 4 + 8 + 8 + 8
 
 
@@ -80,6 +80,25 @@ def test_workspace_structure_cache_is_bounded():
     without = ws.wingspan_spgemm_workspace_size(desc(n, n, 4_000_000), desc(n, n, 4_000_000), ws.F32,
                                                 ws.make_options(window_cols=8192))
     assert 0 < with_cache - without <= (4 << 30) + 2 * n * 4 + 1024
+
+
+def test_workspace_follows_the_cache_budget():
+    # options.cache_mib bounds the structure cache: one bitmap of ceil(ncols / 2048) * 256 bytes per row, at most
+    # one per row of A; -1 keeps no cache (nor its two per-row tables)
+    n = 262_144
+    A = B = desc(n, n, 4_000_000)
+    row = -(-n // 2048) * 256
+
+    def size(**kw):
+        return ws.wingspan_spgemm_workspace_size(A, B, ws.F32, ws.make_options(**kw) if kw else None)
+
+    default = size()
+    assert size(cache_mib=4096) == default
+    assert default - size(cache_mib=-1) == (4 << 30) // row * row + 2 * n * 4
+    # twice the budget caches every row (n rows of 32 KiB each: 8 GiB)
+    assert size(cache_mib=8192) - default == (n - (4 << 30) // row) * row
+    assert size(cache_mib=16384) == size(cache_mib=8192)
+    assert size(cache_mib=1) - size(cache_mib=-1) == (1 << 20) // row * row + 2 * n * 4
 
 
 @pytest.mark.parametrize("A,B,code", [
@@ -120,7 +139,7 @@ def test_bad_dtype():
 
 @pytest.mark.parametrize("opts", [
     dict(max_lds_slots=100), dict(max_lds_slots=32), dict(max_lds_slots=1 << 15),
-    dict(window_cols=2048), dict(tiny_max=7), dict(tiny_max=65), dict(dense_min_nnz=-2),
+    dict(window_cols=2048), dict(tiny_max=7), dict(tiny_max=65), dict(dense_min_nnz=-2), dict(cache_mib=-2),
 ])
 def test_bad_options(opts):
     got, msg = status_of(ws.wingspan_spgemm_workspace_size, desc(4, 4, 1), desc(4, 4, 1), ws.F32,

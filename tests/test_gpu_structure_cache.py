@@ -205,3 +205,19 @@ def test_single_pass_between_phases_invalidates_the_kept_state():
     got, num = _numeric(dA, dA, c_rp, nnz, wsb, nbytes, DENSE)
     assert num["structure_cache_rows"] == 0
     assert_matches(got, ref, A.val.dtype, what="numeric after a single pass")
+
+
+@pytest.mark.parametrize("cache_mib,cached", [(-1, 0), (1, 8), (0, 64)])
+def test_cache_budget_bounds_the_cached_rows(cache_mib, cached):
+    # B has 2^20 columns, so a row's bitmap takes 128 KiB: 1 MiB holds 8 of the 64 dense rows, the default
+    # budget all of them, -1 none; the rows past the budget run their own structure pass
+    A = matgen.er(64, 512, 16, seed=57, dtype=np.float32, dist="open01")
+    B = matgen.er(512, 1 << 20, 64, seed=58, dtype=np.float32, dist="open01")
+    opts = dict(DENSE, cache_mib=cache_mib)
+    dA, dB = _dev(A), _dev(B)
+    wsb, nbytes = _workspace(dA, dB, opts)
+    c_rp, nnz = _symbolic(dA, dB, wsb, nbytes, opts)
+    got, num = _numeric(dA, dB, c_rp, nnz, wsb, nbytes, opts)
+    assert num["rows"]["dense"] == 64
+    assert num["structure_cache_rows"] == cached
+    assert_matches(got, oracle.spgemm(A, B), A.val.dtype, what=f"cache budget {cache_mib} MiB")
