@@ -193,7 +193,7 @@ wingspan_status wingspan_spgemm(const wingspan_csr *A, const wingspan_csr *B, wi
  * from the library's first use on that device until the process ends. The
  * call allocates nothing (no hipMalloc, no library allocation). The scratch
  * holds no structure cache (the numeric phase computes its dense rows'
- * column sets itself) and a spill pool sized to what the other arrays leave.
+ * column sets itself; options->cache_mib is ignored) and a spill pool sized to what the other arrays leave.
  * A product whose scratch would exceed WINGSPAN_NOALLOC_SCRATCH_BYTES returns
  * WINGSPAN_ERR_WORKSPACE_TOO_SMALL before any HIP call; wingspan_spgemm with
  * a caller-owned workspace takes it. options->timing is refused

@@ -275,6 +275,36 @@ __device__ __forceinline__ double readlane_d(double x, int lane) {
 // any update, and dead lanes look up safe_col() (no branch around a lookup).
 struct TwoPhaseVisit {};
 
+constexpr int kDppRowShl1 = 0x101;
+
+// Marks columns in an LDS bitmap whose word j is bm[j * STRIDE], columns taken
+// relative to col0. Several lanes of one atomic instruction that hit the same
+// word are serialised by LDS, and the lanes of a block over a long B slice
+// hold increasing columns, so neighbours often share a word. Each odd lane
+// therefore first takes the bit of the even lane before it when both name the
+// same word, and only lanes whose word differs from the next lane's, or odd
+// lanes, issue the atomic: every bit reaches a lane that does, whatever the
+// order of the columns. Needs the whole wave active (the block steps of
+// for_each_product_wg are). A dead lane's post gets -1 and marks nothing.
+template <int STRIDE>
+struct BitmapMark : TwoPhaseVisit {
+    uint32_t *bm;
+    int col0;
+    __device__ __forceinline__ int pre(int col) const { return col - col0; }
+    __device__ __forceinline__ int safe_col() const { return col0; }
+    __device__ __forceinline__ void post(int rel, double) const {
+        const int w = rel >> 5;   // -1 for a dead lane
+        int bit = rel >= 0 ? static_cast<int>(1u << (rel & 31)) : 0;
+        const int wp = __builtin_amdgcn_update_dpp(kMaxIdentity, w, kDppRowShr1, 0xf, 0xf, false);
+        const int bp = __builtin_amdgcn_update_dpp(0, bit, kDppRowShr1, 0xf, 0xf, false);
+        bit |= wp == w ? bp : 0;
+        const int wn = __builtin_amdgcn_update_dpp(kMaxIdentity, w, kDppRowShl1, 0xf, 0xf, false);
+        if (rel >= 0 && (wn != w || (lane_id() & 1)))
+            atomicOr(&bm[w * STRIDE], static_cast<uint32_t>(bit));
+    }
+    __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
+};
+
 // Processes blocks [lb0, lb1) (block = 64 consecutive products) of one
 // 64-entry A chunk whose lanes hold (boff, av, len, incl): the shared body of
 // the product iterators. `mark` is this wave's LDS mark array (all -1).

@@ -611,7 +611,7 @@ __global__ void __launch_bounds__(BLOCK) bitmap_sym_kernel(Mats<float> M,
     __syncthreads();
     for_each_product_wg<BLOCK, float, false, true, true>(
         M.a_col, nullptr, M.a_rp[row], M.a_rp[row + 1], BRowRange{M.b_rp}, M.b_col, nullptr, mark, ctot,
-        [&](int col, double) { atomicOr(&bm[col >> 5], 1u << (col & 31)); },
+        BitmapMark<1>{{}, bm, 0},
         EntryCache{e_col, e_bs, e_len, nullptr, false});
     __syncthreads();
     int cnt = 0;
@@ -1098,10 +1098,7 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                     __syncthreads();
                     for_each_product_wg<BLOCK, V, false, true, true>(
                         M.a_col, M.a_val, a_lo, a_hi, BWindowRange{wtab, stride, rg0, rg1}, M.b_col, M.b_val, mark,
-                        ctot, [&](int col, double) {
-                            const int rel = static_cast<int>(col - col0);
-                            atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
-                        });
+                        ctot, BitmapMark<2>{{}, &bw[0].x, static_cast<int>(col0)});
                     int cnt = 0;
                     for (int i = threadIdx.x; i < nwords; i += BLOCK) cnt += __popc(bw[i].x);
                     total += block_sum<BLOCK>(cnt, scratch);
@@ -1164,10 +1161,8 @@ __global__ void __launch_bounds__(RankShape<V>::BLOCK) dense_rank_kernel(
                 __syncthreads();
                 for (int i = threadIdx.x; i < RW; i += BLOCK) bw[i].x = 0u;
                 __syncthreads();
-                auto mark_col = [&](int col, double) {
-                    const int rel = static_cast<int>(col - col0);
-                    atomicOr(&bw[rel >> 5].x, 1u << (rel & 31));
-                };
+                // (the .x words of bw, two words apart)
+                const BitmapMark<2> mark_col{{}, &bw[0].x, static_cast<int>(col0)};
                 if (nwin <= SH::REGION_WINS)
                     for_each_product_wg<BLOCK, V, false, true, true>(M.a_col, M.a_val, a_lo, a_hi,
                                                                      BRowRange{M.b_rp}, M.b_col, M.b_val, mark,
