@@ -275,17 +275,20 @@ __device__ __forceinline__ double readlane_d(double x, int lane) {
 // any update, and dead lanes look up safe_col() (no branch around a lookup).
 struct TwoPhaseVisit {};
 
-constexpr int kDppRowShl1 = 0x101;
+// quad permutations: every lane of a pair (2i, 2i + 1) reads lane 2i, or lane 2i + 1
+constexpr int kDppPairEven = 0xA0;   // quad_perm [0, 0, 2, 2]
+constexpr int kDppPairOdd = 0xF5;    // quad_perm [1, 1, 3, 3]
 
 // Marks columns in an LDS bitmap whose word j is bm[j * STRIDE], columns taken
 // relative to col0. Several lanes of one atomic instruction that hit the same
 // word are serialised by LDS, and the lanes of a block over a long B slice
-// hold increasing columns, so neighbours often share a word. Each odd lane
-// therefore first takes the bit of the even lane before it when both name the
-// same word, and only lanes whose word differs from the next lane's, or odd
-// lanes, issue the atomic: every bit reaches a lane that does, whatever the
-// order of the columns. Needs the whole wave active (the block steps of
-// for_each_product_wg are). A dead lane's post gets -1 and marks nothing.
+// hold increasing columns, so neighbours often share a word. Lanes therefore
+// work in pairs (2i, 2i + 1): the odd lane also sets the even lane's bit when
+// both name the same word, and the even lane issues its atomic only when they
+// do not. Every bit is set whatever the order of the columns. The pair
+// exchange is a quad permutation, so the whole wave must be active (the block
+// steps of for_each_product_wg are). A dead lane's post gets -1 and marks
+// nothing; its word (-1) matches no live lane's.
 template <int STRIDE>
 struct BitmapMark : TwoPhaseVisit {
     uint32_t *bm;
@@ -294,13 +297,12 @@ struct BitmapMark : TwoPhaseVisit {
     __device__ __forceinline__ int safe_col() const { return col0; }
     __device__ __forceinline__ void post(int rel, double) const {
         const int w = rel >> 5;   // -1 for a dead lane
-        int bit = rel >= 0 ? static_cast<int>(1u << (rel & 31)) : 0;
-        const int wp = __builtin_amdgcn_update_dpp(kMaxIdentity, w, kDppRowShr1, 0xf, 0xf, false);
-        const int bp = __builtin_amdgcn_update_dpp(0, bit, kDppRowShr1, 0xf, 0xf, false);
-        bit |= wp == w ? bp : 0;
-        const int wn = __builtin_amdgcn_update_dpp(kMaxIdentity, w, kDppRowShl1, 0xf, 0xf, false);
-        if (rel >= 0 && (wn != w || (lane_id() & 1)))
-            atomicOr(&bm[w * STRIDE], static_cast<uint32_t>(bit));
+        const int bit = static_cast<int>(1u << (rel & 31));
+        const int w_even = __builtin_amdgcn_mov_dpp(w, kDppPairEven, 0xf, 0xf, false);
+        const int bit_even = __builtin_amdgcn_mov_dpp(bit, kDppPairEven, 0xf, 0xf, false);
+        const int w_odd = __builtin_amdgcn_mov_dpp(w, kDppPairOdd, 0xf, 0xf, false);
+        if (rel >= 0 && ((lane_id() & 1) || w_odd != w))
+            atomicOr(&bm[w * STRIDE], static_cast<uint32_t>(w_even == w ? (bit | bit_even) : bit));
     }
     __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
 };
