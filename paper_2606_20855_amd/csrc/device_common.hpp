@@ -305,7 +305,28 @@ struct BitmapMark : TwoPhaseVisit {
             atomicOr(&bm[w * STRIDE], static_cast<uint32_t>(w_even == w ? (bit | bit_even) : bit));
     }
     __device__ __forceinline__ void operator()(int col, double prod) const { post(pre(col), prod); }
+    // Four consecutive columns of one B slice, in one lane (a span step of entry-aligned blocks, see
+    // chunk_blocks_aligned): each run of columns in one word ORs its bits into the run's last column, which
+    // alone issues the atomic. As above, any column order gives the same bitmap.
+    __device__ __forceinline__ void run4(int c0, int c1, int c2, int c3) const {
+        const int r0 = c0 - col0, r1 = c1 - col0, r2 = c2 - col0, r3 = c3 - col0;
+        const int w0 = r0 >> 5, w1 = r1 >> 5, w2 = r2 >> 5, w3 = r3 >> 5;
+        const uint32_t b0 = 1u << (r0 & 31), b1 = 1u << (r1 & 31), b2 = 1u << (r2 & 31), b3 = 1u << (r3 & 31);
+        const bool s01 = w0 == w1, s12 = w1 == w2, s23 = w2 == w3;
+        const uint32_t p1 = b1 | (s01 ? b0 : 0u);
+        const uint32_t p2 = b2 | (s12 ? p1 : 0u);
+        const uint32_t p3 = b3 | (s23 ? p2 : 0u);
+        if (!s01) atomicOr(&bm[w0 * STRIDE], b0);
+        if (!s12) atomicOr(&bm[w1 * STRIDE], p1);
+        if (!s23) atomicOr(&bm[w2 * STRIDE], p2);
+        atomicOr(&bm[w3 * STRIDE], p3);
+    }
 };
+// Whether a visitor takes four consecutive columns of one lane at once (run4).
+template <typename T, typename = void>
+struct has_run4 : std::false_type {};
+template <typename T>
+struct has_run4<T, std::void_t<decltype(std::declval<const T &>().run4(0, 0, 0, 0))>> : std::true_type {};
 
 // Processes blocks [lb0, lb1) (block = 64 consecutive products) of one
 // 64-entry A chunk whose lanes hold (boff, av, len, incl): the shared body of
@@ -543,6 +564,16 @@ __device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len,
         const int k = lb - __builtin_amdgcn_readlane(bstart, o);   // block of entry o
         if (lb + SB <= lb1 && (k + SB) * kWave <= __builtin_amdgcn_readlane(len, o)) {
             const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(bs, o)) + k * kWave;
+            if constexpr (!VALUES && has_run4<Visit>::value) {
+                // structure only: lane l takes products 4l .. 4l + 3 of the span with one 16-byte load (4-byte
+                // aligned), so a lane's columns sharing a word are merged in registers before any LDS atomic
+                static_assert(SB == 4, "four consecutive columns per lane");
+                typedef int32_t i32x4u __attribute__((ext_vector_type(4), aligned(4)));
+                const i32x4u q = *reinterpret_cast<const i32x4u *>(b_col + b0 + 4 * ln);
+                visit.run4(q.x, q.y, q.z, q.w);
+                lb += SB;
+                continue;
+            }
             const int32_t *cp = b_col + b0 + ln;
             const V *vp = b_val + b0 + ln;
             const double a = VALUES ? readlane_d(av, o) : 0.0;
