@@ -562,45 +562,52 @@ __device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len,
         const uint64_t m0 = ballot(bfirst <= lb);
         const int o = 63 - __clzll(m0 | 1ull);
         const int k = lb - __builtin_amdgcn_readlane(bstart, o);   // block of entry o
-        if (lb + SB <= lb1 && (k + SB) * kWave <= __builtin_amdgcn_readlane(len, o)) {
-            const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(bs, o)) + k * kWave;
-            if constexpr (!VALUES && has_run4<Visit>::value) {
-                // structure only: lane l takes products 4l .. 4l + 3 of the span with one 16-byte load (4-byte
-                // aligned), so a lane's columns sharing a word are merged in registers before any LDS atomic
-                static_assert(SB == 4, "four consecutive columns per lane");
-                typedef int32_t i32x4u __attribute__((ext_vector_type(4), aligned(4)));
-                const i32x4u q = *reinterpret_cast<const i32x4u *>(b_col + b0 + 4 * ln);
-                visit.run4(q.x, q.y, q.z, q.w);
-                lb += SB;
-                continue;
-            }
-            const int32_t *cp = b_col + b0 + ln;
-            const V *vp = b_val + b0 + ln;
+        const int len_o = __builtin_amdgcn_readlane(len, o);
+        if (lb + SB <= lb1 && (k + SB) * kWave <= len_o) {
+            // every span step of entry o inside [lb, lb1), its data read from the lanes once
+            int nsp = (len_o / kWave - k) / SB;
+            const int nmax = (lb1 - lb) / SB;
+            nsp = nsp < nmax ? nsp : nmax;
+            const int64_t bo = static_cast<int64_t>(__builtin_amdgcn_readlane(bs, o)) + k * kWave;
             const double a = VALUES ? readlane_d(av, o) : 0.0;
-            int c[SB];
-            V v[SB];
+            for (int t = 0; t < nsp; ++t) {
+                const int64_t b0 = bo + t * (SB * kWave);
+                if constexpr (!VALUES && has_run4<Visit>::value) {
+                    // structure only: lane l takes products 4l .. 4l + 3 of the span with one 16-byte load (4-byte
+                    // aligned), so a lane's columns sharing a word are merged in registers before any LDS atomic
+                    static_assert(SB == 4, "four consecutive columns per lane");
+                    typedef int32_t i32x4u __attribute__((ext_vector_type(4), aligned(4)));
+                    const i32x4u q = *reinterpret_cast<const i32x4u *>(b_col + b0 + 4 * ln);
+                    visit.run4(q.x, q.y, q.z, q.w);
+                    continue;
+                }
+                const int32_t *cp = b_col + b0 + ln;
+                const V *vp = b_val + b0 + ln;
+                int c[SB];
+                V v[SB];
 #pragma unroll
-            for (int u = 0; u < SB; ++u) {
-                c[u] = cp[u * kWave];
-                if (VALUES) v[u] = vp[u * kWave];
+                for (int u = 0; u < SB; ++u) {
+                    c[u] = cp[u * kWave];
+                    if (VALUES) v[u] = vp[u * kWave];
+                }
+                // keep the compiler from sinking a load into its use
+#pragma unroll
+                for (int u = 0; u < SB; ++u) {
+                    asm volatile("" : "+v"(c[u]));
+                    if (VALUES) asm volatile("" : "+v"(v[u]));
+                }
+                if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
+                    int kk[SB];
+#pragma unroll
+                    for (int u = 0; u < SB; ++u) kk[u] = visit.pre(c[u]);
+#pragma unroll
+                    for (int u = 0; u < SB; ++u) visit.post(kk[u], VALUES ? a * to_d(v[u]) : 0.0);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < SB; ++u) visit(c[u], VALUES ? a * to_d(v[u]) : 0.0);
+                }
             }
-            // keep the compiler from sinking a load into its use
-#pragma unroll
-            for (int u = 0; u < SB; ++u) {
-                asm volatile("" : "+v"(c[u]));
-                if (VALUES) asm volatile("" : "+v"(v[u]));
-            }
-            if constexpr (std::is_base_of<TwoPhaseVisit, Visit>::value) {
-                int kk[SB];
-#pragma unroll
-                for (int u = 0; u < SB; ++u) kk[u] = visit.pre(c[u]);
-#pragma unroll
-                for (int u = 0; u < SB; ++u) visit.post(kk[u], VALUES ? a * to_d(v[u]) : 0.0);
-            } else {
-#pragma unroll
-                for (int u = 0; u < SB; ++u) visit(c[u], VALUES ? a * to_d(v[u]) : 0.0);
-            }
-            lb += SB;
+            lb += nsp * SB;
             continue;
         }
         // SB blocks, each inside one entry
