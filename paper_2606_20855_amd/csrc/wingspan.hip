@@ -44,6 +44,11 @@ constexpr int64_t kStructCacheBytes = int64_t(4) << 30;   // default budget of t
 // cheaper than a large LDS hash, and the rank-indexed numeric kernel, which then skips its structure
 // pass, cheaper than a numeric hash table of 2^12 slots or more.
 constexpr int64_t kCachedDenseMin = 2048;
+// The single pass (no cache) sends rows from this many products up to the rank kernel when B's columns fit
+// one of its regions: its structure pass is then one bitmap pass, cheaper than an LDS hash table sized by
+// the row's products. Where B is wider a row is counted region by region first, and the LDS hash stays the
+// cheaper tier wherever it fits.
+constexpr int64_t kShardedDenseMin = 2048;
 constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
 constexpr int64_t kPoolBytes = int64_t(1) << 30;   // spill pool: at most this, unless one table needs more
 constexpr int64_t kMaxSlabCap = int64_t(1) << 27;
@@ -543,8 +548,9 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
         // the rank kernel writes a pool row once its count is known (a row of several regions counts them
         // first)
         cfg.dense_ok = c.L.rank_mode && c.L.nwin > 0;
-        // without a structure cache the LDS hash is the cheaper tier wherever it fits
-        cfg.dense_min_nnz = c.o.dense_min_explicit ? c.o.dense_min_nnz : INT64_MAX;
+        cfg.dense_min_nnz = c.o.dense_min_explicit
+                                ? c.o.dense_min_nnz
+                                : (B->ncols <= RankShape<float>::REGION_COLS ? kShardedDenseMin : INT64_MAX);
     }
     if (m > 0) {
         bin_count<<<blocks_for(m, 256), 256, 0, c.st>>>(A->row_ptr, c.pref, c_rp, m, cfg, c.ctrl,
