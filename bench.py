@@ -424,27 +424,28 @@ def measure_spgemm(ws, torch, A, B, dev, steps, warmup, tier_steps=3):
     c_val = torch.empty(max(nnz, 1), dtype=dA.val.dtype, device=dev)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
-    def step(opts):
-        ev[0].record(stream)
+    def step(opts, e=ev):
+        e[0].record(stream)
         ws.wingspan_spgemm_symbolic(Ad, Bd, c_rp.data_ptr(), wsb.data_ptr(), nbytes, h, opts)
-        ev[1].record(stream)
+        e[1].record(stream)
         ws.wingspan_spgemm_numeric(Ad, Bd, dt, c_rp.data_ptr(), c_col.data_ptr(), c_val.data_ptr(),
                                    wsb.data_ptr(), nbytes, h, opts)
-        ev[2].record(stream)
+        e[2].record(stream)
 
     for _ in range(warmup):
         step(base)
     torch.cuda.synchronize()
-    sym_ms, num_ms = [], []
+    # the timed steps follow each other without a host wait in between (the calls' own read-backs aside);
+    # each step's phase events are read after the last one
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     t_start = time.perf_counter()
-    for _ in range(steps):
-        step(base)
-        ev[2].synchronize()
-        sym_ms.append(ev[0].elapsed_time(ev[1]))
-        num_ms.append(ev[1].elapsed_time(ev[2]))
+    for e in evs:
+        step(base, e)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed / steps * 1e3
+    sym_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    num_ms = [e[1].elapsed_time(e[2]) for e in evs]
     # per-tier kernel times (the library's events on its stream)
     tier_ms, ana_ms = {t: [] for t in ws.TIERS}, []
     for _ in range(tier_steps):
