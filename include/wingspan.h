@@ -91,9 +91,10 @@ typedef struct {
     int32_t dense_min_nnz;  /* rows with at least this many output entries (numeric) or
                                products (symbolic, single pass) use the dense tier even if
                                they fit an LDS hash table; -1 disables the dense tier; 0
-                               means 2048 when the structure cache applies and in a single
-                               pass whose B has at most 262144 columns, else only rows too
-                               large for the LDS hash tables */
+                               means 2048 when the structure cache applies (1024 in its
+                               symbolic phase if B has at most 262144 columns) and in a
+                               single pass whose B has at most 262144 columns, else only
+                               rows too large for the LDS hash tables */
     int32_t timing;         /* 1: time each tier's kernels with HIP events on `stream`
                                (the call then synchronizes the stream before returning) */
     int32_t wide_offsets;   /* 1: the dense tier forms B's entry offsets in 64 bits even

@@ -49,6 +49,10 @@ constexpr int64_t kCachedDenseMin = 2048;
 // the row's products. Where B is wider a row is counted region by region first, and the LDS hash stays the
 // cheaper tier wherever it fits.
 constexpr int64_t kShardedDenseMin = 2048;
+// With the structure cache and B's columns in one rank region, the symbolic phase already sends rows from
+// this many products up to the bitmap kernel: below kCachedDenseMin they go back to the LDS hash in the
+// numeric phase, but counting them in a bitmap costs less than in a hash table of 2^11 slots or more.
+constexpr int64_t kSymbolicDenseMin = 1024;
 constexpr int kDefaultWindow = 16384;         // 16K doubles = 128 KB of LDS
 constexpr int64_t kPoolBytes = int64_t(1) << 30;   // spill pool: at most this, unless one table needs more
 constexpr int64_t kMaxSlabCap = int64_t(1) << 27;
@@ -544,6 +548,8 @@ wingspan_status analyze(Ctx &c, const wingspan_csr *A, const wingspan_csr *B, An
         cfg = numeric_bin_cfg(c, B);
     } else if (mode == kModeSymbolic) {
         cfg.dense_ok = !c.o.dense_disabled && B->ncols <= kBitmapMaxCols;
+        if (!c.o.dense_min_explicit && c.L.cache_rows > 0 && B->ncols <= RankShape<float>::REGION_COLS)
+            cfg.dense_min_nnz = kSymbolicDenseMin;
     } else {
         // the rank kernel writes a pool row once its count is known (a row of several regions counts them
         // first)
