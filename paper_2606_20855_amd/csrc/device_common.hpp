@@ -570,17 +570,37 @@ __device__ __forceinline__ void chunk_blocks_aligned(int bs, double av, int len,
             nsp = nsp < nmax ? nsp : nmax;
             const int64_t bo = static_cast<int64_t>(__builtin_amdgcn_readlane(bs, o)) + k * kWave;
             const double a = VALUES ? readlane_d(av, o) : 0.0;
+            if constexpr (!VALUES && has_run4<Visit>::value) {
+                // structure only: lane l takes products 4l .. 4l + 3 of each span with one 16-byte load (4-byte
+                // aligned), so a lane's columns sharing a word are merged in registers before any LDS atomic;
+                // four spans' loads go out before the first is visited
+                static_assert(SB == 4, "four consecutive columns per lane");
+                typedef int32_t i32x4u __attribute__((ext_vector_type(4), aligned(4)));
+                const int32_t *qp = b_col + bo + 4 * ln;
+                int t = 0;
+                for (; t + 3 < nsp; t += 4) {
+                    i32x4u q0 = *reinterpret_cast<const i32x4u *>(qp + t * (SB * kWave));
+                    i32x4u q1 = *reinterpret_cast<const i32x4u *>(qp + (t + 1) * (SB * kWave));
+                    i32x4u q2 = *reinterpret_cast<const i32x4u *>(qp + (t + 2) * (SB * kWave));
+                    i32x4u q3 = *reinterpret_cast<const i32x4u *>(qp + (t + 3) * (SB * kWave));
+                    asm volatile("" : "+v"(q0));
+                    asm volatile("" : "+v"(q1));
+                    asm volatile("" : "+v"(q2));
+                    asm volatile("" : "+v"(q3));
+                    visit.run4(q0.x, q0.y, q0.z, q0.w);
+                    visit.run4(q1.x, q1.y, q1.z, q1.w);
+                    visit.run4(q2.x, q2.y, q2.z, q2.w);
+                    visit.run4(q3.x, q3.y, q3.z, q3.w);
+                }
+                for (; t < nsp; ++t) {
+                    const i32x4u q = *reinterpret_cast<const i32x4u *>(qp + t * (SB * kWave));
+                    visit.run4(q.x, q.y, q.z, q.w);
+                }
+                lb += nsp * SB;
+                continue;
+            }
             for (int t = 0; t < nsp; ++t) {
                 const int64_t b0 = bo + t * (SB * kWave);
-                if constexpr (!VALUES && has_run4<Visit>::value) {
-                    // structure only: lane l takes products 4l .. 4l + 3 of the span with one 16-byte load (4-byte
-                    // aligned), so a lane's columns sharing a word are merged in registers before any LDS atomic
-                    static_assert(SB == 4, "four consecutive columns per lane");
-                    typedef int32_t i32x4u __attribute__((ext_vector_type(4), aligned(4)));
-                    const i32x4u q = *reinterpret_cast<const i32x4u *>(b_col + b0 + 4 * ln);
-                    visit.run4(q.x, q.y, q.z, q.w);
-                    continue;
-                }
                 const int32_t *cp = b_col + b0 + ln;
                 const V *vp = b_val + b0 + ln;
                 int c[SB];
